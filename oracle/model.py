@@ -1,0 +1,345 @@
+"""Plain float64 statement of the hierarchical byte LM with multi-byte prediction.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()`` and
+``bench.py``'s ``cpu_baseline`` leg, never by the library.  Every function is the
+definition written out, with no caching, blocking or fusion, so it can be checked
+against the paper by eye.  Each docstring names the passage it follows.
+
+Paper: "Dynamic Multi-Byte Prediction With Hierarchical Language Models".
+Readings taken where the paper is silent or ambiguous (each is listed, with its
+reason, in the design notes of this repository):
+
+* n counts all candidate distributions of a step: 1 next-byte + (n-1) MB rows.
+* The boundary byte opens the new group: byte i uses latent L(i) = #{boundaries <= i}.
+* r2 is the LM-module input row: the MB input of group j is z_j = h'[j] + LMin[j].
+* Window mode 0 (default): the MB layers run on the window only (previous group,
+  current group, n-2 virtual rows); mode 1 runs them on the whole sequence.
+* A segment also closes when it reaches ``max_patch`` bytes (0 = pure space rule).
+* Attention score = q.k / sqrt(d_head) * attn_scale; RoPE rotates adjacent pairs.
+* argmax ties resolve to the lowest byte value; acceptance compares P >= tau.
+* Self-verify: c_1 is the next-byte greedy byte; c_m (m >= 2) is kept while it equals
+  the greedy byte after x ++ c_1..c_{m-1}.  The correction byte at the first mismatch
+  is the next step's c_1, so the emitted sequence is the greedy one.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+SPACE = 0x20
+
+
+# ---------------------------------------------------------------- primitives --
+
+def rms_norm(x, g, eps):
+    """RMSNorm (Llama 3 blocks, model-architecture paragraph of the experimental
+    setup; eps = 1e-6): x / sqrt(mean(x^2) + eps) * g over the last axis."""
+    x = np.asarray(x, np.float64)
+    ms = np.mean(x * x, axis=-1, keepdims=True)
+    return x / np.sqrt(ms + eps) * np.asarray(g, np.float64)
+
+
+def rope(x, pos, base):
+    """Rotary embedding (base 1e5, model-architecture paragraph).
+
+    ``x``: [T, H, dh].  Pair (2i, 2i+1) of the row at position p is rotated by the
+    angle p * base^(-2i/dh).
+    """
+    x = np.asarray(x, np.float64)
+    dh = x.shape[-1]
+    inv = base ** (-np.arange(0, dh, 2, dtype=np.float64) / dh)
+    ang = np.asarray(pos, np.float64)[:, None] * inv[None, :]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    x0 = x[..., 0::2]
+    x1 = x[..., 1::2]
+    out = np.empty_like(x)
+    out[..., 0::2] = x0 * c - x1 * s
+    out[..., 1::2] = x0 * s + x1 * c
+    return out
+
+
+def causal_mask(T):
+    """Standard causal mask (encoder, LM module, NT decoder): i attends j iff j <= i."""
+    return np.tril(np.ones((T, T), dtype=bool))
+
+
+def lca_mask(G):
+    """Latent Causal Attention mask (Figure 2 caption; Section 3).
+
+    ``G[i]`` is the group (latent token) of row i.  Row i may attend to itself, to
+    earlier rows of its own group, and to every row of the immediately preceding
+    group; later rows and older groups are masked out.
+    """
+    G = np.asarray(G)
+    T = len(G)
+    m = np.zeros((T, T), dtype=bool)
+    for i in range(T):
+        for j in range(T):
+            own_group_so_far = G[j] == G[i] and j <= i
+            previous_group = G[j] == G[i] - 1
+            m[i, j] = own_group_so_far or previous_group
+    return m
+
+
+def attention(x, P, mask, pos, n_heads, rope_base, attn_scale):
+    """Multi-head self-attention with RoPE on q and k (8 KV heads = query heads in the
+    paper; here as many KV heads as query heads), score scaled by attn_scale/sqrt(dh),
+    masked positions excluded from the softmax."""
+    x = np.asarray(x, np.float64)
+    T, d = x.shape
+    dh = d // n_heads
+    q = (x @ P["wq"].T).reshape(T, n_heads, dh)
+    k = (x @ P["wk"].T).reshape(T, n_heads, dh)
+    v = (x @ P["wv"].T).reshape(T, n_heads, dh)
+    q = rope(q, pos, rope_base)
+    k = rope(k, pos, rope_base)
+    scores = np.einsum("ihd,jhd->hij", q, k) * (attn_scale / np.sqrt(dh))
+    scores = np.where(mask[None, :, :], scores, -np.inf)
+    scores = scores - scores.max(axis=-1, keepdims=True)
+    p = np.exp(scores)
+    p = p / p.sum(axis=-1, keepdims=True)
+    o = np.einsum("hij,jhd->ihd", p, v).reshape(T, d)
+    return o @ P["wo"].T
+
+
+def silu(x):
+    return x / (1.0 + np.exp(-x))
+
+
+def ffn(x, P):
+    """SwiGLU feed-forward, d_inner = 4 d (Llama 3 style): W_d (SiLU(W_g x) * W_u x)."""
+    return (silu(x @ P["w_gate"].T) * (x @ P["w_up"].T)) @ P["w_down"].T
+
+
+def block(u, P, mask, pos, cfg):
+    """Pre-norm Llama block: a = u + Attn(RMSNorm(u)); out = a + FFN(RMSNorm(a))."""
+    a = u + attention(rms_norm(u, P["attn_norm"], cfg.rms_eps), P, mask, pos,
+                      cfg.n_heads, cfg.rope_base, cfg.attn_scale)
+    return a + ffn(rms_norm(a, P["ffn_norm"], cfg.rms_eps), P)
+
+
+def _params(W, prefix):
+    parts = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
+    return {p: np.asarray(W[f"{prefix}.{p}"], np.float64) for p in parts}
+
+
+def stack(u, W, name, n_layers, mask, pos, cfg):
+    h = np.asarray(u, np.float64)
+    for i in range(n_layers):
+        h = block(h, _params(W, f"{name}.{i}"), mask, pos, cfg)
+    return h
+
+
+# ------------------------------------------------------------- segmentation --
+
+def boundaries(x, max_patch):
+    """Boundary positions q_1 < q_2 < ... (0-based byte indices).
+
+    A segment ends at a space byte (0x20), or when it reaches ``max_patch`` bytes
+    (the boundary predictor of the encoder-module paragraph is replaced by this rule).
+    """
+    q = []
+    prev = -1
+    for i, b in enumerate(np.asarray(x)):
+        if int(b) == SPACE or (max_patch > 0 and i - prev >= max_patch):
+            q.append(i)
+            prev = i
+    return q
+
+
+def group_ids(T, q):
+    """L(i) = number of boundaries q_j <= i: the latent a byte is upsampled from
+    (the boundary byte already uses the latent of the segment it closes)."""
+    L = np.zeros(T, dtype=np.int64)
+    for i in range(T):
+        L[i] = sum(1 for qj in q if qj <= i)
+    return L
+
+
+def group_start(j, q):
+    """First byte of group j: 0 for j = 0, else the j-th boundary byte."""
+    return 0 if j == 0 else q[j - 1]
+
+
+def downsample(h_e, q):
+    """Mean-pool each closed segment (encoder-module paragraph): latent j is the mean
+    of h_e over bytes q_{j-1}+1 .. q_j (q_0 = -1); an open trailing segment gives none."""
+    out = []
+    prev = -1
+    for qj in q:
+        out.append(np.mean(h_e[prev + 1: qj + 1], axis=0))
+        prev = qj
+    d = h_e.shape[1]
+    return np.array(out, dtype=np.float64).reshape(len(out), d)
+
+
+# -------------------------------------------------------------------- model --
+
+def trunk(W, cfg, x):
+    """Encoder, boundaries, downsample, LM module and next-byte decoder over the whole
+    byte sequence (Algorithm 1, first half; Section 2.2 module paragraphs).
+
+    Returns h_e, the boundaries q, LMin = [BOS; h_down], h_lm = LMModule(LMin), the
+    group ids L and the next-byte decoder output h1.
+    """
+    x = np.asarray(x, dtype=np.int64)
+    T = len(x)
+    pos = np.arange(T)
+    E = np.asarray(W["emb"], np.float64)[x]
+    h_e = stack(E, W, "enc", cfg.n_enc, causal_mask(T), pos, cfg)
+    q = boundaries(x, cfg.max_patch)
+    h_down = downsample(h_e, q)
+    LMin = np.vstack([np.asarray(W["bos"], np.float64)[None, :], h_down])
+    K1 = LMin.shape[0]
+    h_lm = stack(LMin, W, "lm", cfg.n_lm, causal_mask(K1), np.arange(K1), cfg)
+    L = group_ids(T, q)
+    nt_in = h_lm[L] + h_e
+    h1 = stack(nt_in, W, "nt", cfg.n_nb, causal_mask(T), pos, cfg)
+    return {"h_e": h_e, "q": q, "LMin": LMin, "h_lm": h_lm, "L": L, "h1": h1}
+
+
+def head_logits(h, g, W, eps):
+    """Shared unembedding (Section 3: both heads share one unembedding matrix) after
+    the head's final RMSNorm."""
+    return rms_norm(h, g, eps) @ np.asarray(W["unembed"], np.float64).T
+
+
+def mb_window(q, L, t, n, window_mode=0):
+    """Rows the MB layers run on (Algorithm 1: duplicate the last position n-2 times,
+    slice from the start of the previous segment).
+
+    Returns the window start s, the positions P = s..t+n-2 (virtual rows t+1..t+n-2
+    keep increasing positions) and their groups G (virtual rows belong to the current
+    group g = L(t)).  Window mode 1 starts at byte 0 instead.
+    """
+    g = int(L[t])
+    if window_mode == 0:
+        s = group_start(g - 1, q) if g >= 1 else 0
+    else:
+        s = 0
+    P = np.arange(s, t + n - 1)
+    G = np.array([int(L[p]) if p <= t else g for p in P], dtype=np.int64)
+    return s, P, G
+
+
+def mb_logits(W, cfg, tr, n):
+    """Rows 2..n of the step's candidate distributions from the MB head.
+
+    LCA (Algorithm 1, second half; Section 3): z_j = h'[j] + LMin[j]; every byte of
+    group j gets input z_j; the last position is duplicated n-2 times as virtual rows
+    t+1..t+n-2 of the current group; the window starts at the first byte of the
+    previous group; the MB layers run under the LCA mask; rows t..t+n-2 go to the
+    head (row t predicts x_{t+2}, the MB target shifted by two).
+
+    MLP (Section 4.1, MLP-MBP baseline): head m-1 is a residual pre-norm SwiGLU block
+    on h1[t]; its output goes through the NT final norm and the shared unembedding.
+    """
+    if n < 2:
+        return np.zeros((0, 256))
+    x_len = tr["h1"].shape[0]
+    t = x_len - 1
+    if cfg.head == "mlp":
+        h = tr["h1"][t]
+        rows = []
+        for m in range(2, n + 1):
+            P = {k: np.asarray(W[f"mlp.{m - 2}.{k}"], np.float64) for k in ("norm", "w_gate", "w_up", "w_down")}
+            y = h + ffn(rms_norm(h, P["norm"], cfg.rms_eps)[None, :], P)[0]
+            rows.append(head_logits(y, W["nt_norm"], W, cfg.rms_eps))
+        return np.array(rows)
+    s, P, G = mb_window(tr["q"], tr["L"], t, n, cfg.window_mode)
+    z = tr["h_lm"] + tr["LMin"]
+    u = z[G]
+    h2 = stack(u, W, "mb", cfg.n_mb, lca_mask(G), P, cfg)
+    rows = h2[t - s: t - s + n - 1]
+    return head_logits(rows, W["mb_norm"], W, cfg.rms_eps)
+
+
+def step_logits(W, cfg, x, n):
+    """The n x 256 logits of one step: row 1 from the next-byte head on h1[t]
+    (always accepted), rows 2..n from the MB head."""
+    tr = trunk(W, cfg, x)
+    t = len(x) - 1
+    l1 = head_logits(tr["h1"][t], W["nt_norm"], W, cfg.rms_eps)
+    return np.vstack([l1[None, :], mb_logits(W, cfg, tr, n)])
+
+
+def top1(logits):
+    """Per row: the greedy byte (lowest index among equal maxima) and its softmax
+    probability at temperature 1 over all 256 bytes."""
+    logits = np.asarray(logits, np.float64)
+    c = np.argmax(logits, axis=-1)
+    mx = np.take_along_axis(logits, c[:, None], axis=-1)
+    p = 1.0 / np.sum(np.exp(logits - mx), axis=-1)
+    return c.astype(np.int64), p
+
+
+def threshold_accept(prob, tau):
+    """Byte acceptance (Section 3.1): the next-byte candidate is always accepted; MB
+    candidates are accepted left to right while P >= tau; the first failure and all
+    later candidates are discarded.  Returns the number of accepted bytes k."""
+    k = 1
+    while k < len(prob) and prob[k] >= tau:
+        k += 1
+    return k
+
+
+def step(W, cfg, x, n, tau):
+    """One threshold-acceptance step of Algorithm 1 on the byte sequence ``x``."""
+    logits = step_logits(W, cfg, x, n)
+    cand, prob = top1(logits)
+    return {"logits": logits, "cand": cand, "prob": prob, "k": threshold_accept(prob, tau)}
+
+
+def _greedy_byte(W, cfg, x):
+    tr = trunk(W, cfg, x)
+    l1 = head_logits(tr["h1"][len(x) - 1], W["nt_norm"], W, cfg.rms_eps)
+    return int(top1(l1[None, :])[0][0])
+
+
+def verify_drafts(W, cfg, x, drafts):
+    """Greedy speculative verification (Section 6.2, following Leviathan et al.): draft
+    c_1 is kept; c_m (m >= 2) is kept while it equals the next-byte greedy byte after
+    x ++ c_1..c_{m-1}.  Returns the number of kept drafts j and the greedy bytes seen."""
+    drafts = np.asarray(drafts, np.int64)
+    j = 1
+    gammas = []
+    for m in range(2, len(drafts) + 1):
+        gm = _greedy_byte(W, cfg, np.concatenate([np.asarray(x, np.int64), drafts[: m - 1]]))
+        gammas.append(gm)
+        if gm != int(drafts[m - 1]):
+            break
+        j += 1
+    return j, gammas
+
+
+def verify_step(W, cfg, x, n):
+    """Self-verification step: drafts c_1..c_n from the next-byte and MB heads (c_1 is
+    the greedy byte), verified by extra next-byte passes."""
+    s = step(W, cfg, x, n, tau=2.0)
+    j, gammas = verify_drafts(W, cfg, x, s["cand"])
+    return {"logits": s["logits"], "cand": s["cand"], "prob": s["prob"], "k": j, "gamma": gammas}
+
+
+def generate(W, cfg, prompt, n_new, n, tau, mode="threshold"):
+    """Run steps until ``n_new`` bytes are emitted; the last step is truncated."""
+    x = [int(b) for b in prompt]
+    out, steps = [], []
+    while len(out) < n_new:
+        r = step(W, cfg, x, n, tau) if mode == "threshold" else verify_step(W, cfg, x, n)
+        k = min(r["k"], n_new - len(out))
+        acc = [int(c) for c in r["cand"][:k]]
+        steps.append({"k": r["k"], "cand": r["cand"].copy(), "prob": r["prob"].copy()})
+        out += acc
+        x += acc
+    return np.array(out, dtype=np.uint8), steps
+
+
+def greedy_generate(W, cfg, prompt, n_new):
+    """Byte-by-byte next-byte decoding (the n = 1 case)."""
+    x = [int(b) for b in prompt]
+    out = []
+    for _ in range(n_new):
+        b = _greedy_byte(W, cfg, x)
+        out.append(b)
+        x.append(b)
+    return np.array(out, dtype=np.uint8)

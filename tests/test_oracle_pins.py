@@ -1,0 +1,443 @@
+"""Pins of the CPU oracle against facts fixed by the paper and by mathematics.
+
+Each test checks the oracle against something other than itself: a closed form, a
+hand-computed fixture under tests/golden/, a brute-force loop written differently, or
+an invariant the paper states (causality of the LCA inputs, always-accepted next-byte
+candidate, verification reproducing next-byte decoding).
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import synth
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+TINY = synth.WORKLOADS["tiny_f32"].model
+
+
+def _bytes(text):
+    return np.frombuffer(text.encode("latin-1"), dtype=np.uint8)
+
+
+# ------------------------------------------------------------- primitives --
+
+def test_rms_norm_constant_vector_closed_form():
+    d, c, eps = 16, -3.0, 1e-6
+    g = np.linspace(0.5, 2.0, d)
+    out = oracle.rms_norm(np.full(d, c), g, eps)
+    # mean(x^2) = c^2, so every entry is c / sqrt(c^2 + eps) * g_i
+    expect = (c / math.sqrt(c * c + eps)) * g
+    np.testing.assert_allclose(out, expect, rtol=1e-15, atol=0)
+
+
+def test_rms_norm_unit_rms_and_eps_effect():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5, 64)) * 7.0
+    y = oracle.rms_norm(x, np.ones(64), 0.0)
+    np.testing.assert_allclose(np.sqrt(np.mean(y * y, axis=-1)), 1.0, rtol=1e-13)
+    # eps only shrinks the output; the direction is unchanged
+    y2 = oracle.rms_norm(x, np.ones(64), 1e-6)
+    cos = np.sum(y * y2, -1) / np.linalg.norm(y, axis=-1) / np.linalg.norm(y2, axis=-1)
+    np.testing.assert_allclose(cos, 1.0, rtol=1e-13)
+
+
+def test_rope_basis_vectors_rotate_by_expected_angles():
+    dh, base = 8, 1e5
+    for p in (0, 1, 7, 1234):
+        for pair in range(dh // 2):
+            e = np.zeros((1, 1, dh))
+            e[0, 0, 2 * pair] = 1.0
+            out = oracle.rope(e, [p], base)[0, 0]
+            theta = p * base ** (-(2.0 * pair) / dh)
+            want = np.zeros(dh)
+            want[2 * pair] = math.cos(theta)
+            want[2 * pair + 1] = math.sin(theta)
+            np.testing.assert_allclose(out, want, atol=1e-12)
+            # the odd partner rotates to (-sin, cos)
+            e2 = np.zeros((1, 1, dh))
+            e2[0, 0, 2 * pair + 1] = 1.0
+            out2 = oracle.rope(e2, [p], base)[0, 0]
+            want2 = np.zeros(dh)
+            want2[2 * pair] = -math.sin(theta)
+            want2[2 * pair + 1] = math.cos(theta)
+            np.testing.assert_allclose(out2, want2, atol=1e-12)
+
+
+def test_rope_norm_and_relative_position():
+    rng = np.random.default_rng(2)
+    q = rng.standard_normal((1, 3, 16))
+    k = rng.standard_normal((1, 3, 16))
+    for base in (1e4, 1e5):
+        a = oracle.rope(q, [5], base)
+        np.testing.assert_allclose(np.linalg.norm(a, axis=-1), np.linalg.norm(q, axis=-1), rtol=1e-13)
+        dots = []
+        for shift in (0, 3, 100, 4000):
+            qa = oracle.rope(q, [9 + shift], base)
+            ka = oracle.rope(k, [2 + shift], base)
+            dots.append(np.sum(qa * ka, axis=-1))
+        for dd in dots[1:]:
+            np.testing.assert_allclose(dd, dots[0], rtol=1e-9, atol=1e-11)
+
+
+def _rand_block(rng, d, dff, scale=0.2):
+    return {
+        "attn_norm": 1.0 + 0.1 * rng.standard_normal(d), "ffn_norm": 1.0 + 0.1 * rng.standard_normal(d),
+        "wq": scale * rng.standard_normal((d, d)), "wk": scale * rng.standard_normal((d, d)),
+        "wv": scale * rng.standard_normal((d, d)), "wo": scale * rng.standard_normal((d, d)),
+        "w_gate": scale * rng.standard_normal((dff, d)), "w_up": scale * rng.standard_normal((dff, d)),
+        "w_down": scale * rng.standard_normal((d, dff)),
+    }
+
+
+def test_attention_with_zero_query_key_is_mean_of_visible_values():
+    rng = np.random.default_rng(3)
+    T, d, H = 6, 8, 2
+    P = _rand_block(rng, d, 4 * d)
+    P["wq"][:] = 0.0
+    P["wk"][:] = 0.0
+    x = rng.standard_normal((T, d))
+    for mask in (oracle.causal_mask(T), oracle.lca_mask([0, 0, 1, 1, 2, 2])):
+        out = oracle.attention(x, P, mask, np.arange(T), H, 1e5, 1.0)
+        v = x @ P["wv"].T
+        mean_v = np.array([v[mask[i]].mean(axis=0) for i in range(T)])
+        np.testing.assert_allclose(out, mean_v @ P["wo"].T, rtol=1e-12, atol=1e-12)
+
+
+def test_attention_matches_scalar_loop():
+    """Independent scalar-loop attention: per head, per query, explicit RoPE angles,
+    dot products, max-subtracted exponentials and weighted sums."""
+    rng = np.random.default_rng(4)
+    T, d, H, base, scale = 5, 8, 2, 1e5, 1.0
+    dh = d // H
+    P = _rand_block(rng, d, 4 * d, scale=0.5)
+    x = rng.standard_normal((T, d))
+    pos = [3, 4, 5, 9, 10]
+    mask = oracle.lca_mask([0, 1, 1, 2, 2])
+    got = oracle.attention(x, P, mask, np.array(pos), H, base, scale)
+
+    def matvec(Wm, v):
+        return [sum(Wm[r][c] * v[c] for c in range(len(v))) for r in range(len(Wm))]
+
+    def rot(vec, p):
+        out = list(vec)
+        for i in range(dh // 2):
+            ang = p * base ** (-(2.0 * i) / dh)
+            a, b = vec[2 * i], vec[2 * i + 1]
+            out[2 * i] = a * math.cos(ang) - b * math.sin(ang)
+            out[2 * i + 1] = a * math.sin(ang) + b * math.cos(ang)
+        return out
+
+    Q = [matvec(P["wq"], x[i]) for i in range(T)]
+    Kx = [matvec(P["wk"], x[i]) for i in range(T)]
+    V = [matvec(P["wv"], x[i]) for i in range(T)]
+    concat = [[0.0] * d for _ in range(T)]
+    for h in range(H):
+        sl = slice(h * dh, (h + 1) * dh)
+        for i in range(T):
+            qi = rot(Q[i][sl], pos[i])
+            scores = {}
+            for j in range(T):
+                if mask[i, j]:
+                    kj = rot(Kx[j][sl], pos[j])
+                    scores[j] = sum(a * b for a, b in zip(qi, kj)) / math.sqrt(dh) * scale
+            mx = max(scores.values())
+            w = {j: math.exp(s - mx) for j, s in scores.items()}
+            z = sum(w.values())
+            for c in range(dh):
+                concat[i][h * dh + c] = sum(w[j] / z * V[j][sl][c] for j in w)
+    want = np.array([matvec(P["wo"], concat[i]) for i in range(T)])
+    np.testing.assert_allclose(got, want, rtol=1e-10, atol=1e-12)
+
+
+def test_ffn_matches_scalar_loop_and_zero_down_projection():
+    rng = np.random.default_rng(5)
+    d, dff = 4, 16
+    P = _rand_block(rng, d, dff, scale=0.7)
+    x = rng.standard_normal((3, d))
+    got = oracle.ffn(x, P)
+    for r in range(3):
+        hidden = []
+        for j in range(dff):
+            gj = sum(P["w_gate"][j][c] * x[r][c] for c in range(d))
+            uj = sum(P["w_up"][j][c] * x[r][c] for c in range(d))
+            hidden.append(gj / (1.0 + math.exp(-gj)) * uj)
+        for o in range(d):
+            want = sum(P["w_down"][o][j] * hidden[j] for j in range(dff))
+            assert abs(got[r][o] - want) < 1e-12
+    P["w_down"][:] = 0
+    assert np.all(oracle.ffn(x, P) == 0)
+
+
+def test_block_with_zero_weights_is_identity():
+    rng = np.random.default_rng(6)
+    d = 8
+    P = {k: np.zeros_like(v) if k.startswith("w") else v for k, v in _rand_block(rng, d, 32).items()}
+    u = rng.standard_normal((4, d))
+    np.testing.assert_array_equal(oracle.block(u, P, oracle.causal_mask(4), np.arange(4), TINY.replace(n_heads=2, d_model=8)), u)
+
+
+# ------------------------------------------------------------ segmentation --
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+@pytest.mark.parametrize("case", _golden("segmentation.json")["cases"])
+def test_boundaries_groups_segments(case):
+    x = _bytes(case["text"])
+    q = oracle.boundaries(x, case["max_patch"])
+    assert q == case["q"]
+    assert list(oracle.group_ids(len(x), q)) == case["L"]
+    # mean pool over h_e[i] = i * 1: latent j is the midpoint of its segment
+    h_e = np.repeat(np.arange(len(x), dtype=np.float64)[:, None], 3, axis=1)
+    down = oracle.downsample(h_e, q)
+    assert down.shape == (len(case["segments"]), 3)
+    for j, (a, b) in enumerate(case["segments"]):
+        np.testing.assert_allclose(down[j], (a + b) / 2.0, rtol=1e-15)
+
+
+@pytest.mark.parametrize("case", _golden("segmentation.json")["windows"]["cases"])
+def test_mb_window(case):
+    x = _bytes(case["text"])
+    q = oracle.boundaries(x, case["max_patch"])
+    L = oracle.group_ids(len(x), q)
+    s, P, G = oracle.mb_window(q, L, len(x) - 1, case["n"])
+    assert s == case["s"]
+    assert list(P) == case["P"]
+    assert list(G) == case["G"]
+
+
+@pytest.mark.parametrize("case", _golden("lca_masks.json")["cases"])
+def test_lca_mask_hand_matrices(case):
+    np.testing.assert_array_equal(oracle.lca_mask(case["G"]).astype(int), np.array(case["mask"]))
+
+
+# ---------------------------------------------------------- whole-model pins --
+
+def _zero_blocks(W):
+    out = dict(W)
+    for k, v in W.items():
+        if k.split(".")[-1] in ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down"):
+            out[k] = np.zeros_like(v)
+    return out
+
+
+def _rms(v, g, eps=1e-6):
+    return v / math.sqrt(float(np.mean(v * v)) + eps) * g
+
+
+@pytest.mark.parametrize("text,n", [("ab cd efg", 4), ("xyz", 3), ("a b c dd", 2), ("hello world  ok", 5)])
+def test_zero_block_model_closed_form(text, n):
+    """With every block matrix zero each block is the identity, so the whole step has
+    a closed form: h_e = E, LMin = [BOS; segment means of E], h' = LMin,
+    l_1 = U RMS(LMin[L(t)] + E[t]), and every MB row = U RMS(2 LMin[g])."""
+    cfg = TINY.replace(max_patch=0)
+    W = _zero_blocks(synth.make_weights(cfg, seed=11, gain_jitter=0.3))
+    x = _bytes(text)
+    t = len(x) - 1
+    E = W["emb"].astype(np.float64)[x]
+    q = [i for i, b in enumerate(x) if b == 0x20]
+    lat = [W["bos"].astype(np.float64)]
+    prev = -1
+    for qj in q:
+        lat.append(E[prev + 1: qj + 1].mean(axis=0))
+        prev = qj
+    g = sum(1 for qj in q if qj <= t)
+    U = W["unembed"].astype(np.float64)
+    l1 = U @ _rms(lat[g] + E[t], W["nt_norm"])
+    lmb = U @ _rms(2.0 * lat[g], W["mb_norm"])
+    got = oracle.step_logits(W, cfg, x, n)
+    assert got.shape == (n, 256)
+    np.testing.assert_allclose(got[0], l1, rtol=1e-12, atol=1e-13)
+    for m in range(1, n):
+        np.testing.assert_allclose(got[m], lmb, rtol=1e-12, atol=1e-13)
+
+
+def test_zero_block_mlp_head_rows_equal_next_byte_row():
+    cfg = TINY.replace(head="mlp", n_mb=3)
+    W = _zero_blocks(synth.make_weights(cfg, seed=3, gain_jitter=0.2))
+    got = oracle.step_logits(W, cfg, _bytes("abc de f"), 4)
+    for m in range(1, 4):
+        np.testing.assert_allclose(got[m], got[0], rtol=1e-13, atol=1e-14)
+
+
+def test_mlp_head_with_zero_down_projection_equals_next_byte_head():
+    cfg = TINY.replace(head="mlp", n_mb=3)
+    W = synth.make_weights(cfg, seed=4, gain_jitter=0.2)
+    x = synth.make_bytes(5, 40)
+    full = oracle.step_logits(W, cfg, x, 4)
+    W2 = dict(W)
+    W2["mlp.1.w_down"] = np.zeros_like(W["mlp.1.w_down"])
+    got = oracle.step_logits(W2, cfg, x, 4)
+    np.testing.assert_allclose(got[2], got[0], rtol=1e-13, atol=1e-14)
+    np.testing.assert_array_equal(got[[0, 1, 3]], full[[0, 1, 3]])
+    assert not np.allclose(full[2], full[0])
+
+
+def test_lm_module_with_zero_layers_is_identity():
+    cfg = TINY.replace(n_lm=0)
+    W = synth.make_weights(cfg, seed=8)
+    x = synth.make_bytes(9, 30)
+    tr = oracle.trunk(W, cfg, x)
+    np.testing.assert_array_equal(tr["h_lm"], tr["LMin"])
+
+
+def test_trunk_is_causal():
+    """h1[i] depends only on x_0..x_i: changing later bytes (including adding spaces,
+    which changes the later segmentation) leaves earlier rows unchanged."""
+    W = synth.make_weights(TINY, seed=12, gain_jitter=0.2)
+    x = synth.make_bytes(13, 50)
+    y = x.copy()
+    y[30:] = synth.make_bytes(14, 20)
+    a = oracle.trunk(W, TINY, x)["h1"]
+    b = oracle.trunk(W, TINY, y)["h1"]
+    np.testing.assert_allclose(a[:30], b[:30], rtol=1e-12, atol=1e-13)
+    assert not np.allclose(a[30:], b[30:])
+
+
+def _current_group_start(x, max_patch):
+    q = oracle.boundaries(x, max_patch)
+    return q[-1] if q else 0
+
+
+def test_mb_rows_do_not_depend_on_current_group_bytes():
+    """Section 3: inputs inside the current latent token are duplicates plus residuals
+    of the previous latent token, so the MB rows cannot see the bytes of the current
+    group after its boundary; the next-byte row does."""
+    cfg = TINY.replace(max_patch=0)
+    W = synth.make_weights(cfg, seed=15, gain_jitter=0.2)
+    x = _bytes("abc defgh ijk lmnop")
+    y = _bytes("abc defgh ijk lQRSp")
+    a = oracle.step_logits(W, cfg, x, 5)
+    b = oracle.step_logits(W, cfg, y, 5)
+    np.testing.assert_array_equal(a[1:], b[1:])
+    assert np.max(np.abs(a[0] - b[0])) > 1e-3
+    # a byte of the previous group does change the MB rows
+    z = _bytes("abc defgh iZk lmnop")
+    c = oracle.step_logits(W, cfg, z, 5)
+    assert np.max(np.abs(a[1:] - c[1:])) > 1e-6
+
+
+@pytest.mark.parametrize("window_mode", [0, 1])
+def test_mb_rows_prefix_stable_in_n(window_mode):
+    cfg = TINY.replace(window_mode=window_mode)
+    W = synth.make_weights(cfg, seed=16, gain_jitter=0.2)
+    x = synth.make_bytes(17, 60)
+    prev = oracle.step_logits(W, cfg, x, 2)
+    for n in range(3, 8):
+        cur = oracle.step_logits(W, cfg, x, n)
+        np.testing.assert_allclose(cur[:n - 1], prev, rtol=1e-11, atol=1e-12)
+        prev = cur
+
+
+def test_mb_rows_stable_when_one_non_boundary_byte_is_accepted():
+    """Row t+m-2 of the MB window is the same row whether it is virtual (step t) or
+    real (step t+1) while the group is unchanged: candidate m at t equals candidate
+    m-1 at t+1."""
+    cfg = TINY.replace(max_patch=0)
+    W = synth.make_weights(cfg, seed=18, gain_jitter=0.2)
+    x = _bytes("abc defgh ijk lm")
+    n = 5
+    a = oracle.step_logits(W, cfg, x, n)
+    b = oracle.step_logits(W, cfg, np.append(x, np.uint8(ord("q"))), n)
+    np.testing.assert_allclose(b[1:n - 1], a[2:n], rtol=1e-11, atol=1e-12)
+
+
+def test_window_modes_agree_with_one_mb_layer():
+    W = synth.make_weights(TINY, seed=19, gain_jitter=0.2)
+    x = synth.make_bytes(20, 70)
+    a = oracle.step_logits(W, TINY.replace(window_mode=0), x, 4)
+    b = oracle.step_logits(W, TINY.replace(window_mode=1), x, 4)
+    np.testing.assert_allclose(a, b, rtol=1e-11, atol=1e-12)
+    cfg2 = TINY.replace(n_mb=2)
+    W2 = synth.make_weights(cfg2, seed=19, gain_jitter=0.2)
+    a2 = oracle.step_logits(W2, cfg2.replace(window_mode=0), x, 4)
+    b2 = oracle.step_logits(W2, cfg2.replace(window_mode=1), x, 4)
+    assert np.max(np.abs(a2[1:] - b2[1:])) > 1e-9
+
+
+# ---------------------------------------------------------------- acceptance --
+
+def test_top1_matches_brute_force_softmax():
+    rng = np.random.default_rng(21)
+    logits = rng.standard_normal((6, 256)) * 3
+    logits[2, 10] = logits[2, 200] = logits[2].max() + 1.0  # tie: lowest index wins
+    c, p = oracle.top1(logits)
+    for r in range(6):
+        row = [float(v) for v in logits[r]]
+        best = 0
+        for j in range(256):
+            if row[j] > row[best]:
+                best = j
+        z = sum(math.exp(v) for v in row)
+        assert c[r] == best
+        assert abs(p[r] - math.exp(row[best]) / z) < 1e-14
+    assert c[2] == 10
+
+
+def test_threshold_acceptance_rule():
+    assert oracle.threshold_accept([0.1, 0.9, 0.8, 0.2, 0.99], 0.75) == 3
+    assert oracle.threshold_accept([0.1, 0.5, 0.99], 0.75) == 1
+    assert oracle.threshold_accept([0.1, 0.75, 0.75], 0.75) == 3  # P >= tau accepts
+    assert oracle.threshold_accept([0.3], 0.0) == 1
+    assert oracle.threshold_accept([0.3, 0.2, 0.1], 0.0) == 3
+
+
+@pytest.mark.parametrize("gain", [1.0, 25.0])
+def test_tau_extremes_and_monotonicity(gain):
+    W = synth.make_weights(TINY, seed=22, logit_gain=gain)
+    x = synth.make_prompt(0, 64)
+    n = 5
+    logits = oracle.step_logits(W, TINY, x, n)
+    _, prob = oracle.top1(logits)
+    assert np.all(prob < 1.0)
+    assert oracle.threshold_accept(prob, 1.0) == 1
+    assert oracle.threshold_accept(prob, 0.0) == n
+    ks = [oracle.threshold_accept(prob, tau) for tau in np.linspace(0, 1, 41)]
+    assert all(a >= b for a, b in zip(ks, ks[1:]))
+    assert all(1 <= k <= n for k in ks)
+
+
+def test_generation_tau_one_accepts_one_byte_per_step():
+    W = synth.make_weights(TINY, seed=23, logit_gain=20.0)
+    out, steps = oracle.generate(W, TINY, synth.make_prompt(0, 48), 10, 4, 1.0)
+    assert len(out) == 10 and len(steps) == 10
+    assert all(s["k"] == 1 for s in steps)
+
+
+def test_n1_and_threshold_generation_first_byte_is_greedy():
+    W = synth.make_weights(TINY, seed=24)
+    p = synth.make_prompt(1, 40)
+    g = oracle.greedy_generate(W, TINY, p, 12)
+    out1, _ = oracle.generate(W, TINY, p, 12, 1, 0.5)
+    np.testing.assert_array_equal(out1, g)
+
+
+# ------------------------------------------------------------- verification --
+
+def test_verify_forced_drafts():
+    W = synth.make_weights(TINY, seed=25, gain_jitter=0.2)
+    x = synth.make_prompt(2, 40)
+    g = oracle.greedy_generate(W, TINY, x, 6)
+    j, _ = oracle.verify_drafts(W, TINY, x, g)
+    assert j == 6
+    for m in range(2, 7):
+        bad = g.copy()
+        bad[m - 1] = (int(bad[m - 1]) + 1) % 256
+        j, _ = oracle.verify_drafts(W, TINY, x, bad)
+        assert j == m - 1
+
+
+@pytest.mark.parametrize("gain,n", [(1.0, 3), (30.0, 4), (30.0, 7)])
+def test_verify_generation_equals_greedy(gain, n):
+    W = synth.make_weights(TINY, seed=26, logit_gain=gain)
+    p = synth.make_prompt(3, 40)
+    g = oracle.greedy_generate(W, TINY, p, 14)
+    out, steps = oracle.generate(W, TINY, p, 14, n, 0.0, mode="verify")
+    np.testing.assert_array_equal(out, g)
+    assert all(1 <= s["k"] <= n for s in steps)
