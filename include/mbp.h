@@ -1,0 +1,183 @@
+/*
+ * mbp.h -- C ABI of the multi-byte-prediction (MBP) decode library for MI355X (gfx950).
+ *
+ * The library runs the decode loop of a byte-level hierarchical language model with
+ * multi-byte prediction, as defined in "Dynamic Multi-Byte Prediction With
+ * Hierarchical Language Models" (Algorithm 1, "Multi-byte Prediction with LCA";
+ * Section 3 and its "Byte Acceptance" paragraph; Section 6.2 for speculative
+ * verification).  Per batch row it keeps:
+ *   - the encoder and next-byte (NT) decoder KV caches over bytes,
+ *   - the mean-pooled latents ("LMin" = [BOS; h_down]) and the LM-module outputs h',
+ *     with the LM-module KV cache over latents (the LM runs only when a segment
+ *     closes -- the cached-LM inference of Algorithm 1),
+ *   - the MB-head window cache (LCA variant) over the previous and current groups,
+ *   - the last NT decoder row h1[t].
+ *
+ * Conventions
+ *   - Every pointer documented as "device" must point to memory of the current HIP
+ *     device; "host" pointers to ordinary host memory.
+ *   - The caller owns all device memory: weights, the workspace and all output
+ *     buffers.  The library never allocates or frees device memory; it carves the
+ *     caller's workspace.  It keeps a small host-side state per handle.
+ *   - All device work is enqueued on the stream given to mbp_init.  Device outputs
+ *     are valid once the caller synchronizes that stream.  Calls that need host-side
+ *     values (mbp_accept, mbp_decode_step in verify mode) synchronize it themselves.
+ *   - Every function returns an mbp_status (0 = success) and never throws or exits.
+ *     Arguments are validated before any device work; MBP_EINVAL / MBP_ECAPACITY
+ *     leave the handle's state unchanged.  A failed HIP call returns MBP_EHIP and
+ *     poisons the handle: afterwards only mbp_reset, mbp_destroy and mbp_last_error
+ *     are accepted (others return MBP_ESTATE).
+ *   - A handle is not thread-safe; use one handle per host thread.
+ */
+#ifndef MBP_H
+#define MBP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mbp_handle mbp_handle;
+
+typedef enum {
+  MBP_OK = 0,
+  MBP_EINVAL = -1,    /* invalid argument or configuration */
+  MBP_ECAPACITY = -2, /* request exceeds a capacity fixed at mbp_init */
+  MBP_EHIP = -3,      /* a HIP runtime call failed; the handle is poisoned */
+  MBP_ESTATE = -4     /* call not allowed in the handle's current state */
+} mbp_status;
+
+typedef enum { MBP_HEAD_LCA = 0, MBP_HEAD_MLP = 1 } mbp_head;
+typedef enum { MBP_F32 = 0, MBP_BF16 = 1, MBP_F16 = 2 } mbp_dtype;
+typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
+
+/* Model architecture and capacities.
+ *   d_model, n_heads          hidden size and attention heads (KV heads = heads);
+ *                             d_model / n_heads must be 32 or 64.
+ *   d_ff                      SwiGLU inner size (the paper's d_inner = 4 d_model).
+ *   n_enc, n_lm, n_nb, n_mb   layers of the encoder, LM module, next-byte decoder,
+ *                             and MB head (LCA: transformer layers; MLP: heads).
+ *   head, dtype               mbp_head, mbp_dtype (MBP_F32 or MBP_BF16): storage type
+ *                             of the weights.  Activations, residual streams, norms,
+ *                             accumulation and softmax are float32.
+ *   max_batch, max_ctx        rows, and bytes per row (prompt + generated + max_n).
+ *   max_latents               closed segments per row (latents, BOS excluded).
+ *   max_n                     candidates per step, 1..8.
+ *   max_patch                 a segment also closes when it reaches this many bytes;
+ *                             0 = only the space byte (0x20) closes a segment.
+ *   max_window                MB window rows; 0 = 2*max_patch + max_n - 2 (needs
+ *                             max_patch > 0).
+ *   max_chunk                 tokens per internal pass of a long commit (0 = 4096).
+ *   rope_base, rms_eps, attn_scale   1e5, 1e-6 and 1.0 in the paper.  Attention
+ *                             scores are q.k / sqrt(d_head) * attn_scale.
+ *   window_mode               0: the MB layers run on the window of Algorithm 1 only
+ *                             (previous + current group + n-2 virtual rows).  Other
+ *                             values are rejected with MBP_EINVAL.
+ *   kv_dtype                  storage type of every KV cache: MBP_F32, MBP_BF16 or
+ *                             MBP_F16.  MBP_F16 stores the same bytes as bf16 with 3
+ *                             more mantissa bits; values beyond +-65504 saturate.
+ */
+typedef struct {
+  int32_t d_model, n_heads, d_ff;
+  int32_t n_enc, n_lm, n_nb, n_mb;
+  int32_t head, dtype;
+  int32_t max_batch, max_ctx, max_latents, max_n, max_patch, max_window, max_chunk;
+  float rope_base, rms_eps, attn_scale;
+  int32_t window_mode;
+  int32_t kv_dtype;
+} mbp_config;
+
+/* Number of weight tensors of the manifest for cfg, or a negative status. */
+int32_t mbp_weight_count(const mbp_config *cfg);
+
+/* Name and shape of manifest tensor idx.  Matrices are [rows = out_features,
+ * cols = in_features] row-major (y = W x); vectors have cols = 1.  Order: emb [256,d],
+ * bos [d]; per encoder, LM-module, NT-decoder block: attn_norm, wq, wk, wv, wo,
+ * ffn_norm, w_gate, w_up, w_down; nt_norm [d]; unembed [256,d]; then the head: LCA
+ * blocks (same 9 tensors) and mb_norm, or per MLP head: norm, w_gate, w_up, w_down.
+ * name_buf receives a NUL-terminated name (may be NULL). */
+int mbp_weight_info(const mbp_config *cfg, int32_t idx, char *name_buf, size_t name_len,
+                    int64_t *rows, int64_t *cols);
+
+/* Device workspace bytes needed by mbp_init for cfg (0 on an invalid cfg). */
+size_t mbp_workspace_bytes(const mbp_config *cfg);
+
+/* Create a handle.
+ *   d_weights   n_weights device pointers in manifest order, each holding the tensor
+ *               in cfg->dtype (bf16 = raw IEEE bfloat16 bits), row-major.  Borrowed
+ *               until mbp_destroy.
+ *   d_workspace device buffer of ws_bytes >= mbp_workspace_bytes(cfg), 256-byte
+ *               aligned.  Borrowed until mbp_destroy; contents need no initialization.
+ *   hip_stream  hipStream_t all work is enqueued on (NULL = default stream).
+ * Enqueues a small table-initialization kernel. */
+int mbp_init(const mbp_config *cfg, const void *const *d_weights, int32_t n_weights,
+             void *d_workspace, size_t ws_bytes, void *hip_stream, mbp_handle **out);
+
+/* Start every row from an empty state and commit its prompt (Algorithm 1 before the
+ * first step: encoder over the prompt, segmentation, LM module over BOS and every
+ * closed segment, NT decoder over the prompt).
+ *   h_bytes  host; the prompts back to back, row r at offset sum(h_lens[0..r-1]).
+ *   h_lens   host; batch lengths, each >= 1.
+ *   batch    1..max_batch; rows >= batch become inactive.
+ * MBP_ECAPACITY if a prompt exceeds max_ctx or its segments exceed max_latents. */
+int mbp_prefill(mbp_handle *h, const uint8_t *h_bytes, const int32_t *h_lens, int32_t batch);
+
+/* One decode step for every active row (Algorithm 1 body): the NT head on h1[t]
+ * gives candidate 1; the MB head gives candidates 2..n (LCA: the window of the
+ * previous and current groups plus n-2 duplicated rows under the LCA mask; MLP:
+ * head m-1 on h1[t]).  For each candidate row the greedy byte (lowest index among
+ * equal maxima) and its softmax probability over the 256 bytes are computed.
+ *   n      1..max_n (MLP head: n-1 <= n_mb).
+ *   tau    acceptance threshold in [0, 1] (threshold mode).
+ *   mode   MBP_ACCEPT_THRESHOLD: accept_len = 1 + number of leading candidates
+ *          m >= 2 with P_m >= tau (Section 3, "Byte Acceptance").  Caches unchanged.
+ *          MBP_ACCEPT_SELF_VERIFY: the n candidates are drafts; they are committed
+ *          tentatively, verified against the NT greedy byte at each draft position,
+ *          and the caches are rolled back to the accepted prefix (accept_len =
+ *          1 + number of leading verified drafts; Section 6.2).  Synchronizes.
+ *   d_cand        device uint8  [batch, n]   candidate bytes.
+ *   d_prob        device float  [batch, n]   their probabilities (may be NULL).
+ *   d_accept_len  device int32  [batch]      accepted count, 1..n (0 for inactive rows).
+ * Row r's accepted bytes are d_cand[r, 0 : d_accept_len[r]]. */
+int mbp_decode_step(mbp_handle *h, int32_t n, float tau, int32_t mode, uint8_t *d_cand,
+                    float *d_prob, int32_t *d_accept_len);
+
+/* Copy the last step's accepted bytes to the host (synchronizes the stream).
+ *   h_bytes  host [batch, max_n]: row r's bytes at h_bytes[r*max_n ...].
+ *   h_lens   host [batch]: accepted counts. */
+int mbp_last_accepted(mbp_handle *h, uint8_t *h_bytes, int32_t *h_lens);
+
+/* Commit bytes into every cache (Algorithm 1, "append accepted bytes", followed by
+ * the encoder / segmentation / LM / NT work of the next iteration).
+ *   h_override == NULL: commit the last decode step's accepted bytes (for a verify
+ *     step they are already committed; this only closes the step).
+ *   h_override != NULL: host [batch, max_n] bytes and h_override_len host [batch]
+ *     counts (0..max_n) to commit instead (teacher forcing); a pending verify step
+ *     is rolled back first.
+ * MBP_ESTATE if no decode step is pending and no override is given; MBP_ECAPACITY if
+ * a row would exceed max_ctx or max_latents. */
+int mbp_accept(mbp_handle *h, const uint8_t *h_override, const int32_t *h_override_len);
+
+/* Copy the last step's logits, float [batch, n, 256], into d_logits (device). */
+int mbp_get_logits(mbp_handle *h, float *d_logits);
+
+/* Current committed length of row r (host value), or a negative status. */
+int32_t mbp_row_length(const mbp_handle *h, int32_t row);
+
+/* Forget all rows (no device work); the handle becomes usable again after a HIP
+ * error. */
+int mbp_reset(mbp_handle *h);
+
+/* Free the host-side handle.  Device memory stays the caller's. */
+void mbp_destroy(mbp_handle *h);
+
+/* Last error message of the handle ("" if none); valid until the next call. */
+const char *mbp_last_error(const mbp_handle *h);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MBP_H */

@@ -7,6 +7,7 @@ Algorithm 1 ("Multi-byte Prediction with LCA") at every step.
 """
 from .model import (  # noqa: F401
     SPACE,
+    to_float64,
     rms_norm,
     rope,
     causal_mask,

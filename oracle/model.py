@@ -91,14 +91,15 @@ def attention(x, P, mask, pos, n_heads, rope_base, attn_scale):
     q = (x @ P["wq"].T).reshape(T, n_heads, dh)
     k = (x @ P["wk"].T).reshape(T, n_heads, dh)
     v = (x @ P["wv"].T).reshape(T, n_heads, dh)
-    q = rope(q, pos, rope_base)
-    k = rope(k, pos, rope_base)
-    scores = np.einsum("ihd,jhd->hij", q, k) * (attn_scale / np.sqrt(dh))
+    q = rope(q, pos, rope_base).transpose(1, 0, 2)  # [H, T, dh]
+    k = rope(k, pos, rope_base).transpose(1, 0, 2)
+    v = v.transpose(1, 0, 2)
+    scores = (q @ k.transpose(0, 2, 1)) * (attn_scale / np.sqrt(dh))  # [H, T(query), T(key)]
     scores = np.where(mask[None, :, :], scores, -np.inf)
     scores = scores - scores.max(axis=-1, keepdims=True)
     p = np.exp(scores)
     p = p / p.sum(axis=-1, keepdims=True)
-    o = np.einsum("hij,jhd->ihd", p, v).reshape(T, d)
+    o = (p @ v).transpose(1, 0, 2).reshape(T, d)
     return o @ P["wo"].T
 
 
@@ -116,6 +117,11 @@ def block(u, P, mask, pos, cfg):
     a = u + attention(rms_norm(u, P["attn_norm"], cfg.rms_eps), P, mask, pos,
                       cfg.n_heads, cfg.rope_base, cfg.attn_scale)
     return a + ffn(rms_norm(a, P["ffn_norm"], cfg.rms_eps), P)
+
+
+def to_float64(W):
+    """The weight dict with every tensor as a float64 array (done once per model)."""
+    return {k: np.asarray(v, np.float64) for k, v in W.items()}
 
 
 def _params(W, prefix):
@@ -150,10 +156,8 @@ def boundaries(x, max_patch):
 def group_ids(T, q):
     """L(i) = number of boundaries q_j <= i: the latent a byte is upsampled from
     (the boundary byte already uses the latent of the segment it closes)."""
-    L = np.zeros(T, dtype=np.int64)
-    for i in range(T):
-        L[i] = sum(1 for qj in q if qj <= i)
-    return L
+    qa = np.asarray(q, dtype=np.int64).reshape(1, -1)
+    return (qa <= np.arange(T, dtype=np.int64)[:, None]).sum(axis=1).astype(np.int64)
 
 
 def group_start(j, q):

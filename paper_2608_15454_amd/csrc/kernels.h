@@ -1,0 +1,109 @@
+// Internal interface between the host runtime (runtime.hip) and the gfx950 kernels
+// (kernels.hip).  Not part of the public C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mbp {
+
+// A list of M token rows processed together by one module pass.  Row i belongs to
+// batch row b[i]; pos[i] is its RoPE position, slot[i] its KV-cache slot, kvlen[i]
+// the number of visible cache slots (slots 0..kvlen-1), grp[i] its group id (only
+// read when an attention pass uses a group table).
+struct Tok {
+  const int32_t* b;
+  const int32_t* pos;
+  const int32_t* slot;
+  const int32_t* kvlen;
+  const int32_t* grp;
+  int32_t M;
+};
+
+// Weight rows of one linear layer.  SINGLE: N rows of m[0].  QKV: rows [0,rows) of
+// m[0], then m[1], then m[2].  GATEUP: virtual row 2j is row j of m[0] (gate), 2j+1
+// row j of m[1] (up), so a gate/up pair lands in one thread.
+enum MatMode { MAT_SINGLE = 0, MAT_QKV = 1, MAT_GATEUP = 2 };
+struct Mats {
+  const void* m[3];
+  int32_t rows;
+  int32_t mode;
+};
+
+// Epilogue of a linear layer applied to output (row i, column n).
+//   STORE:  Y[i*ldy + n] = acc
+//   RESID:  Y[i*ldy + n] += acc
+//   SWIGLU: columns (2j, 2j+1) = (gate, up) -> Y[i*ldy + j] = silu(gate) * up
+//   QKV:    columns [0,d) -> RoPE -> Q[i*d + c]; [d,2d) -> RoPE -> K cache;
+//           [2d,3d) -> V cache.  Cache element of (row b, head h, slot s, e) is at
+//           kc[b*b_stride + (h*cap + s)*dh + e].
+enum EpiKind { EPI_STORE = 0, EPI_RESID = 1, EPI_SWIGLU = 2, EPI_QKV = 3 };
+struct Epi {
+  int32_t kind;
+  float* Y;
+  int32_t ldy;
+  float* Q;
+  void* kc;
+  void* vc;
+  int64_t b_stride;
+  int32_t cap, H, dh, d;
+  const float2* rope;  // [position][dh/2] = (cos, sin)
+  Tok tok;
+  int32_t kvt;  // cache element type: 0 float32, 1 bfloat16, 2 float16
+};
+
+struct Linear {
+  const float* X;  // [M, ldx] float32 inputs
+  int32_t ldx, M, K, N;
+  const float* gain;  // RMSNorm gain over K (float32) or nullptr for no norm
+  float eps;
+  Mats mats;
+  Epi epi;
+};
+
+// Attention of M query rows (Q [M, ldq], head h at columns h*dh) over a KV cache.
+struct Attn {
+  const float* Q;
+  int32_t ldq;
+  const void* kc;
+  const void* vc;
+  int64_t b_stride;
+  int32_t cap, H, dh;
+  Tok tok;
+  const int32_t* grp_tab;  // [B, cap] group ids of cache slots, or nullptr (causal only)
+  float scale;
+  float* O;  // [M, ldo]
+  int32_t ldo;
+};
+
+// Launchers.  wdt: 0 = float32 weights, 1 = bfloat16.  kvt: cache element type,
+// 0 = float32, 1 = bfloat16, 2 = float16.
+hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms_scratch, hipStream_t st);
+// Split-KV attention; part: scratch of M*H*splits*(dh+2) floats; max_kv bounds kvlen.
+hipError_t launch_attn_split(const Attn& a, int kvt, int max_kv, float* part, int64_t part_floats,
+                             hipStream_t st);
+// Tiled causal attention for long runs of consecutive slots of one batch row.
+// tiles: device int32 [ntiles*2] = (first token, count <= 64) with consecutive slots.
+hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int ntiles, hipStream_t st);
+
+hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st);
+// dst[dst_idx[i]] = src[src_idx[i]] (+ src2[src2_idx[i]]); null index arrays mean i.
+hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const float* src2,
+                            const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d, int M,
+                            hipStream_t st);
+// Mean of cnt[i] rows of src starting at row lo[i] -> dst[dst_idx[i]]; cnt 0 copies bos.
+hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, const float* bos,
+                       float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st);
+// out[dst_idx[i]] = RMSNorm(src[src_idx[i]]) * gain; null index arrays mean i.
+hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps,
+                            float* out, const int32_t* dst_idx, int d, int M, hipStream_t st);
+// Per batch row b < B: greedy byte and probability of each of the n logit rows,
+// then accept_len (threshold mode; write_len = 0 leaves accept_len untouched).
+hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active,
+                         uint8_t* cand, float* prob, int32_t* accept_len, int write_len, hipStream_t st);
+// Greedy verification: NT logits of the n tentative rows vs the drafts.
+hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
+                         int32_t* accept_len, hipStream_t st);
+hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st);
+hipError_t launch_rope_table(float2* tab, int npos, int dh, double base, hipStream_t st);
+
+}  // namespace mbp

@@ -1,0 +1,981 @@
+// Host runtime of the MBP decode library: the C ABI declared in include/mbp.h.
+//
+// The host keeps, per batch row, the committed bytes and their segmentation
+// (boundary positions); it turns every commit and decode step into token lists
+// ("plans") that are uploaded in one copy and consumed by the gfx950 kernels in
+// kernels.hip.  All model state (KV caches, pooled latents, LM outputs, MB window
+// cache, last NT row) lives in the caller's device workspace.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "kernels.h"
+#include "mbp.h"
+
+using namespace mbp;
+
+namespace {
+
+constexpr int kMaxN = 8;
+constexpr int kParts = 9;  // tensors per transformer block in the manifest
+
+struct BlockW {
+  const float* attn_norm;
+  const void *wq, *wk, *wv, *wo;
+  const float* ffn_norm;
+  const void *wg, *wu, *wd;
+};
+
+struct MlpW {
+  const float* norm;
+  const void *wg, *wu, *wd;
+};
+
+struct KV {  // one module's KV cache: layer l of row b at k + l*layer_stride + b*b_stride
+  void* k = nullptr;
+  void* v = nullptr;
+  int64_t layer_stride = 0, b_stride = 0;
+  int32_t cap = 0;
+};
+
+struct Row {
+  bool active = false;
+  std::vector<uint8_t> x;   // committed bytes
+  std::vector<int32_t> q;   // boundary positions (each closes one latent)
+  int32_t lm_rows = 0;      // latent rows the LM module has processed (BOS + closed)
+  int64_t epoch = 0;        // bumped whenever the latent list changes
+  int64_t win_epoch = -1;   // epoch of the MB window cache
+  int32_t win_s = 0, win_valid = 0;
+};
+
+struct Sizes {
+  int d, H, dh, dff, B, Tcap, Kcap, Wcap, Mc, Ml, nmax, Smax;
+  int64_t part_floats;
+  size_t es;  // element size of the KV caches
+};
+
+struct Regions {
+  size_t gains, rope, enc_k, enc_v, lm_k, lm_v, nt_k, nt_v, mb_k, mb_v, he, lat_in, lat_out, mbh, h1, h1_save,
+      mlp_out, head_in, logits, vlogits, X, Xl, Q, O, Hid, inv, part, plan0, plan1, active, total;
+  size_t plan_ints;
+};
+
+bool valid_cfg(const mbp_config* c, std::string* why) {
+  auto bad = [&](const char* m) {
+    if (why) *why = m;
+    return false;
+  };
+  if (!c) return bad("null config");
+  if (c->d_model <= 0 || c->n_heads <= 0 || c->d_model % c->n_heads) return bad("d_model must be a positive multiple of n_heads");
+  const int dh = c->d_model / c->n_heads;
+  if (dh != 32 && dh != 64) return bad("d_model / n_heads must be 32 or 64");
+  if (c->d_model % 64) return bad("d_model must be a multiple of 64");
+  if (c->d_ff <= 0 || c->d_ff % 64) return bad("d_ff must be a positive multiple of 64");
+  if (c->n_enc < 0 || c->n_lm < 0 || c->n_nb < 0 || c->n_mb < 0) return bad("negative layer count");
+  if (c->n_enc > 64 || c->n_lm > 256 || c->n_nb > 64 || c->n_mb > 64) return bad("layer count too large");
+  if (c->head != MBP_HEAD_LCA && c->head != MBP_HEAD_MLP) return bad("head must be MBP_HEAD_LCA or MBP_HEAD_MLP");
+  if (c->dtype != MBP_F32 && c->dtype != MBP_BF16) return bad("dtype must be MBP_F32 or MBP_BF16");
+  if (c->max_batch < 1 || c->max_batch > 4096) return bad("max_batch out of range");
+  if (c->max_ctx < 2) return bad("max_ctx must be >= 2");
+  if (c->max_latents < 1 || c->max_latents > c->max_ctx) return bad("max_latents must be in [1, max_ctx]");
+  if (c->max_n < 1 || c->max_n > kMaxN) return bad("max_n must be in [1, 8]");
+  if (c->max_patch < 0) return bad("max_patch must be >= 0");
+  if (c->max_window < 0) return bad("max_window must be >= 0");
+  if (c->max_window == 0 && c->max_patch == 0) return bad("max_window must be given when max_patch = 0");
+  if (c->max_chunk < 0) return bad("max_chunk must be >= 0");
+  if (c->window_mode != 0) return bad("only window_mode 0 is implemented");
+  if (c->kv_dtype != MBP_F32 && c->kv_dtype != MBP_BF16 && c->kv_dtype != MBP_F16) return bad("bad kv_dtype");
+  if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f) || !std::isfinite(c->attn_scale)) return bad("bad rope_base/rms_eps/attn_scale");
+  return true;
+}
+
+Sizes sizes_of(const mbp_config& c) {
+  Sizes s;
+  s.d = c.d_model;
+  s.H = c.n_heads;
+  s.dh = c.d_model / c.n_heads;
+  s.dff = c.d_ff;
+  s.B = c.max_batch;
+  s.Tcap = c.max_ctx;
+  s.Kcap = c.max_latents + 1;
+  s.nmax = c.max_n;
+  s.Wcap = c.max_window > 0 ? c.max_window : std::max(2 * c.max_patch + c.max_n - 2, c.max_n);
+  const int chunk = c.max_chunk > 0 ? c.max_chunk : 4096;
+  s.Mc = std::max({chunk, s.B * s.nmax, s.B * s.Wcap});
+  s.Ml = s.Mc + s.B;
+  s.Smax = (s.Tcap + 255) / 256;
+  s.part_floats = (int64_t)s.B * (s.nmax + 1) * s.H * s.Smax * (s.dh + 2);
+  s.es = c.kv_dtype == MBP_F32 ? 4 : 2;
+  return s;
+}
+
+int n_gain_vectors(const mbp_config& c) {
+  int n = 2 * (c.n_enc + c.n_lm + c.n_nb) + 1 /*nt_norm*/ + 1 /*bos*/;
+  if (c.head == MBP_HEAD_LCA) n += 2 * c.n_mb + 1;
+  else n += c.n_mb;
+  return n;
+}
+
+Regions layout(const mbp_config& c) {
+  const Sizes s = sizes_of(c);
+  Regions r{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  const int npos = std::max(s.Tcap + s.nmax, s.Kcap) + 1;
+  r.gains = take((size_t)n_gain_vectors(c) * s.d * 4);
+  r.rope = take((size_t)npos * (s.dh / 2) * 8);
+  const size_t kv_bt = (size_t)s.B * s.Tcap * s.d * s.es;
+  const size_t kv_bk = (size_t)s.B * s.Kcap * s.d * s.es;
+  const size_t kv_bw = (size_t)s.B * s.Wcap * s.d * s.es;
+  r.enc_k = take(kv_bt * c.n_enc);
+  r.enc_v = take(kv_bt * c.n_enc);
+  r.lm_k = take(kv_bk * c.n_lm);
+  r.lm_v = take(kv_bk * c.n_lm);
+  r.nt_k = take(kv_bt * c.n_nb);
+  r.nt_v = take(kv_bt * c.n_nb);
+  const int nmb_layers = c.head == MBP_HEAD_LCA ? c.n_mb : 0;
+  r.mb_k = take(kv_bw * nmb_layers);
+  r.mb_v = take(kv_bw * nmb_layers);
+  r.he = take((size_t)s.B * s.Tcap * s.d * 4);
+  r.lat_in = take((size_t)s.B * s.Kcap * s.d * 4);
+  r.lat_out = take((size_t)s.B * s.Kcap * s.d * 4);
+  r.mbh = take((size_t)s.B * s.Wcap * s.d * 4);
+  r.h1 = take((size_t)s.B * s.d * 4);
+  r.h1_save = take((size_t)s.B * s.d * 4);
+  r.mlp_out = take((size_t)s.B * s.nmax * s.d * 4);
+  r.head_in = take((size_t)s.B * s.nmax * s.d * 4);
+  r.logits = take((size_t)s.B * s.nmax * 256 * 4);
+  r.vlogits = take((size_t)s.B * s.nmax * 256 * 4);
+  // every per-pass buffer holds Ml = Mc + B rows: a chunk of Mc bytes can close
+  // up to Mc segments, plus one BOS latent per row
+  r.X = take((size_t)s.Ml * s.d * 4);
+  r.Xl = take((size_t)s.Ml * s.d * 4);
+  r.Q = take((size_t)s.Ml * s.d * 4);
+  r.O = take((size_t)s.Ml * s.d * 4);
+  r.Hid = take((size_t)s.Ml * s.dff * 4);
+  r.inv = take((size_t)s.Ml * 4);
+  r.part = take((size_t)s.part_floats * 4);
+  r.plan_ints = (size_t)20 * s.Ml + (size_t)s.B * s.Wcap + 64;
+  r.plan0 = take(r.plan_ints * 4);
+  r.plan1 = take(r.plan_ints * 4);
+  r.active = take((size_t)s.B * 4);
+  r.total = off;
+  return r;
+}
+
+// ------------------------------------------------------------------ manifest --
+struct WInfo {
+  std::string name;
+  int64_t rows, cols;
+};
+
+std::vector<WInfo> manifest(const mbp_config& c) {
+  std::vector<WInfo> m;
+  const int64_t d = c.d_model, f = c.d_ff;
+  m.push_back({"emb", 256, d});
+  m.push_back({"bos", d, 1});
+  auto block = [&](const std::string& p) {
+    m.push_back({p + ".attn_norm", d, 1});
+    m.push_back({p + ".wq", d, d});
+    m.push_back({p + ".wk", d, d});
+    m.push_back({p + ".wv", d, d});
+    m.push_back({p + ".wo", d, d});
+    m.push_back({p + ".ffn_norm", d, 1});
+    m.push_back({p + ".w_gate", f, d});
+    m.push_back({p + ".w_up", f, d});
+    m.push_back({p + ".w_down", d, f});
+  };
+  for (int i = 0; i < c.n_enc; ++i) block("enc." + std::to_string(i));
+  for (int i = 0; i < c.n_lm; ++i) block("lm." + std::to_string(i));
+  for (int i = 0; i < c.n_nb; ++i) block("nt." + std::to_string(i));
+  m.push_back({"nt_norm", d, 1});
+  m.push_back({"unembed", 256, d});
+  if (c.head == MBP_HEAD_LCA) {
+    for (int i = 0; i < c.n_mb; ++i) block("mb." + std::to_string(i));
+    m.push_back({"mb_norm", d, 1});
+  } else {
+    for (int i = 0; i < c.n_mb; ++i) {
+      const std::string p = "mlp." + std::to_string(i);
+      m.push_back({p + ".norm", d, 1});
+      m.push_back({p + ".w_gate", f, d});
+      m.push_back({p + ".w_up", f, d});
+      m.push_back({p + ".w_down", d, f});
+    }
+  }
+  return m;
+}
+
+// Host-side staging of one device plan (int32 arrays at recorded offsets).
+struct Plan {
+  std::vector<int32_t> buf;
+  int32_t* dev = nullptr;
+  size_t cap = 0;
+  size_t add(const std::vector<int32_t>& a) {
+    const size_t o = buf.size();
+    buf.insert(buf.end(), a.begin(), a.end());
+    while (buf.size() % 4) buf.push_back(0);
+    return o;
+  }
+  const int32_t* at(size_t o) const { return dev + o; }
+};
+
+struct Toks {  // host token list of one module pass
+  std::vector<int32_t> b, pos, slot, kvlen, grp;
+  void push(int32_t bb, int32_t p, int32_t s, int32_t kv, int32_t g) {
+    b.push_back(bb);
+    pos.push_back(p);
+    slot.push_back(s);
+    kvlen.push_back(kv);
+    grp.push_back(g);
+  }
+  int size() const { return (int)b.size(); }
+};
+
+struct TokOffs {
+  size_t b, pos, slot, kvlen, grp;
+};
+
+}  // namespace
+
+struct mbp_handle {
+  mbp_config cfg;
+  Sizes sz;
+  Regions rg;
+  int wdt;
+  hipStream_t st;
+  char* ws;
+  bool poisoned = false;
+  std::string err;
+
+  const void* emb;
+  const void* unembed;
+  const float* bos32;
+  const float* g_nt;
+  const float* g_mb;
+  std::vector<BlockW> enc, lm, nt, mb;
+  std::vector<MlpW> mlp;
+  KV kv_enc, kv_lm, kv_nt, kv_mb;
+  float2* rope;
+
+  std::vector<Row> rows;
+  int batch = 0;
+  bool pending = false;
+  int last_n = 0, last_mode = 0;
+  std::vector<uint8_t> h_cand;
+  std::vector<int32_t> h_len;
+  std::vector<int32_t> pre_len;
+  Plan plan[2];
+
+  template <typename T>
+  T* R(size_t off) { return reinterpret_cast<T*>(ws + off); }
+};
+
+namespace {
+
+int fail(mbp_handle* h, int code, const std::string& msg) {
+  h->err = msg;
+  return code;
+}
+
+int fail_hip(mbp_handle* h, hipError_t e, const char* what) {
+  h->poisoned = true;
+  h->err = std::string("HIP error in ") + what + ": " + hipGetErrorString(e);
+  return MBP_EHIP;
+}
+
+#define HIPCK(h, x)                                  \
+  do {                                               \
+    hipError_t e_ = (x);                             \
+    if (e_ != hipSuccess) return fail_hip(h, e_, #x); \
+  } while (0)
+
+int upload(mbp_handle* h, Plan& p) {
+  if (p.buf.size() > p.cap) return fail(h, MBP_ECAPACITY, "internal plan exceeds its capacity");
+  if (!p.buf.empty())
+    HIPCK(h, hipMemcpyAsync(p.dev, p.buf.data(), p.buf.size() * 4, hipMemcpyHostToDevice, h->st));
+  return MBP_OK;
+}
+
+TokOffs add_toks(Plan& p, const Toks& t) {
+  TokOffs o;
+  o.b = p.add(t.b);
+  o.pos = p.add(t.pos);
+  o.slot = p.add(t.slot);
+  o.kvlen = p.add(t.kvlen);
+  o.grp = p.add(t.grp);
+  return o;
+}
+
+Tok dev_tok(const Plan& p, const TokOffs& o, int M) {
+  Tok t;
+  t.b = p.at(o.b);
+  t.pos = p.at(o.pos);
+  t.slot = p.at(o.slot);
+  t.kvlen = p.at(o.kvlen);
+  t.grp = p.at(o.grp);
+  t.M = M;
+  return t;
+}
+
+// Tiles of <= 64 consecutive tokens of one batch row (for the tiled attention).
+std::vector<int32_t> make_tiles(const Toks& t) {
+  std::vector<int32_t> tiles;
+  int i = 0;
+  const int M = t.size();
+  while (i < M) {
+    int j = i + 1;
+    while (j < M && j - i < 64 && t.b[j] == t.b[i] && t.slot[j] == t.slot[j - 1] + 1) ++j;
+    tiles.push_back(i);
+    tiles.push_back(j - i);
+    i = j;
+  }
+  return tiles;
+}
+
+// Run one transformer stack over the token rows in X (residual stream, [M, d]).
+int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
+              const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv) {
+  const Sizes& s = h->sz;
+  const int M = tok.M;
+  if (M == 0) return MBP_OK;
+  float* Q = h->R<float>(h->rg.Q);
+  float* O = h->R<float>(h->rg.O);
+  float* Hid = h->R<float>(h->rg.Hid);
+  float* inv = h->R<float>(h->rg.inv);
+  float* part = h->R<float>(h->rg.part);
+  const float scale = h->cfg.attn_scale / std::sqrt((float)s.dh);
+  for (size_t l = 0; l < layers.size(); ++l) {
+    const BlockW& w = layers[l];
+    char* kc = reinterpret_cast<char*>(kv.k) + l * kv.layer_stride * s.es;
+    char* vc = reinterpret_cast<char*>(kv.v) + l * kv.layer_stride * s.es;
+    Linear qkv{};
+    qkv.X = X; qkv.ldx = s.d; qkv.M = M; qkv.K = s.d; qkv.N = 3 * s.d;
+    qkv.gain = w.attn_norm; qkv.eps = h->cfg.rms_eps;
+    qkv.mats.m[0] = w.wq; qkv.mats.m[1] = w.wk; qkv.mats.m[2] = w.wv;
+    qkv.mats.rows = s.d; qkv.mats.mode = MAT_QKV;
+    qkv.epi.kind = EPI_QKV; qkv.epi.Q = Q; qkv.epi.kc = kc; qkv.epi.vc = vc;
+    qkv.epi.b_stride = kv.b_stride; qkv.epi.cap = kv.cap; qkv.epi.H = s.H; qkv.epi.dh = s.dh; qkv.epi.d = s.d;
+    qkv.epi.rope = h->rope; qkv.epi.tok = tok; qkv.epi.kvt = h->cfg.kv_dtype;
+    HIPCK(h, launch_linear(qkv, h->wdt, inv, h->st));
+
+    Attn a{};
+    a.Q = Q; a.ldq = s.d; a.kc = kc; a.vc = vc; a.b_stride = kv.b_stride; a.cap = kv.cap;
+    a.H = s.H; a.dh = s.dh; a.tok = tok; a.grp_tab = grp_tab; a.scale = scale; a.O = O; a.ldo = s.d;
+    if (tiled) HIPCK(h, launch_attn_prefill(a, h->cfg.kv_dtype, tiles, ntiles, h->st));
+    else HIPCK(h, launch_attn_split(a, h->cfg.kv_dtype, max_kv, part, s.part_floats, h->st));
+
+    Linear o{};
+    o.X = O; o.ldx = s.d; o.M = M; o.K = s.d; o.N = s.d; o.gain = nullptr;
+    o.mats.m[0] = w.wo; o.mats.rows = s.d; o.mats.mode = MAT_SINGLE;
+    o.epi.kind = EPI_RESID; o.epi.Y = X; o.epi.ldy = s.d;
+    HIPCK(h, launch_linear(o, h->wdt, inv, h->st));
+
+    Linear gu{};
+    gu.X = X; gu.ldx = s.d; gu.M = M; gu.K = s.d; gu.N = 2 * s.dff;
+    gu.gain = w.ffn_norm; gu.eps = h->cfg.rms_eps;
+    gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
+    gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
+    HIPCK(h, launch_linear(gu, h->wdt, inv, h->st));
+
+    Linear dn{};
+    dn.X = Hid; dn.ldx = s.dff; dn.M = M; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
+    dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
+    dn.epi.kind = EPI_RESID; dn.epi.Y = X; dn.epi.ldy = s.d;
+    HIPCK(h, launch_linear(dn, h->wdt, inv, h->st));
+  }
+  return MBP_OK;
+}
+
+int32_t group_of(const Row& r, int32_t p) {  // L(p): boundaries at or before p
+  return (int32_t)(std::upper_bound(r.q.begin(), r.q.end(), p) - r.q.begin());
+}
+
+// Number of boundaries a row would have after appending bytes (capacity check).
+int32_t simulate_latents(const mbp_config& c, const Row& r, const uint8_t* add, int n) {
+  int32_t prev = r.q.empty() ? -1 : r.q.back();
+  int32_t K = (int32_t)r.q.size();
+  int32_t pos = (int32_t)r.x.size();
+  for (int i = 0; i < n; ++i, ++pos) {
+    if (add[i] == 0x20 || (c.max_patch > 0 && pos - prev >= c.max_patch)) {
+      prev = pos;
+      ++K;
+    }
+  }
+  return K;
+}
+
+void truncate_row(Row& r, int32_t T) {
+  if ((int32_t)r.x.size() <= T) return;
+  r.x.resize(T);
+  bool changed = false;
+  while (!r.q.empty() && r.q.back() >= T) {
+    r.q.pop_back();
+    changed = true;
+  }
+  if (changed) {
+    r.epoch++;
+    r.lm_rows = (int32_t)r.q.size() + 1;
+  }
+}
+
+// Commit add[b] (bytes) to every row: encoder, segmentation + pooling, LM module on
+// the segments that close, NT decoder; the last NT row of each row goes to h1.
+// Rows keep the NT outputs of the final chunk in X (token order).
+int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  for (int b = 0; b < h->batch; ++b) {
+    const Row& r = h->rows[b];
+    const int n = (int)add[b].size();
+    if (n == 0) continue;
+    if ((int64_t)r.x.size() + n > s.Tcap) return fail(h, MBP_ECAPACITY, "row would exceed max_ctx");
+    if (simulate_latents(c, r, add[b].data(), n) > c.max_latents)
+      return fail(h, MBP_ECAPACITY, "row would exceed max_latents");
+  }
+  struct Item {
+    int b, idx;
+  };
+  std::vector<Item> items;
+  for (int b = 0; b < h->batch; ++b)
+    for (int i = 0; i < (int)add[b].size(); ++i) items.push_back({b, i});
+  float* X = h->R<float>(h->rg.X);
+  float* Xl = h->R<float>(h->rg.Xl);
+  float* he = h->R<float>(h->rg.he);
+  float* lat_in = h->R<float>(h->rg.lat_in);
+  float* lat_out = h->R<float>(h->rg.lat_out);
+  float* h1 = h->R<float>(h->rg.h1);
+  size_t first = 0;
+  bool first_chunk = true;
+  while (first < items.size()) {
+    const size_t last = std::min(items.size(), first + (size_t)s.Mc);
+    if (!first_chunk) HIPCK(h, hipStreamSynchronize(h->st));  // plan buffer reuse
+    first_chunk = false;
+    Toks te, tl;
+    std::vector<int32_t> bytes, he_row, nt_src, lo_row, cnt, lat_row, last_src, last_dst;
+    int max_kv_e = 0, max_kv_l = 0;
+    std::vector<int> rows_in_chunk;
+    for (size_t it = first; it < last; ++it) {
+      const int b = items[it].b;
+      Row& r = h->rows[b];
+      if (rows_in_chunk.empty() || rows_in_chunk.back() != b) {
+        rows_in_chunk.push_back(b);
+        if (r.lm_rows == 0) {  // BOS latent of a fresh row
+          tl.push(b, 0, 0, 1, 0);
+          lo_row.push_back(0);
+          cnt.push_back(0);
+          lat_row.push_back(b * s.Kcap);
+          r.lm_rows = 1;
+          r.epoch++;
+          max_kv_l = std::max(max_kv_l, 1);
+        }
+      }
+      const uint8_t byte = add[b][items[it].idx];
+      const int32_t pos = (int32_t)r.x.size();
+      r.x.push_back(byte);
+      const int32_t prev = r.q.empty() ? -1 : r.q.back();
+      if (byte == 0x20 || (c.max_patch > 0 && pos - prev >= c.max_patch)) {
+        r.q.push_back(pos);
+        const int32_t j = (int32_t)r.q.size();
+        tl.push(b, j, j, j + 1, 0);
+        lo_row.push_back(b * s.Tcap + prev + 1);
+        cnt.push_back(pos - prev);
+        lat_row.push_back(b * s.Kcap + j);
+        r.lm_rows = j + 1;
+        r.epoch++;
+        max_kv_l = std::max(max_kv_l, j + 1);
+      }
+      const int32_t L = (int32_t)r.q.size();  // group of this byte
+      te.push(b, pos, pos, pos + 1, 0);
+      bytes.push_back(byte);
+      he_row.push_back(b * s.Tcap + pos);
+      nt_src.push_back(b * s.Kcap + L);
+      max_kv_e = std::max(max_kv_e, pos + 1);
+      if (it + 1 == last || items[it + 1].b != b) {
+        last_src.push_back(te.size() - 1);
+        last_dst.push_back(b);
+      }
+    }
+    const int Me = te.size(), Ml = tl.size();
+    const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
+    const bool tiled_l = Ml >= 16 * (int)rows_in_chunk.size();
+    std::vector<int32_t> tiles_e = make_tiles(te), tiles_l = make_tiles(tl);
+    Plan& p = h->plan[0];
+    p.buf.clear();
+    const TokOffs oe = add_toks(p, te), ol = add_toks(p, tl);
+    const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_nts = p.add(nt_src), o_lo = p.add(lo_row),
+                 o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_ls = p.add(last_src), o_ld = p.add(last_dst),
+                 o_te = p.add(tiles_e), o_tl = p.add(tiles_l);
+    int rc = upload(h, p);
+    if (rc) return rc;
+    const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
+
+    HIPCK(h, launch_embed(h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st));
+    rc = run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e);
+    if (rc) return rc;
+    HIPCK(h, launch_copy_rows(X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st));
+    if (Ml > 0) {
+      HIPCK(h, launch_pool(he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st));
+      HIPCK(h, launch_copy_rows(lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st));
+      rc = run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l);
+      if (rc) return rc;
+      HIPCK(h, launch_copy_rows(Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st));
+    }
+    HIPCK(h, launch_copy_rows(lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st));
+    rc = run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e);
+    if (rc) return rc;
+    HIPCK(h, launch_copy_rows(X, p.at(o_ls), nullptr, nullptr, h1, p.at(o_ld), s.d, (int)last_src.size(), h->st));
+    first = last;
+  }
+  return MBP_OK;
+}
+
+int check_ready(mbp_handle* h) {
+  if (!h) return MBP_EINVAL;
+  if (h->poisoned) return fail(h, MBP_ESTATE, "handle poisoned by an earlier HIP error; call mbp_reset");
+  return MBP_OK;
+}
+
+}  // namespace
+
+// ======================================================================= C ABI ==
+
+extern "C" int32_t mbp_weight_count(const mbp_config* cfg) {
+  if (!valid_cfg(cfg, nullptr)) return MBP_EINVAL;
+  return (int32_t)manifest(*cfg).size();
+}
+
+extern "C" int mbp_weight_info(const mbp_config* cfg, int32_t idx, char* name_buf, size_t name_len, int64_t* rows,
+                               int64_t* cols) {
+  if (!valid_cfg(cfg, nullptr)) return MBP_EINVAL;
+  const auto m = manifest(*cfg);
+  if (idx < 0 || idx >= (int32_t)m.size()) return MBP_EINVAL;
+  if (name_buf && name_len > 0) {
+    std::snprintf(name_buf, name_len, "%s", m[idx].name.c_str());
+  }
+  if (rows) *rows = m[idx].rows;
+  if (cols) *cols = m[idx].cols;
+  return MBP_OK;
+}
+
+extern "C" size_t mbp_workspace_bytes(const mbp_config* cfg) {
+  if (!valid_cfg(cfg, nullptr)) return 0;
+  return layout(*cfg).total;
+}
+
+extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int32_t n_weights, void* d_workspace,
+                        size_t ws_bytes, void* hip_stream, mbp_handle** out) {
+  if (!out) return MBP_EINVAL;
+  *out = nullptr;
+  if (!valid_cfg(cfg, nullptr)) return MBP_EINVAL;
+  const auto man = manifest(*cfg);
+  if (!d_weights || n_weights != (int32_t)man.size()) return MBP_EINVAL;
+  for (int i = 0; i < n_weights; ++i)
+    if (!d_weights[i]) return MBP_EINVAL;
+  if (!d_workspace || (reinterpret_cast<uintptr_t>(d_workspace) & 255)) return MBP_EINVAL;
+  const Regions rg = layout(*cfg);
+  if (ws_bytes < rg.total) return MBP_ECAPACITY;
+
+  mbp_handle* h = new (std::nothrow) mbp_handle();
+  if (!h) return MBP_EINVAL;
+  h->cfg = *cfg;
+  h->sz = sizes_of(*cfg);
+  h->rg = rg;
+  h->wdt = cfg->dtype == MBP_BF16 ? 1 : 0;
+  h->st = reinterpret_cast<hipStream_t>(hip_stream);
+  h->ws = reinterpret_cast<char*>(d_workspace);
+  const Sizes& s = h->sz;
+
+  // norm gains and BOS converted to float32 once
+  float* gains = h->R<float>(rg.gains);
+  int gi = 0;
+  auto gain = [&](int widx) -> const float* {
+    float* dst = gains + (size_t)gi * s.d;
+    ++gi;
+    hipError_t e = launch_to_f32(d_weights[widx], h->wdt, dst, s.d, h->st);
+    if (e != hipSuccess) h->poisoned = true;
+    return dst;
+  };
+  int w = 0;
+  h->emb = d_weights[w++];
+  h->bos32 = gain(w++);
+  auto block = [&]() {
+    BlockW b;
+    b.attn_norm = gain(w);
+    b.wq = d_weights[w + 1];
+    b.wk = d_weights[w + 2];
+    b.wv = d_weights[w + 3];
+    b.wo = d_weights[w + 4];
+    b.ffn_norm = gain(w + 5);
+    b.wg = d_weights[w + 6];
+    b.wu = d_weights[w + 7];
+    b.wd = d_weights[w + 8];
+    w += kParts;
+    return b;
+  };
+  for (int i = 0; i < cfg->n_enc; ++i) h->enc.push_back(block());
+  for (int i = 0; i < cfg->n_lm; ++i) h->lm.push_back(block());
+  for (int i = 0; i < cfg->n_nb; ++i) h->nt.push_back(block());
+  h->g_nt = gain(w++);
+  h->unembed = d_weights[w++];
+  if (cfg->head == MBP_HEAD_LCA) {
+    for (int i = 0; i < cfg->n_mb; ++i) h->mb.push_back(block());
+    h->g_mb = gain(w++);
+  } else {
+    h->g_mb = nullptr;
+    for (int i = 0; i < cfg->n_mb; ++i) {
+      MlpW m;
+      m.norm = gain(w);
+      m.wg = d_weights[w + 1];
+      m.wu = d_weights[w + 2];
+      m.wd = d_weights[w + 3];
+      w += 4;
+      h->mlp.push_back(m);
+    }
+  }
+  auto kvof = [&](size_t ko, size_t vo, int cap) {
+    KV k;
+    k.k = h->ws + ko;
+    k.v = h->ws + vo;
+    k.cap = cap;
+    k.b_stride = (int64_t)s.H * cap * s.dh;
+    k.layer_stride = (int64_t)s.B * k.b_stride;
+    return k;
+  };
+  h->kv_enc = kvof(rg.enc_k, rg.enc_v, s.Tcap);
+  h->kv_nt = kvof(rg.nt_k, rg.nt_v, s.Tcap);
+  h->kv_lm = kvof(rg.lm_k, rg.lm_v, s.Kcap);
+  h->kv_mb = kvof(rg.mb_k, rg.mb_v, s.Wcap);
+  h->rope = h->R<float2>(rg.rope);
+  const int npos = std::max(s.Tcap + s.nmax, s.Kcap) + 1;
+  hipError_t e = launch_rope_table(h->rope, npos, s.dh, (double)cfg->rope_base, h->st);
+  if (e != hipSuccess || h->poisoned) {
+    delete h;
+    return MBP_EHIP;
+  }
+  for (int i = 0; i < 2; ++i) {
+    h->plan[i].dev = h->R<int32_t>(i == 0 ? rg.plan0 : rg.plan1);
+    h->plan[i].cap = rg.plan_ints;
+  }
+  h->rows.assign(s.B, Row());
+  *out = h;
+  return MBP_OK;
+}
+
+extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t* h_lens, int32_t batch) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  const Sizes& s = h->sz;
+  if (!h_bytes || !h_lens || batch < 1 || batch > s.B) return fail(h, MBP_EINVAL, "bad prefill arguments");
+  std::vector<std::vector<uint8_t>> add(batch);
+  size_t off = 0;
+  for (int b = 0; b < batch; ++b) {
+    if (h_lens[b] < 1) return fail(h, MBP_EINVAL, "prompt lengths must be >= 1");
+    if (h_lens[b] > s.Tcap) return fail(h, MBP_ECAPACITY, "prompt exceeds max_ctx");
+    add[b].assign(h_bytes + off, h_bytes + off + h_lens[b]);
+    off += h_lens[b];
+    Row empty;
+    if (simulate_latents(h->cfg, empty, add[b].data(), h_lens[b]) > h->cfg.max_latents)
+      return fail(h, MBP_ECAPACITY, "prompt exceeds max_latents");
+  }
+  h->rows.assign(s.B, Row());
+  for (int b = 0; b < batch; ++b) h->rows[b].active = true;
+  h->batch = batch;
+  h->pending = false;
+  std::vector<int32_t> act(s.B, 0);
+  for (int b = 0; b < batch; ++b) act[b] = 1;
+  HIPCK(h, hipMemcpyAsync(h->R<int32_t>(h->rg.active), act.data(), s.B * 4, hipMemcpyHostToDevice, h->st));
+  HIPCK(h, hipStreamSynchronize(h->st));
+  return commit(h, add);
+}
+
+namespace {
+
+// Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
+// per-row greedy bytes / probabilities (and accept_len in threshold mode).
+int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len) {
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  const int B = h->batch;
+  Plan& p = h->plan[1];
+  p.buf.clear();
+  float* h1 = h->R<float>(h->rg.h1);
+  float* head_in = h->R<float>(h->rg.head_in);
+  float* logits = h->R<float>(h->rg.logits);
+  float* lat_in = h->R<float>(h->rg.lat_in);
+  float* lat_out = h->R<float>(h->rg.lat_out);
+  float* mbh = h->R<float>(h->rg.mbh);
+  float* Xm = h->R<float>(h->rg.X);
+  float* Hid = h->R<float>(h->rg.Hid);
+  float* inv = h->R<float>(h->rg.inv);
+
+  std::vector<int32_t> nt_src, nt_dst, mb_src, mb_dst;
+  for (int b = 0; b < B; ++b) {
+    nt_src.push_back(b);
+    nt_dst.push_back(b * n);
+  }
+  Toks tm;
+  std::vector<int32_t> zrow, wrow, grp_tab;
+  int max_w = 0;
+  const bool lca = c.head == MBP_HEAD_LCA;
+  if (lca && n >= 2) {
+    grp_tab.assign((size_t)B * s.Wcap, 0);
+    for (int b = 0; b < B; ++b) {
+      Row& r = h->rows[b];
+      const int32_t t = (int32_t)r.x.size() - 1;
+      const int32_t g = (int32_t)r.q.size();
+      const int32_t sw = g >= 1 ? (g - 1 == 0 ? 0 : r.q[g - 2]) : 0;
+      const int32_t W = t + n - 1 - sw;
+      if (W > s.Wcap) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
+      if (r.win_epoch != r.epoch || r.win_s != sw) {
+        r.win_epoch = r.epoch;
+        r.win_s = sw;
+        r.win_valid = 0;
+      }
+      for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
+        const int32_t pos = sw + w;
+        grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
+      }
+      for (int32_t w = r.win_valid; w < W; ++w) {
+        const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
+        tm.push(b, sw + w, w, w + 1, G);
+        zrow.push_back(b * s.Kcap + G);
+        wrow.push_back(b * s.Wcap + w);
+        max_w = std::max(max_w, w + 1);
+      }
+      r.win_valid = std::max(r.win_valid, W);
+      for (int m = 1; m < n; ++m) {
+        mb_src.push_back(b * s.Wcap + (t - sw) + m - 1);
+        mb_dst.push_back(b * n + m);
+      }
+    }
+  } else if (!lca && n >= 2) {
+    for (int b = 0; b < B; ++b)
+      for (int m = 1; m < n; ++m) {
+        mb_src.push_back(b * s.nmax + m);
+        mb_dst.push_back(b * n + m);
+      }
+  }
+  const TokOffs om = add_toks(p, tm);
+  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab), o_ns = p.add(nt_src),
+               o_nd = p.add(nt_dst), o_ms = p.add(mb_src), o_md = p.add(mb_dst);
+  int rc = upload(h, p);
+  if (rc) return rc;
+
+  if (lca && tm.size() > 0) {
+    const Tok tok = dev_tok(p, om, tm.size());
+    HIPCK(h, launch_copy_rows(lat_out, p.at(o_z), lat_in, p.at(o_z), Xm, nullptr, s.d, tm.size(), h->st));
+    rc = run_stack(h, h->mb, h->kv_mb, Xm, tok, p.at(o_g), false, nullptr, 0, max_w);
+    if (rc) return rc;
+    HIPCK(h, launch_copy_rows(Xm, nullptr, nullptr, nullptr, mbh, p.at(o_w), s.d, tm.size(), h->st));
+  }
+  float* mlp_out = h->R<float>(h->rg.mlp_out);
+  if (!lca && n >= 2) {
+    for (int m = 1; m < n; ++m) {
+      const MlpW& w = h->mlp[m - 1];
+      // residual base: mlp_out[b, m] = h1[b]
+      HIPCK(h, hipMemcpy2DAsync(mlp_out + (size_t)m * s.d, (size_t)s.nmax * s.d * 4, h1, (size_t)s.d * 4,
+                                (size_t)s.d * 4, B, hipMemcpyDeviceToDevice, h->st));
+      Linear gu{};
+      gu.X = h1; gu.ldx = s.d; gu.M = B; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.norm; gu.eps = c.rms_eps;
+      gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
+      gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
+      HIPCK(h, launch_linear(gu, h->wdt, inv, h->st));
+      Linear dn{};
+      dn.X = Hid; dn.ldx = s.dff; dn.M = B; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
+      dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
+      dn.epi.kind = EPI_RESID; dn.epi.Y = mlp_out + (size_t)m * s.d; dn.epi.ldy = s.nmax * s.d;
+      HIPCK(h, launch_linear(dn, h->wdt, inv, h->st));
+    }
+  }
+  // head inputs: RMSNorm * gain of each candidate row, then the shared unembedding
+  HIPCK(h, launch_norm_rows(h1, p.at(o_ns), h->g_nt, c.rms_eps, head_in, p.at(o_nd), s.d, B, h->st));
+  if (n >= 2) {
+    const float* src = lca ? mbh : mlp_out;
+    const float* g = lca ? h->g_mb : h->g_nt;
+    HIPCK(h, launch_norm_rows(src, p.at(o_ms), g, c.rms_eps, head_in, p.at(o_md), s.d, (int)mb_src.size(), h->st));
+  }
+  Linear un{};
+  un.X = head_in; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = nullptr;
+  un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
+  un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
+  HIPCK(h, launch_linear(un, h->wdt, inv, h->st));
+  HIPCK(h, launch_accept(logits, B, n, tau, h->R<int32_t>(h->rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
+                         h->st));
+  return MBP_OK;
+}
+
+}  // namespace
+
+extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, uint8_t* d_cand, float* d_prob,
+                               int32_t* d_accept_len) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  if (h->batch == 0) return fail(h, MBP_ESTATE, "no prefill");
+  if (h->pending) return fail(h, MBP_ESTATE, "the previous step was not accepted");
+  if (n < 1 || n > s.nmax) return fail(h, MBP_EINVAL, "n out of range");
+  if (c.head == MBP_HEAD_MLP && n - 1 > c.n_mb) return fail(h, MBP_EINVAL, "n - 1 exceeds the MLP heads");
+  if (!(tau >= 0.f && tau <= 1.f)) return fail(h, MBP_EINVAL, "tau must be in [0, 1]");
+  if (mode != MBP_ACCEPT_THRESHOLD && mode != MBP_ACCEPT_SELF_VERIFY) return fail(h, MBP_EINVAL, "bad mode");
+  if (!d_cand || !d_accept_len) return fail(h, MBP_EINVAL, "null output pointer");
+  if (mode == MBP_ACCEPT_SELF_VERIFY) {
+    for (int b = 0; b < h->batch; ++b)
+      if ((int64_t)h->rows[b].x.size() + n > s.Tcap) return fail(h, MBP_ECAPACITY, "verify drafts exceed max_ctx");
+  }
+  const int B = h->batch;
+  h->h_cand.assign((size_t)B * n, 0);
+  h->h_len.assign(B, 0);
+  if (mode == MBP_ACCEPT_THRESHOLD) {
+    rc = draft(h, n, tau, true, d_cand, d_prob, d_accept_len);
+    if (rc) return rc;
+    HIPCK(h, hipMemcpyAsync(h->h_cand.data(), d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+    HIPCK(h, hipMemcpyAsync(h->h_len.data(), d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+    h->pending = true;
+    h->last_n = n;
+    h->last_mode = mode;
+    return MBP_OK;
+  }
+  // self-verify: drafts, tentative commit of all n drafts, greedy check, rollback
+  rc = draft(h, n, tau, false, d_cand, d_prob, d_accept_len);
+  if (rc) return rc;
+  HIPCK(h, hipMemcpyAsync(h->h_cand.data(), d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipStreamSynchronize(h->st));
+  std::vector<std::vector<uint8_t>> add(B);
+  h->pre_len.assign(B, 0);
+  for (int b = 0; b < B; ++b) {
+    h->pre_len[b] = (int32_t)h->rows[b].x.size();
+    add[b].assign(h->h_cand.begin() + (size_t)b * n, h->h_cand.begin() + (size_t)(b + 1) * n);
+  }
+  // capacity of the tentative commit
+  for (int b = 0; b < B; ++b)
+    if (simulate_latents(c, h->rows[b], add[b].data(), n) > c.max_latents)
+      return fail(h, MBP_ECAPACITY, "verify drafts exceed max_latents");
+  float* h1 = h->R<float>(h->rg.h1);
+  float* h1s = h->R<float>(h->rg.h1_save);
+  HIPCK(h, hipMemcpyAsync(h1s, h1, (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
+  rc = commit(h, add);
+  if (rc) return rc;
+  // NT outputs of the B*n tentative rows are in X (row-major by batch row)
+  float* X = h->R<float>(h->rg.X);
+  float* head_in = h->R<float>(h->rg.head_in);
+  float* vlog = h->R<float>(h->rg.vlogits);
+  HIPCK(h, launch_norm_rows(X, nullptr, h->g_nt, c.rms_eps, head_in, nullptr, s.d, B * n, h->st));
+  Linear un{};
+  un.X = head_in; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = nullptr;
+  un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
+  un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
+  HIPCK(h, launch_linear(un, h->wdt, h->R<float>(h->rg.inv), h->st));
+  HIPCK(h, launch_verify(vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len, h->st));
+  HIPCK(h, hipMemcpyAsync(h->h_len.data(), d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipStreamSynchronize(h->st));
+  // roll back to the accepted prefix; h1 = NT row of the last accepted draft
+  Plan& p = h->plan[1];
+  p.buf.clear();
+  std::vector<int32_t> src, dst;
+  for (int b = 0; b < B; ++b) {
+    const int j = std::max(1, std::min(n, h->h_len[b]));
+    truncate_row(h->rows[b], h->pre_len[b] + j);
+    src.push_back(b * n + j - 1);
+    dst.push_back(b);
+  }
+  const size_t os = p.add(src), od = p.add(dst);
+  rc = upload(h, p);
+  if (rc) return rc;
+  HIPCK(h, launch_copy_rows(X, p.at(os), nullptr, nullptr, h1, p.at(od), s.d, B, h->st));
+  h->pending = true;
+  h->last_n = n;
+  h->last_mode = mode;
+  return MBP_OK;
+}
+
+extern "C" int mbp_last_accepted(mbp_handle* h, uint8_t* h_bytes, int32_t* h_lens) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  if (!h->pending) return fail(h, MBP_ESTATE, "no pending step");
+  if (!h_bytes || !h_lens) return fail(h, MBP_EINVAL, "null pointer");
+  HIPCK(h, hipStreamSynchronize(h->st));
+  const int n = h->last_n, mx = h->sz.nmax;
+  for (int b = 0; b < h->batch; ++b) {
+    h_lens[b] = h->h_len[b];
+    for (int m = 0; m < mx; ++m) h_bytes[b * mx + m] = m < n ? h->h_cand[(size_t)b * n + m] : 0;
+  }
+  return MBP_OK;
+}
+
+extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_t* h_override_len) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  if (h->batch == 0) return fail(h, MBP_ESTATE, "no prefill");
+  const Sizes& s = h->sz;
+  if (!h_override && !h->pending) return fail(h, MBP_ESTATE, "no pending step to accept");
+  if ((h_override == nullptr) != (h_override_len == nullptr)) return fail(h, MBP_EINVAL, "override needs both arrays");
+  HIPCK(h, hipStreamSynchronize(h->st));
+  const int B = h->batch;
+  std::vector<std::vector<uint8_t>> add(B);
+  if (h_override) {
+    for (int b = 0; b < B; ++b)
+      if (h_override_len[b] < 0 || h_override_len[b] > s.nmax) return fail(h, MBP_EINVAL, "override length out of range");
+    const bool rollback = h->pending && h->last_mode == MBP_ACCEPT_SELF_VERIFY;
+    for (int b = 0; b < B; ++b) {
+      add[b].assign(h_override + (size_t)b * s.nmax, h_override + (size_t)b * s.nmax + h_override_len[b]);
+      Row sim = h->rows[b];
+      if (rollback) truncate_row(sim, h->pre_len[b]);
+      if ((int64_t)sim.x.size() + (int64_t)add[b].size() > s.Tcap) return fail(h, MBP_ECAPACITY, "row would exceed max_ctx");
+      if (simulate_latents(h->cfg, sim, add[b].data(), (int)add[b].size()) > h->cfg.max_latents)
+        return fail(h, MBP_ECAPACITY, "row would exceed max_latents");
+    }
+    if (rollback) {
+      for (int b = 0; b < B; ++b) truncate_row(h->rows[b], h->pre_len[b]);
+      HIPCK(h, hipMemcpyAsync(h->R<float>(h->rg.h1), h->R<float>(h->rg.h1_save), (size_t)B * s.d * 4,
+                              hipMemcpyDeviceToDevice, h->st));
+    }
+  } else if (h->last_mode == MBP_ACCEPT_THRESHOLD) {
+    const int n = h->last_n;
+    for (int b = 0; b < B; ++b) {
+      const int k = std::max(0, std::min(n, h->h_len[b]));
+      add[b].assign(h->h_cand.begin() + (size_t)b * n, h->h_cand.begin() + (size_t)b * n + k);
+    }
+  }
+  h->pending = false;
+  return commit(h, add);
+}
+
+extern "C" int mbp_get_logits(mbp_handle* h, float* d_logits) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  if (!d_logits) return fail(h, MBP_EINVAL, "null pointer");
+  if (h->last_n == 0) return fail(h, MBP_ESTATE, "no step yet");
+  HIPCK(h, hipMemcpyAsync(d_logits, h->R<float>(h->rg.logits), (size_t)h->batch * h->last_n * 256 * 4,
+                          hipMemcpyDeviceToDevice, h->st));
+  return MBP_OK;
+}
+
+extern "C" int32_t mbp_row_length(const mbp_handle* h, int32_t row) {
+  if (!h || row < 0 || row >= h->batch) return MBP_EINVAL;
+  return (int32_t)h->rows[row].x.size();
+}
+
+extern "C" int mbp_reset(mbp_handle* h) {
+  if (!h) return MBP_EINVAL;
+  h->rows.assign(h->sz.B, Row());
+  h->batch = 0;
+  h->pending = false;
+  h->last_n = 0;
+  h->poisoned = false;
+  h->err.clear();
+  return MBP_OK;
+}
+
+extern "C" void mbp_destroy(mbp_handle* h) { delete h; }
+
+extern "C" const char* mbp_last_error(const mbp_handle* h) { return h ? h->err.c_str() : "null handle"; }

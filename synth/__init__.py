@@ -145,10 +145,10 @@ def head_manifest_start(cfg: ModelConfig) -> int:
 def round_bf16(a: np.ndarray) -> np.ndarray:
     """float32 -> nearest bfloat16 (ties to even), returned as float32 values."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16) << 16
-    return r.astype(np.uint32).view(np.float32).reshape(a.shape)
+    u = a.view(np.uint32)
+    # finite inputs: u + 0x8000 stays below 2**32, so uint32 arithmetic is exact
+    r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) & np.uint32(0xFFFF0000)
+    return r.view(np.float32).reshape(a.shape)
 
 
 def _is_gain(name: str) -> bool:

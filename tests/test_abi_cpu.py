@@ -1,0 +1,118 @@
+"""Host-only checks of the C ABI: the library loads, exports every function that
+include/mbp.h declares, validates configurations, and agrees with the seeded
+generator's weight manifest.  No compute call is made (no GPU here)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def mbp():
+    import paper_2608_15454_amd as m
+
+    if not os.path.exists(m.lib_path()):
+        pytest.fail("libmbp.so is not built; run __graft_entry__.build()")
+    m.lib()
+    return m
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "mbp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mbp_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_four_entry_points():
+    names = _declared_functions()
+    for n in ("mbp_init", "mbp_prefill", "mbp_decode_step", "mbp_accept"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol(mbp):
+    L = ctypes.CDLL(mbp.lib_path())
+    missing = [n for n in _declared_functions() if not hasattr(L, n)]
+    assert not missing, missing
+
+
+def _cfg(mbp, wl="lca_d1024_b1", **kw):
+    w = synth.WORKLOADS[wl]
+    args = dict(max_batch=w.batch, max_ctx=w.prompt_len + w.gen_len + 8, max_n=8)
+    args.update(kw)
+    return mbp.make_config(w.model, **args)
+
+
+@pytest.mark.parametrize("wl", list(synth.WORKLOADS))
+def test_manifest_matches_generator(mbp, wl):
+    cfg = _cfg(mbp, wl)
+    lib_man = mbp.weight_manifest(cfg)
+    gen_man = synth.manifest(synth.WORKLOADS[wl].model)
+    assert len(lib_man) == len(gen_man)
+    for (ln, (r, c)), (gn, shape) in zip(lib_man, gen_man):
+        assert ln == gn
+        assert r * c == int(__import__("numpy").prod(shape))
+        assert (r, c) == (shape[0], shape[1] if len(shape) > 1 else 1)
+
+
+def test_workspace_bytes_positive_and_monotone(mbp):
+    L = mbp.lib()
+    a = L.mbp_workspace_bytes(ctypes.byref(_cfg(mbp, max_ctx=1000)))
+    b = L.mbp_workspace_bytes(ctypes.byref(_cfg(mbp, max_ctx=2000)))
+    assert 0 < a < b
+
+
+@pytest.mark.parametrize("field,value", [
+    ("d_model", 0), ("n_heads", 3), ("d_ff", 100), ("n_lm", -1), ("head", 5), ("dtype", 7),
+    ("max_batch", 0), ("max_ctx", 1), ("max_n", 0), ("max_n", 9), ("max_patch", -1),
+    ("window_mode", 1), ("rope_base", 0.0),
+])
+def test_invalid_configs_rejected(mbp, field, value):
+    L = mbp.lib()
+    cfg = _cfg(mbp)
+    setattr(cfg, field, value)
+    assert L.mbp_workspace_bytes(ctypes.byref(cfg)) == 0
+    assert L.mbp_weight_count(ctypes.byref(cfg)) == mbp.EINVAL
+    h = ctypes.c_void_p()
+    ptrs = (ctypes.c_void_p * 1)(1)
+    assert L.mbp_init(ctypes.byref(cfg), ptrs, 1, ctypes.c_void_p(256), 1 << 40, None, ctypes.byref(h)) == mbp.EINVAL
+    assert not h.value
+
+
+def test_pure_space_rule_needs_max_window(mbp):
+    L = mbp.lib()
+    model = synth.WORKLOADS["tiny_f32"].model.replace(max_patch=0)
+    cfg = mbp.make_config(model, max_batch=1, max_ctx=100, max_n=4)
+    assert L.mbp_workspace_bytes(ctypes.byref(cfg)) == 0
+    cfg.max_window = 64
+    assert L.mbp_workspace_bytes(ctypes.byref(cfg)) > 0
+
+
+def test_init_argument_checks_before_any_device_work(mbp):
+    L = mbp.lib()
+    cfg = _cfg(mbp, "tiny_f32")
+    n = L.mbp_weight_count(ctypes.byref(cfg))
+    ptrs = (ctypes.c_void_p * n)(*([4096] * n))
+    h = ctypes.c_void_p()
+    ws = L.mbp_workspace_bytes(ctypes.byref(cfg))
+    # wrong weight count, null weight, misaligned workspace, small workspace, null out
+    assert L.mbp_init(ctypes.byref(cfg), ptrs, n - 1, ctypes.c_void_p(4096), ws, None, ctypes.byref(h)) == mbp.EINVAL
+    ptrs0 = (ctypes.c_void_p * n)(*([4096] * (n - 1) + [0]))
+    assert L.mbp_init(ctypes.byref(cfg), ptrs0, n, ctypes.c_void_p(4096), ws, None, ctypes.byref(h)) == mbp.EINVAL
+    assert L.mbp_init(ctypes.byref(cfg), ptrs, n, ctypes.c_void_p(4096 + 8), ws, None, ctypes.byref(h)) == mbp.EINVAL
+    assert L.mbp_init(ctypes.byref(cfg), ptrs, n, ctypes.c_void_p(4096), ws - 1, None, ctypes.byref(h)) == mbp.ECAPACITY
+    assert L.mbp_init(ctypes.byref(cfg), ptrs, n, ctypes.c_void_p(4096), ws, None, None) == mbp.EINVAL
+
+
+def test_null_handle_calls(mbp):
+    L = mbp.lib()
+    assert L.mbp_prefill(None, None, None, 1) == mbp.EINVAL
+    assert L.mbp_decode_step(None, 3, 0.5, 0, None, None, None) == mbp.EINVAL
+    assert L.mbp_accept(None, None, None) == mbp.EINVAL
+    assert L.mbp_reset(None) == mbp.EINVAL
+    assert L.mbp_row_length(None, 0) == mbp.EINVAL
+    L.mbp_destroy(None)

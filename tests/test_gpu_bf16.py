@@ -1,0 +1,92 @@
+"""GPU parity at the bfloat16 shapes: d=1024 / 16 heads and d=2048 / 32 heads, layers
+2/16/2/2 (LCA) or 2/16/2 + 3 MLP heads.  Tolerance 2e-2 absolute on logits (scaled
+by the logit gain where one is used to make acceptance ragged)."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_harness import (SELF_VERIFY, THRESHOLD, base_tol, forced_run, free_run, new_decoder)
+
+pytestmark = pytest.mark.gpu
+
+D1024 = synth.WORKLOADS["lca_d1024_b1"].model
+D1024_MLP = synth.WORKLOADS["mlp_d1024_b1"].model
+D2048 = synth.WORKLOADS["verify_d2048_b16"].model
+GAIN = 8.0
+
+
+@pytest.fixture(scope="module")
+def w1024():
+    raw = synth.make_weights(D1024, seed=0, logit_gain=GAIN)
+    return raw, oracle.to_float64(raw)
+
+
+@pytest.fixture(scope="module")
+def w1024_plain():
+    raw = synth.make_weights(D1024, seed=0)
+    return raw, oracle.to_float64(raw)
+
+
+@pytest.mark.timeout(600)
+def test_d1024_lca_random_init_forced(w1024_plain):
+    """The d=1024 LCA model as the workload specifies it (logit gain 1)."""
+    raw, W = w1024_plain
+    dec = new_decoder(D1024, raw, 1, 700)
+    st = forced_run(dec, W, D1024, [synth.make_prompt(0, 512)], 8, 3, 0.75, label="d1024")
+    print(st)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n", [3, 7])
+def test_d1024_lca_forced_ragged(w1024, n):
+    raw, W = w1024
+    dec = new_decoder(D1024, raw, 1, 700)
+    st = forced_run(dec, W, D1024, [synth.make_prompt(1, 400)], 10, n, 0.75, tol=base_tol(D1024) * GAIN,
+                    label=f"d1024 n={n}")
+    print(st)
+
+
+@pytest.mark.timeout(600)
+def test_d1024_mlp_forced():
+    raw = synth.make_weights(D1024_MLP, seed=0, logit_gain=GAIN)
+    W = oracle.to_float64(raw)
+    dec = new_decoder(D1024_MLP, raw, 1, 700)
+    st = forced_run(dec, W, D1024_MLP, [synth.make_prompt(2, 400)], 8, 4, 0.75, tol=base_tol(D1024) * GAIN,
+                    label="mlp")
+    print(st)
+
+
+@pytest.mark.timeout(900)
+def test_d1024_batched_ragged(w1024):
+    raw, W = w1024
+    lens = [64, 130, 257, 300]
+    prompts = [synth.make_prompt(10 + r, L) for r, L in enumerate(lens)]
+    dec = new_decoder(D1024, raw, len(lens), 600)
+    for tau in (0.5, 0.9):
+        st = forced_run(dec, W, D1024, prompts, 4, 5, tau, tol=base_tol(D1024) * GAIN, label=f"b4 tau={tau}")
+        print(st)
+
+
+@pytest.mark.timeout(900)
+def test_d1024_full_prompt_sampled_steps(w1024_plain):
+    """Full 4096-byte prompt of the batch-1 workload: the first steps compared."""
+    raw, W = w1024_plain
+    dec = new_decoder(D1024, raw, 1, 4096 + 64)
+    st = forced_run(dec, W, D1024, [synth.make_prompt(0, 4096)], 2, 3, 0.75, label="d1024 T=4096")
+    print(st)
+
+
+@pytest.mark.timeout(1200)
+def test_d2048_verify():
+    raw = synth.make_weights(D2048, seed=0, logit_gain=GAIN)
+    W = oracle.to_float64(raw)
+    prompts = [synth.make_prompt(20, 150), synth.make_prompt(21, 90)]
+    dec = new_decoder(D2048, raw, 2, 400)
+    st = forced_run(dec, W, D2048, prompts, 4, 7, 0.0, mode=SELF_VERIFY, tol=base_tol(D2048) * GAIN,
+                    label="d2048 verify")
+    print(st)
+    got_v, _ = free_run(dec, prompts, 24, 7, 0.0, mode=SELF_VERIFY)
+    got_g, _ = free_run(dec, prompts, 24, 1, 0.0)
+    for b in range(2):
+        np.testing.assert_array_equal(got_v[b], got_g[b])
