@@ -1,0 +1,202 @@
+#!/usr/bin/env python3
+"""MBP decode benchmark on one MI355X: accepted bytes/s of the multi-byte-prediction
+decode loop (decode step + commit of the accepted bytes), with the roofline of the
+dominant kernel and the CPU oracle timed beside it.
+
+Default workload: d=1024 bf16 LCA-MBP model (encoder 2, LM module 16, NT decoder 2,
+MB head 2 layers, 16 heads), batch 1, 4096-byte seeded Zipf prompt with space-
+delimited patches, n=3, tau=0.75, random N(0, 0.02) weights.
+
+Protocol: prefill + W warm-up steps, reset + prefill again (untimed), then exactly K
+timed steps.  A step is one decode_step (NT head, LCA window head, unembedding,
+softmax / top-1 / tau acceptance) plus one accept (encoder, segmentation and pooling,
+LM module when a segment closes, NT decoder) -- every stage of the hot path.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, vendor figure
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1024)
+    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--workload", default="lca_d1024_b1")
+    ap.add_argument("--n", type=int, default=None)
+    ap.add_argument("--tau", type=float, default=None)
+    ap.add_argument("--logit-gain", type=float, default=1.0)
+    ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for cpu_baseline (0 = skip)")
+    ap.add_argument("--no-timing-pass", action="store_true")
+    return ap.parse_args()
+
+
+def cpu_threads():
+    try:
+        from threadpoolctl import threadpool_info
+
+        info = [i for i in threadpool_info() if i.get("internal_api") in ("openblas", "mkl", "blis")]
+        if info:
+            return int(info[0]["num_threads"])
+    except Exception:
+        pass
+    return len(os.sched_getaffinity(0))
+
+
+def run_steps(dec, steps, n, tau, mode):
+    for _ in range(steps):
+        dec.decode_step(n, tau, mode)
+        dec.accept()
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU; the decode rows are independent and would shard "
+              "by batch row with no per-step exchange, but no multi-GPU run is provided.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_15454_amd import SELF_VERIFY, THRESHOLD, Decoder, make_config
+
+    wl = synth.WORKLOADS[args.workload]
+    model = wl.model
+    n = args.n or wl.n
+    tau = wl.tau if args.tau is None else args.tau
+    mode = SELF_VERIFY if wl.mode == "verify" else THRESHOLD
+    B, K, W = wl.batch, args.steps, args.warmup
+    log(f"[bench] workload {wl.name} B={B} prompt={wl.prompt_len} n={n} tau={tau} steps={K} warmup={W}")
+
+    t0 = time.time()
+    weights = synth.make_weights(model, seed=0, logit_gain=args.logit_gain)
+    prompts = [synth.make_prompt(r, wl.prompt_len) for r in range(B)]
+    max_ctx = wl.prompt_len + (max(K, W) + 2) * n + 16
+    dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max(n, 8)), weights)
+    log(f"[bench] weights + init {time.time() - t0:.1f}s")
+
+    t0 = time.time()
+    dec.prefill(prompts)
+    torch.cuda.synchronize()
+    log(f"[bench] prefill {time.time() - t0:.2f}s")
+    run_steps(dec, W, n, tau, mode)
+    torch.cuda.synchronize()
+    log("[bench] warm-up done")
+
+    # ---- timed pass
+    dec.reset()
+    dec.prefill(prompts)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    w0 = time.perf_counter()
+    run_steps(dec, K, n, tau, mode)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    gpu_ms = ev0.elapsed_time(ev1)
+    lens = [dec.row_length(b) for b in range(B)]
+    accepted = sum(L - wl.prompt_len for L in lens)
+    elapsed = max(wall, gpu_ms / 1000.0)
+    value = accepted / elapsed
+    log(f"[bench] timed: {K} steps {elapsed * 1000:.1f} ms, accepted {accepted} bytes, {value:.1f} B/s")
+
+    # ---- kernel timing pass (identical steps, launches bracketed by HIP events)
+    roofline, classes, timing_step_ms = None, {}, None
+    if not args.no_timing_pass:
+        dec.reset()
+        dec.prefill(prompts)
+        dec.set_timing(True)
+        w1 = time.perf_counter()
+        run_steps(dec, K, n, tau, mode)
+        torch.cuda.synchronize()
+        timing_step_ms = (time.perf_counter() - w1) * 1000.0 / K
+        classes = dec.read_timing()
+        dec.set_timing(False)
+        dom = max(classes, key=lambda c: classes[c][1])
+        launches, ms, nbytes = classes[dom]
+        achieved = nbytes / (ms / 1000.0) / 1e9 if ms > 0 else 0.0
+        roofline = {
+            "bound": "hbm", "kernel": f"{dom} (all launches of the class in the timed steps)",
+            "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+            "launches": launches, "avg_launch_us": round(ms * 1000.0 / max(launches, 1), 3),
+            "bytes_per_launch": round(nbytes / max(launches, 1)),
+        }
+        log(f"[bench] kernel classes: " + ", ".join(f"{k}: {v[0]} launches {v[1]:.1f} ms {v[2] / 1e9:.2f} GB"
+                                                     for k, v in classes.items()))
+
+    # ---- CPU oracle beside it
+    cpu = None
+    if args.cpu_steps > 0:
+        import oracle
+
+        W64 = oracle.to_float64(weights)
+        x = [int(b) for b in prompts[0]]
+        got = 0
+        c0 = time.perf_counter()
+        for _ in range(args.cpu_steps):
+            r = oracle.step(W64, model, x, n, tau) if mode == THRESHOLD else oracle.verify_step(W64, model, x, n)
+            acc = [int(c) for c in r["cand"][: r["k"]]]
+            x += acc
+            got += len(acc)
+        cs = time.perf_counter() - c0
+        cpu = {"value": round(got / cs, 4), "unit": "accepted bytes/s", "cores": cpu_threads(), "kind": "oracle",
+               "sample": f"{args.cpu_steps} steps of batch row 0 of the same workload (float64 full recompute, "
+                         f"{cs:.1f}s)"}
+        log(f"[bench] cpu oracle {got} bytes in {cs:.1f}s")
+
+    step_bytes = sum(v[2] for v in classes.values()) / K if classes else None
+    out = {
+        "metric": "accepted bytes/sec per MI355X (MBP decode)",
+        "value": round(value, 2),
+        "unit": "accepted bytes/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": round(elapsed * 1000.0 / K, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{wl.name}: d={model.d_model} heads={model.n_heads} layers enc/lm/nt/mb="
+                        f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb} head={model.head}, "
+                        f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
+            "batch": B, "prompt_len": wl.prompt_len, "n": n, "tau": tau, "mode": wl.mode,
+            "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32",
+            "logit_gain": args.logit_gain, "max_patch": model.max_patch,
+        },
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "steps_per_s": round(K / elapsed, 2),
+        "mean_accepted_per_step": round(accepted / (K * B), 4),
+        "step_algorithmic_bytes": round(step_bytes) if step_bytes else None,
+        "step_hbm_frac": round(step_bytes / (elapsed / K) / 1e9 / HBM_PEAK_GBS, 4) if step_bytes else None,
+        "timing_pass_ms_per_step": round(timing_step_ms, 4) if timing_step_ms else None,
+        "kernel_classes": {k: {"launches": v[0], "ms": round(v[1], 3), "GB": round(v[2] / 1e9, 4)}
+                           for k, v in classes.items()},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -163,6 +163,25 @@ int mbp_accept(mbp_handle *h, const uint8_t *h_override, const int32_t *h_overri
 /* Copy the last step's logits, float [batch, n, 256], into d_logits (device). */
 int mbp_get_logits(mbp_handle *h, float *d_logits);
 
+/* Kernel-class timing, for roofline reporting.  While enabled, every kernel launch
+ * the library enqueues is bracketed by a pair of HIP events on the handle's stream,
+ * and the algorithmic bytes the launch must move are recorded with it (weights and
+ * activations read and written by a linear layer; K/V rows read by attention).
+ * Classes: weight-streaming GEMV (<= 8 rows), tiled GEMM, attention, other. */
+enum { MBP_KCLASS_GEMV = 0, MBP_KCLASS_GEMM = 1, MBP_KCLASS_ATTN = 2, MBP_KCLASS_OTHER = 3,
+       MBP_KCLASS_COUNT = 4 };
+typedef struct {
+  int64_t launches;
+  double ms;     /* summed event-to-event durations */
+  double bytes;  /* summed algorithmic bytes */
+} mbp_kernel_time;
+
+/* Enable (on != 0) or disable launch timing; enabling clears the totals. */
+int mbp_set_timing(mbp_handle *h, int32_t on);
+
+/* Synchronize the stream and copy the totals since enabling into out[MBP_KCLASS_COUNT]. */
+int mbp_read_timing(mbp_handle *h, mbp_kernel_time *out);
+
 /* Current committed length of row r (host value), or a negative status. */
 int32_t mbp_row_length(const mbp_handle *h, int32_t row);
 

@@ -42,6 +42,12 @@ class MbpConfig(ctypes.Structure):
     ]
 
 
+class KernelTime(ctypes.Structure):
+    _fields_ = [("launches", ctypes.c_int64), ("ms", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
+KCLASSES = ("gemv", "gemm", "attention", "other")
+
 _lib = None
 
 
@@ -83,6 +89,10 @@ def lib():
     L.mbp_destroy.restype = None
     L.mbp_last_error.argtypes = [P]
     L.mbp_last_error.restype = ctypes.c_char_p
+    L.mbp_set_timing.argtypes = [P, ctypes.c_int32]
+    L.mbp_set_timing.restype = ctypes.c_int
+    L.mbp_read_timing.argtypes = [P, ctypes.POINTER(KernelTime)]
+    L.mbp_read_timing.restype = ctypes.c_int
     _lib = L
     return L
 
@@ -240,3 +250,12 @@ class Decoder:
     def reset(self):
         self._check(self.L.mbp_reset(self.h))
         self.batch = 0
+
+    def set_timing(self, on: bool):
+        self._check(self.L.mbp_set_timing(self.h, 1 if on else 0))
+
+    def read_timing(self):
+        """{class: (launches, ms, algorithmic bytes)} since timing was enabled."""
+        out = (KernelTime * len(KCLASSES))()
+        self._check(self.L.mbp_read_timing(self.h, out))
+        return {k: (out[i].launches, out[i].ms, out[i].bytes) for i, k in enumerate(KCLASSES)}

@@ -51,10 +51,16 @@ struct Epi {
   int32_t kvt;  // cache element type: 0 float32, 1 bfloat16, 2 float16
 };
 
+// y = W x over M rows.  Input row m is X + (xidx ? xidx[m] : m) * ldx.  With a gain,
+// the row is RMS-normalized and scaled by gain, or by gain2 when gain2 is set and
+// m % gain_period != 0.
 struct Linear {
-  const float* X;  // [M, ldx] float32 inputs
+  const float* X;
   int32_t ldx, M, K, N;
-  const float* gain;  // RMSNorm gain over K (float32) or nullptr for no norm
+  const int32_t* xidx;
+  const float* gain;
+  const float* gain2;
+  int32_t gain_period;
   float eps;
   Mats mats;
   Epi epi;
@@ -75,35 +81,49 @@ struct Attn {
   int32_t ldo;
 };
 
+// Optional events stamped by the first kernel's start and the last kernel's end of
+// one launch (hipExtLaunchKernelGGL), for kernel-accurate timing.
+struct Ev {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+
 // Launchers.  wdt: 0 = float32 weights, 1 = bfloat16.  kvt: cache element type,
 // 0 = float32, 1 = bfloat16, 2 = float16.
-hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms_scratch, hipStream_t st);
-// Split-KV attention; part: scratch of M*H*splits*(dh+2) floats; max_kv bounds kvlen.
-hipError_t launch_attn_split(const Attn& a, int kvt, int max_kv, float* part, int64_t part_floats,
-                             hipStream_t st);
+hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms_scratch, hipStream_t st, const Ev& ev = Ev());
+// Whether launch_linear takes the weight-streaming GEMV path for L.
+bool linear_is_gemv(const Linear& L, int wdt);
+// Split-KV attention (blocks of four waves over 256-key splits) followed by a merge
+// kernel when more than one split is needed.  part: scratch of part_floats floats.
+hipError_t launch_attn_decode(const Attn& a, int kvt, int max_kv, float* part, int64_t part_floats, hipStream_t st,
+                              const Ev& ev = Ev());
 // Tiled causal attention for long runs of consecutive slots of one batch row.
 // tiles: device int32 [ntiles*2] = (first token, count <= 64) with consecutive slots.
-hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int ntiles, hipStream_t st);
+hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int ntiles, hipStream_t st,
+                               const Ev& ev = Ev());
 
-hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st);
+hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st,
+                        const Ev& ev = Ev());
 // dst[dst_idx[i]] = src[src_idx[i]] (+ src2[src2_idx[i]]); null index arrays mean i.
 hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const float* src2,
                             const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d, int M,
-                            hipStream_t st);
+                            hipStream_t st, const Ev& ev = Ev());
 // Mean of cnt[i] rows of src starting at row lo[i] -> dst[dst_idx[i]]; cnt 0 copies bos.
 hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, const float* bos,
-                       float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st);
+                       float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());
 // out[dst_idx[i]] = RMSNorm(src[src_idx[i]]) * gain; null index arrays mean i.
 hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps,
-                            float* out, const int32_t* dst_idx, int d, int M, hipStream_t st);
+                            float* out, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());
 // Per batch row b < B: greedy byte and probability of each of the n logit rows,
 // then accept_len (threshold mode; write_len = 0 leaves accept_len untouched).
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active,
-                         uint8_t* cand, float* prob, int32_t* accept_len, int write_len, hipStream_t st);
+                         uint8_t* cand, float* prob, int32_t* accept_len, int write_len, hipStream_t st,
+                         const Ev& ev = Ev());
 // Greedy verification: NT logits of the n tentative rows vs the drafts.
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
-                         int32_t* accept_len, hipStream_t st);
+                         int32_t* accept_len, hipStream_t st, const Ev& ev = Ev());
 hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st);
 hipError_t launch_rope_table(float2* tab, int npos, int dh, double base, hipStream_t st);
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t st);
 
 }  // namespace mbp

@@ -1,13 +1,17 @@
 // gfx950 kernels of the MBP decode path.
 //
-// Numerics: weights and KV caches are stored in the model dtype (float32 or
-// bfloat16); every activation, residual stream, norm, softmax and accumulation is
-// float32.  Linear layers are weight-streaming GEMV kernels for <= 8 rows (each
-// weight byte is read from HBM once per launch, 16-byte loads per lane) and an
-// LDS-tiled kernel for more rows.
-#include "kernels.h"
+// Numerics: weights are stored in the model dtype (float32 or bfloat16), KV caches
+// in float32, bfloat16 or float16; every activation, residual stream, norm, softmax
+// and accumulation is float32.  Linear layers are weight-streaming GEMV kernels for
+// up to 64 rows (each weight byte is read from HBM once per launch with 16-byte
+// loads, issued before the activations are even loaded) and an LDS-tiled kernel for
+// more rows.  Decode attention splits the keys over blocks of four waves; the last
+// block of each (query, head) merges the splits.
+#include <hip/hip_ext.h>
 
 #include <math.h>
+
+#include "kernels.h"
 
 namespace mbp {
 namespace {
@@ -24,7 +28,7 @@ template <typename W>
 struct WT;
 
 template <>
-struct WT<uint16_t> {
+struct WT<uint16_t> {  // bfloat16 bits
   static constexpr int VEC = 8;  // elements per 16-byte load
   __device__ static float ld(const uint16_t* p, size_t i) { return bf2f(p[i]); }
   __device__ static void st(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
@@ -91,14 +95,23 @@ __device__ __forceinline__ const W* mat_row(const Mats& mt, int n, int K) {
   return reinterpret_cast<const W*>(mt.m[which]) + (size_t)r * K;
 }
 
+__device__ __forceinline__ const float* row_gain(const Linear& L, int m) {
+  return (L.gain2 != nullptr && (m % L.gain_period) != 0) ? L.gain2 : L.gain;
+}
+
 __device__ __forceinline__ void epi_single(const Epi& e, int i, int n, float v) {
   float* y = e.Y + (size_t)i * e.ldy + n;
   if (e.kind == EPI_STORE) *y = v;
   else *y += v;
 }
 
+template <typename C>
+__device__ __forceinline__ void cache_store2(void* cache, size_t off, float a0, float a1) {
+  WT<C>::st(reinterpret_cast<C*>(cache), off, a0);
+  WT<C>::st(reinterpret_cast<C*>(cache), off + 1, a1);
+}
+
 // Pair epilogue for columns (n, n+1), n even.
-template <typename W>
 __device__ __forceinline__ void epi_pair(const Epi& e, int i, int n, float a0, float a1) {
   if (e.kind == EPI_SWIGLU) {
     e.Y[(size_t)i * e.ldy + (n >> 1)] = silu(a0) * a1;
@@ -121,129 +134,144 @@ __device__ __forceinline__ void epi_pair(const Epi& e, int i, int n, float a0, f
   }
   void* cache = which == 1 ? e.kc : e.vc;
   const size_t off = (size_t)e.tok.b[i] * e.b_stride + ((size_t)h * e.cap + e.tok.slot[i]) * e.dh + ee;
-  if (e.kvt == 2) {
-    WT<_Float16>::st(reinterpret_cast<_Float16*>(cache), off, a0);
-    WT<_Float16>::st(reinterpret_cast<_Float16*>(cache), off + 1, a1);
-  } else if (e.kvt == 1) {
-    WT<uint16_t>::st(reinterpret_cast<uint16_t*>(cache), off, a0);
-    WT<uint16_t>::st(reinterpret_cast<uint16_t*>(cache), off + 1, a1);
+  if (e.kvt == 2) cache_store2<_Float16>(cache, off, a0, a1);
+  else if (e.kvt == 1) cache_store2<uint16_t>(cache, off, a0, a1);
+  else cache_store2<float>(cache, off, a0, a1);
+}
+
+// Launch with optional start/stop events stamped by the kernel's own execution.
+template <typename Kern, typename... Args>
+hipError_t klaunch(Kern kernel, dim3 grid, dim3 block, size_t shm, hipStream_t st, hipEvent_t e0, hipEvent_t e1,
+                   Args... args) {
+  if (e0 != nullptr || e1 != nullptr) {
+    hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)shm, st, e0, e1, 0, args...);
   } else {
-    WT<float>::st(reinterpret_cast<float*>(cache), off, a0);
-    WT<float>::st(reinterpret_cast<float*>(cache), off + 1, a1);
+    hipLaunchKernelGGL(kernel, grid, block, shm, st, args...);
   }
+  return hipGetLastError();
 }
 
 // ------------------------------------------------------------------ GEMV ------
-// Up to MR rows of X (normalized in LDS) against weight rows streamed once from
-// HBM.  Wave w of block g owns output rows [(4g+w)*R, +R).  Lane l reads 16 bytes
-// at column chunk c*64*VEC + l*VEC of each row, U chunks in flight.
-template <typename W, int MR, int R>
-__global__ __launch_bounds__(256) void gemv_kernel(Linear L) {
-  extern __shared__ float xs[];  // [MR][K]
-  __shared__ float red[4];
-  constexpr int VEC = WT<W>::VEC;
-  constexpr int U = (R * MR >= 16) ? 2 : 4;
-  const int K = L.K, M = L.M;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-
-  for (int m = 0; m < MR; ++m) {
-    float ss = 0.f;
-    if (m < M) {
-      const float* xr = L.X + (size_t)m * L.ldx;
-      for (int k = tid * 4; k < K; k += 1024) {
-        const float4 v = *reinterpret_cast<const float4*>(xr + k);
-        *reinterpret_cast<float4*>(xs + m * K + k) = v;
-        ss += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-      }
-      if (L.gain != nullptr) {
-        ss = wave_sum(ss);
-        if (lane == 0) red[wave] = ss;
-        __syncthreads();
-        const float inv = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)K + L.eps);
-        __syncthreads();
-        for (int k = tid * 4; k < K; k += 1024) {
+// Wave total of V = 2^k values per lane by recursive halving (V - 1 exchanges
+// instead of 6V): afterwards lane l holds the total of value l / (64 / V).
+template <int V>
+__device__ __forceinline__ float multi_sum(float (&v)[V]) {
+  const int lane = threadIdx.x & 63;
 #pragma unroll
-          for (int j = 0; j < 4; ++j) xs[m * K + k + j] *= inv * L.gain[k + j];
-        }
-      }
-    } else {
-      for (int k = tid * 4; k < K; k += 1024) *reinterpret_cast<float4*>(xs + m * K + k) = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int n = V, o = 32; n > 1; n >>= 1, o >>= 1) {
+    const bool upper = (lane & o) != 0;
+#pragma unroll
+    for (int j = 0; j < n / 2; ++j) {
+      // the lower lane keeps value j, the upper lane value j + n/2; selecting between
+      // the two finished sums (not between array slots) keeps v[] in registers
+      const float lo = v[j], hi = v[j + n / 2];
+      const float lo_sum = lo + __shfl_xor(lo, o);
+      const float hi_sum = hi + __shfl_xor(hi, o);
+      v[j] = upper ? hi_sum : lo_sum;
     }
   }
-  __syncthreads();
+  float t = v[0];
+#pragma unroll
+  for (int o = 32 / V; o > 0; o >>= 1) t += __shfl_xor(t, o);
+  return t;
+}
 
+// Wave w of block g owns output rows [(4g+w)*R, +R) and loads its whole R x K weight
+// slice into registers first (lane l holds 16 bytes of every 64*VEC-column chunk),
+// so each weight byte leaves HBM once.  Input rows are processed MR at a time; each
+// lane reads only the slice of the row that matches its weights.  The RMSNorm scale
+// is a per-row scalar, so it is applied after the dot product: the sum of squares
+// accumulates in the same pass.  No LDS and no block-level synchronization.
+template <typename W, int MR, int R, int KC>
+__global__ __launch_bounds__(256) void gemv_kernel(Linear L) {
+  constexpr int VEC = WT<W>::VEC;
+  constexpr int K = KC * 64 * VEC;
+  constexpr int V = R * MR;     // accumulators per lane
+  constexpr int LPV = 64 / V;   // lanes per reduced value
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int n0 = (blockIdx.x * 4 + wave) * R;
   if (n0 >= L.N) return;
-  const W* rows[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) rows[r] = mat_row<W>(L.mats, n0 + r, K);
-  float acc[R][MR];
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int m = 0; m < MR; ++m) acc[r][m] = 0.f;
 
-  const int KC = K / (64 * VEC);
-  for (int c = 0; c < KC; c += U) {
-    uint4 wv[U][R];
+  uint4 wv[R][KC];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-      if (c + u < KC)
+  for (int r = 0; r < R; ++r) {
+    const W* row = mat_row<W>(L.mats, n0 + r, K);
 #pragma unroll
-        for (int r = 0; r < R; ++r)
-          wv[u][r] = *reinterpret_cast<const uint4*>(rows[r] + (size_t)(c + u) * 64 * VEC + lane * VEC);
+    for (int c = 0; c < KC; ++c) wv[r][c] = *reinterpret_cast<const uint4*>(row + c * 64 * VEC + lane * VEC);
+  }
+  const bool norm = L.gain != nullptr;
+
+  for (int m0 = 0; m0 < L.M; m0 += MR) {
+    const float* xrow[MR];
+    const float* grow[MR];
+    bool live[MR];
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (c + u < KC) {
-        const int k0 = (c + u) * 64 * VEC + lane * VEC;
-        float wf[R][VEC];
+    for (int m = 0; m < MR; ++m) {
+      const int mm = m0 + m;
+      live[m] = mm < L.M;
+      xrow[m] = L.X + (size_t)(live[m] ? (L.xidx ? L.xidx[mm] : mm) : 0) * L.ldx;
+      grow[m] = norm ? row_gain(L, live[m] ? mm : 0) : nullptr;
+    }
+    float acc[V], ss[MR];
 #pragma unroll
-        for (int r = 0; r < R; ++r) WT<W>::unpack(wv[u][r], wf[r]);
+    for (int j = 0; j < V; ++j) acc[j] = 0.f;
 #pragma unroll
-        for (int m = 0; m < MR; ++m) {
-          float xv[VEC];
+    for (int m = 0; m < MR; ++m) ss[m] = 0.f;
+#pragma unroll
+    for (int c = 0; c < KC; ++c) {
+      const int k0 = c * 64 * VEC + lane * VEC;
+      float wf[R][VEC];
+#pragma unroll
+      for (int r = 0; r < R; ++r) WT<W>::unpack(wv[r][c], wf[r]);
+#pragma unroll
+      for (int m = 0; m < MR; ++m) {
+        float xv[VEC];
+#pragma unroll
+        for (int v = 0; v < VEC; v += 4) {
+          const float4 t = live[m] ? *reinterpret_cast<const float4*>(xrow[m] + k0 + v) : make_float4(0.f, 0.f, 0.f, 0.f);
+          xv[v] = t.x; xv[v + 1] = t.y; xv[v + 2] = t.z; xv[v + 3] = t.w;
+        }
+        if (norm) {
 #pragma unroll
           for (int v = 0; v < VEC; v += 4) {
-            const float4 t = *reinterpret_cast<const float4*>(xs + m * K + k0 + v);
-            xv[v] = t.x; xv[v + 1] = t.y; xv[v + 2] = t.z; xv[v + 3] = t.w;
+            const float4 g = *reinterpret_cast<const float4*>(grow[m] + k0 + v);
+            ss[m] += xv[v] * xv[v] + xv[v + 1] * xv[v + 1] + xv[v + 2] * xv[v + 2] + xv[v + 3] * xv[v + 3];
+            xv[v] *= g.x; xv[v + 1] *= g.y; xv[v + 2] *= g.z; xv[v + 3] *= g.w;
           }
-#pragma unroll
-          for (int r = 0; r < R; ++r)
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) acc[r][m] += wf[r][v] * xv[v];
         }
+#pragma unroll
+        for (int r = 0; r < R; ++r)
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) acc[r * MR + m] += wf[r][v] * xv[v];
       }
     }
-  }
-#pragma unroll
-  for (int r = 0; r < R; ++r)
-#pragma unroll
-    for (int m = 0; m < MR; ++m) acc[r][m] = wave_sum(acc[r][m]);
-
-  if (L.epi.kind == EPI_STORE || L.epi.kind == EPI_RESID) {
-#pragma unroll
-    for (int r = 0; r < R; ++r)
-#pragma unroll
-      for (int m = 0; m < MR; ++m)
-        if (lane == r * MR + m && m < M) epi_single(L.epi, m, n0 + r, acc[r][m]);
-  } else {
-#pragma unroll
-    for (int p = 0; p < R / 2; ++p)
-#pragma unroll
-      for (int m = 0; m < MR; ++m)
-        if (lane == p * MR + m && m < M) epi_pair<W>(L.epi, m, n0 + 2 * p, acc[2 * p][m], acc[2 * p + 1][m]);
+    float val = multi_sum<V>(acc);  // value (r, m) = l / LPV, r = idx / MR, m = idx % MR
+    const int idx = lane / LPV;
+    const int r = idx / MR, m = idx % MR;
+    if (norm) {
+      const float sst = multi_sum<MR>(ss);  // row (l / (64 / MR)) of the group
+      const float tot = __shfl(sst, m * (64 / MR));
+      val *= 1.0f / sqrtf(tot / (float)K + L.eps);
+    }
+    const bool owner = (lane % LPV) == 0 && m0 + m < L.M;
+    if (L.epi.kind == EPI_STORE || L.epi.kind == EPI_RESID) {
+      if (owner) epi_single(L.epi, m0 + m, n0 + r, val);
+    } else if constexpr (R % 2 == 0) {
+      const float partner = __shfl_down(val, MR * LPV);  // value (r + 1, m)
+      if (owner && (r % 2) == 0) epi_pair(L.epi, m0 + m, n0 + r, val, partner);
+    }
   }
 }
 
 // ------------------------------------------------------------------ GEMM ------
-__global__ __launch_bounds__(256) void rms_kernel(const float* X, int ldx, int M, int K, float eps, float* inv) {
+__global__ __launch_bounds__(256) void rms_kernel(Linear L, float* inv) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
-  if (row >= M) return;
-  const float* x = X + (size_t)row * ldx;
+  if (row >= L.M) return;
+  const float* x = L.X + (size_t)(L.xidx ? L.xidx[row] : row) * L.ldx;
   float ss = 0.f;
-  for (int k = lane; k < K; k += 64) ss += x[k] * x[k];
+  for (int k = lane; k < L.K; k += 64) ss += x[k] * x[k];
   ss = wave_sum(ss);
-  if (lane == 0) inv[row] = 1.0f / sqrtf(ss / (float)K + eps);
+  if (lane == 0) inv[row] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
 }
 
 // 64x64 output tile per block, K step 16, 4x4 outputs per thread, float32 FMA.
@@ -256,9 +284,11 @@ __global__ __launch_bounds__(256) void gemm_kernel(Linear L, const float* inv_rm
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   const int lr = tid >> 2, lk = (tid & 3) * 4;
   const W* brow = mat_row<W>(L.mats, n0 + lr, L.K);
-  const bool arow_ok = (m0 + lr) < L.M;
-  const float* arow = L.X + (size_t)(m0 + lr) * L.ldx;
-  const float ascale = (L.gain != nullptr && arow_ok) ? inv_rms[m0 + lr] : 1.0f;
+  const int am = m0 + lr;
+  const bool arow_ok = am < L.M;
+  const float* arow = L.X + (size_t)(arow_ok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx;
+  const float ascale = (L.gain != nullptr && arow_ok) ? inv_rms[am] : 1.0f;
+  const float* ag = (L.gain != nullptr && arow_ok) ? row_gain(L, am) : nullptr;
   float acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -270,9 +300,9 @@ __global__ __launch_bounds__(256) void gemm_kernel(Linear L, const float* inv_rm
     if (arow_ok) {
       const float4 v = *reinterpret_cast<const float4*>(arow + k0 + lk);
       a[0] = v.x; a[1] = v.y; a[2] = v.z; a[3] = v.w;
-      if (L.gain != nullptr) {
+      if (ag != nullptr) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) a[j] *= ascale * L.gain[k0 + lk + j];
+        for (int j = 0; j < 4; ++j) a[j] *= ascale * ag[k0 + lk + j];
       }
     }
 #pragma unroll
@@ -301,8 +331,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(Linear L, const float* inv_rm
     if (m >= L.M) continue;
     const int n = n0 + tx * 4;
     if (pair) {
-      epi_pair<W>(L.epi, m, n, acc[i][0], acc[i][1]);
-      epi_pair<W>(L.epi, m, n + 2, acc[i][2], acc[i][3]);
+      epi_pair(L.epi, m, n, acc[i][0], acc[i][1]);
+      epi_pair(L.epi, m, n + 2, acc[i][2], acc[i][3]);
     } else {
 #pragma unroll
       for (int j = 0; j < 4; ++j) epi_single(L.epi, m, n + j, acc[i][j]);
@@ -311,95 +341,165 @@ __global__ __launch_bounds__(256) void gemm_kernel(Linear L, const float* inv_rm
 }
 
 // ------------------------------------------------------------- attention ------
-// Split-KV attention: block (split s, head h, query i), one wave.  Lane l scores
-// key j0+l of each 64-key step; the value pass has lane e accumulate dimension e.
-// Online softmax within the split; the combine kernel merges the splits.
+// Decode attention: block (split s, head h, query i) of four waves covers keys
+// [s*chunk, (s+1)*chunk); wave w takes 64-key steps starting at s*chunk + 64w.  G
+// lanes share one key row (one 16-byte load each), so one load instruction covers
+// 64/G keys; every lane keeps the probabilities of its own keys and accumulates
+// their value rows for its VEC dimensions, so no probability leaves the lane.  With
+// S > 1 splits each block writes (max, sum, unnormalized output) and
+// attn_merge_kernel combines them; merging in the last block instead would need an
+// agent-scope fence in every block, which measures slower than the second launch.
+constexpr int kMaxSplits = 128;
+
 template <typename KV, int DH>
-__global__ __launch_bounds__(64) void attn_split_kernel(Attn a, int chunk, int S, float* part) {
+__global__ __launch_bounds__(256) void attn_decode_kernel(Attn a, int chunk, int S, float* part) {
   constexpr int VEC = WT<KV>::VEC;
-  const int s = blockIdx.x, h = blockIdx.y, i = blockIdx.z, lane = threadIdx.x;
+  constexpr int G = DH / VEC;    // lanes per key row
+  constexpr int KPR = 64 / G;    // keys per load round
+  constexpr int NR = 64 / KPR;   // rounds per 64-key step
+  __shared__ float wm[4], wl[4], wo[4][DH];
+  const int s = blockIdx.x, h = blockIdx.y, i = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = lane % G, g = lane / G;
   const int b = a.tok.b[i], kvlen = a.tok.kvlen[i];
   const int lo = s * chunk, hi = min(lo + chunk, kvlen);
-  __shared__ float qs[DH];
-  __shared__ float ps[64];
-  if (lane < DH) qs[lane] = a.Q[(size_t)i * a.ldq + h * DH + lane] * a.scale;
-  __syncthreads();
-  float q[DH];
+
+  float q[VEC];
+  {
+    const float* qp = a.Q + (size_t)i * a.ldq + h * DH + c * VEC;
 #pragma unroll
-  for (int e = 0; e < DH; ++e) q[e] = qs[e];
+    for (int v = 0; v < VEC; ++v) q[v] = qp[v] * a.scale;
+  }
   const int gq = a.grp_tab != nullptr ? a.tok.grp[i] : 0;
-  const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH;
+  const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH + c * VEC;
   const KV* kb = reinterpret_cast<const KV*>(a.kc) + base;
   const KV* vb = reinterpret_cast<const KV*>(a.vc) + base;
   const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
-  float m_run = -INFINITY, l_run = 0.f, o = 0.f;
-  for (int j0 = lo; j0 < hi; j0 += 64) {
-    const int j = j0 + lane;
-    bool vis = j < hi;
-    if (vis && gt != nullptr) {
-      const int gj = gt[j];
-      vis = (gj == gq) || (gj == gq - 1);
+
+  float m_run = -INFINITY, l_run = 0.f;
+  float o[VEC];
+#pragma unroll
+  for (int v = 0; v < VEC; ++v) o[v] = 0.f;
+
+  for (int j0 = lo + wave * 64; j0 < hi; j0 += 256) {
+    uint4 kr[NR], vr[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int j = j0 + r * KPR + g;
+      if (j < hi) {
+        kr[r] = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH);
+        vr[r] = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH);
+      } else {
+        kr[r] = make_uint4(0u, 0u, 0u, 0u);
+        vr[r] = make_uint4(0u, 0u, 0u, 0u);
+      }
     }
-    float sc = -INFINITY;
-    if (vis) {
-      const KV* kr = kb + (size_t)j * DH;
+    float sc[NR];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      float f[VEC];
+      WT<KV>::unpack(kr[r], f);
       float dot = 0.f;
 #pragma unroll
-      for (int e = 0; e < DH; e += VEC) {
-        float f[VEC];
-        WT<KV>::unpack(*reinterpret_cast<const uint4*>(kr + e), f);
+      for (int v = 0; v < VEC; ++v) dot += q[v] * f[v];
 #pragma unroll
-        for (int v = 0; v < VEC; ++v) dot += q[e + v] * f[v];
+      for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
+      const int j = j0 + r * KPR + g;
+      bool vis = j < hi;
+      if (vis && gt != nullptr) {
+        const int gj = gt[j];
+        vis = (gj == gq) || (gj == gq - 1);
       }
-      sc = dot;
+      sc[r] = vis ? dot : -INFINITY;
+      mx = fmaxf(mx, sc[r]);
     }
-    const float mx = wave_max(sc);
+#pragma unroll
+    for (int off = G; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
     if (mx == -INFINITY) continue;  // wave-uniform: nothing visible in this step
     const float m_new = fmaxf(m_run, mx);
     const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
-    const float p = (sc == -INFINITY) ? 0.f : expf(sc - m_new);
-    l_run = l_run * alpha + wave_sum(p);
-    ps[lane] = p;
-    __syncthreads();
-    o *= alpha;
-    const int jn = min(64, hi - j0);
-    if (lane < DH) {
-      for (int jj = 0; jj < jn; ++jj) o += ps[jj] * WT<KV>::ld(vb, (size_t)(j0 + jj) * DH + lane);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) o[v] *= alpha;
+    float ps = 0.f;
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const float p = (sc[r] == -INFINITY) ? 0.f : expf(sc[r] - m_new);
+      ps += p;
+      float f[VEC];
+      WT<KV>::unpack(vr[r], f);
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) o[v] += p * f[v];
     }
+    l_run = l_run * alpha + ps;
     m_run = m_new;
-    __syncthreads();
   }
-  if (S == 1) {
-    if (lane < DH) a.O[(size_t)i * a.ldo + h * DH + lane] = (l_run > 0.f) ? o / l_run : 0.f;
-  } else {
-    float* po = part + (((size_t)i * a.H + h) * S + s) * (DH + 2);
-    if (lane < DH) po[lane] = o;
-    if (lane == 0) {
-      po[DH] = m_run;
-      po[DH + 1] = l_run;
+  // sum over the lanes that share a dimension chunk (different keys, same m_run)
+#pragma unroll
+  for (int off = G; off < 64; off <<= 1) {
+    l_run += __shfl_xor(l_run, off);
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) o[v] += __shfl_xor(o[v], off);
+  }
+  if (lane < G) {
+#pragma unroll
+    for (int v = 0; v < VEC; ++v) wo[wave][c * VEC + v] = o[v];
+  }
+  if (lane == 0) {
+    wm[wave] = m_run;
+    wl[wave] = l_run;
+  }
+  __syncthreads();
+  const float mb = fmaxf(fmaxf(wm[0], wm[1]), fmaxf(wm[2], wm[3]));
+  if (tid < DH) {
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (wm[w] != -INFINITY) {
+        const float e = expf(wm[w] - mb);
+        num += e * wo[w][tid];
+        den += e * wl[w];
+      }
+    }
+    if (S == 1) {
+      a.O[(size_t)i * a.ldo + h * DH + tid] = den > 0.f ? num / den : 0.f;
+    } else {
+      float* pp = part + (((size_t)i * a.H + h) * S + s) * (DH + 2);
+      pp[tid] = num;
+      if (tid == 0) {
+        pp[DH] = mb;
+        pp[DH + 1] = den;
+      }
     }
   }
 }
 
+// Merge of the S split partials of each (query, head) when it is not done inside the
+// decode kernel.
 template <int DH>
-__global__ __launch_bounds__(64) void attn_combine_kernel(const float* part, int S, int H, float* O, int ldo) {
-  const int h = blockIdx.x, i = blockIdx.y, lane = threadIdx.x;
+__global__ __launch_bounds__(256) void attn_merge_kernel(const float* part, int S, int H, float* O, int ldo) {
+  __shared__ float sm[kMaxSplits], sw[kMaxSplits];
+  const int h = blockIdx.x, i = blockIdx.y, tid = threadIdx.x;
   const float* pb = part + ((size_t)i * H + h) * S * (DH + 2);
-  float mx = -INFINITY;
-  for (int s = 0; s < S; ++s) mx = fmaxf(mx, pb[s * (DH + 2) + DH]);
-  float num = 0.f, den = 0.f;
-  for (int s = 0; s < S; ++s) {
-    const float ms = pb[s * (DH + 2) + DH];
-    if (ms == -INFINITY) continue;
-    const float w = expf(ms - mx);
-    den += w * pb[s * (DH + 2) + DH + 1];
-    if (lane < DH) num += w * pb[s * (DH + 2) + lane];
+  for (int t = tid; t < S; t += 256) sm[t] = pb[(size_t)t * (DH + 2) + DH];
+  __syncthreads();
+  float mg = -INFINITY;
+  for (int t = 0; t < S; ++t) mg = fmaxf(mg, sm[t]);
+  for (int t = tid; t < S; t += 256) sw[t] = (sm[t] == -INFINITY) ? 0.f : expf(sm[t] - mg);
+  __syncthreads();
+  if (tid < DH) {
+    float num = 0.f, den = 0.f;
+    for (int t = 0; t < S; ++t) {
+      const float w = sw[t];
+      if (w != 0.f) {
+        num += w * pb[(size_t)t * (DH + 2) + tid];
+        den += w * pb[(size_t)t * (DH + 2) + DH + 1];
+      }
+    }
+    O[(size_t)i * ldo + h * DH + tid] = den > 0.f ? num / den : 0.f;
   }
-  if (lane < DH) O[(size_t)i * ldo + h * DH + lane] = (den > 0.f) ? num / den : 0.f;
 }
 
-// Tiled causal attention: block (tile, head) with up to 64 queries of one batch row
-// at consecutive slots; 64-key blocks staged in LDS; 4 threads per query row.
 template <typename KV, int DH>
 __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t* tiles) {
   constexpr int OD = DH / 4;
@@ -618,144 +718,184 @@ __global__ void rope_table_kernel(float2* tab, int npos, int half, double base) 
   tab[idx] = make_float2((float)cos(ang), (float)sin(ang));
 }
 
-template <typename W, int MR, int R>
-hipError_t gemv_launch(const Linear& L, hipStream_t st) {
-  const int waves = L.N / R;
-  const int blocks = (waves + 3) / 4;
-  const size_t lds = (size_t)MR * L.K * sizeof(float);
-  gemv_kernel<W, MR, R><<<blocks, 256, lds, st>>>(L);
-  return hipGetLastError();
+__global__ void fill_i32_kernel(int32_t* p, int32_t v, int64_t n) {
+  const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
 }
 
-constexpr size_t kGemvLds = 64 * 1024;
+// ---------------------------------------------------------------- launchers ----
+constexpr int kGemvMaxRows = 64;
+
+constexpr int gemv_r(int kc) { return kc <= 4 ? 4 : (kc == 8 ? 2 : 1); }
+// rows per pass: keeps the per-lane input slice (MR x VEC floats) and V = R*MR
+// accumulators small
+constexpr int gemv_mr(int kc) { return kc <= 2 ? 4 : (kc <= 8 ? 2 : 1); }
 
 template <typename W>
-hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st) {
+bool gemv_fits(const Linear& L) {
   constexpr int VEC = WT<W>::VEC;
-  const size_t row_bytes = (size_t)L.K * sizeof(float);
-  const bool gemv_ok = (L.K % (64 * VEC) == 0) && (L.N % 4 == 0) && L.M <= 8;
-  if (gemv_ok) {
-    if (L.M == 1 && row_bytes <= kGemvLds) return gemv_launch<W, 1, 4>(L, st);
-    if (L.M <= 2 && 2 * row_bytes <= kGemvLds) return gemv_launch<W, 2, 4>(L, st);
-    if (L.M <= 4 && 4 * row_bytes <= kGemvLds) return gemv_launch<W, 4, 4>(L, st);
-    if (8 * row_bytes <= kGemvLds) return gemv_launch<W, 8, 2>(L, st);
-  }
-  if (L.gain != nullptr) {
-    rms_kernel<<<(L.M + 3) / 4, 256, 0, st>>>(L.X, L.ldx, L.M, L.K, L.eps, inv_rms);
-  }
-  dim3 grid(L.N / 64, (L.M + 63) / 64);
-  gemm_kernel<W><<<grid, 256, 0, st>>>(L, inv_rms);
-  return hipGetLastError();
+  if (L.M > kGemvMaxRows || L.K % (64 * VEC) != 0) return false;
+  const int kc = L.K / (64 * VEC);
+  if (kc != 1 && kc != 2 && kc != 4 && kc != 8 && kc != 16) return false;
+  const int r = gemv_r(kc);
+  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+  return L.N % r == 0 && !(pair && r % 2 != 0);
 }
 
-template <typename KV>
-hipError_t attn_split_t(const Attn& a, int max_kv, float* part, int64_t part_floats, hipStream_t st) {
+template <typename W, int KC>
+hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
+  constexpr int R = gemv_r(KC);
+  constexpr int MRMAX = gemv_mr(KC);
+  const dim3 grid((L.N / R + 3) / 4);
+  if (L.M == 1) return klaunch(gemv_kernel<W, 1, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
+  if constexpr (MRMAX >= 2) {
+    if (L.M == 2 || MRMAX == 2) return klaunch(gemv_kernel<W, 2, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
+  }
+  if constexpr (MRMAX >= 4) return klaunch(gemv_kernel<W, 4, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
+  return klaunch(gemv_kernel<W, 1, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
+}
+
+template <typename W>
+hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
+  if (gemv_fits<W>(L)) {
+    switch (L.K / (64 * WT<W>::VEC)) {
+      case 1: return gemv_launch<W, 1>(L, st, ev);
+      case 2: return gemv_launch<W, 2>(L, st, ev);
+      case 4: return gemv_launch<W, 4>(L, st, ev);
+      case 8: return gemv_launch<W, 8>(L, st, ev);
+      default: return gemv_launch<W, 16>(L, st, ev);
+    }
+  }
+  const dim3 grid(L.N / 64, (L.M + 63) / 64);
+  if (L.gain != nullptr) {
+    hipError_t e = klaunch(rms_kernel, dim3((L.M + 3) / 4), dim3(256), 0, st, ev.start, nullptr, L, inv_rms);
+    if (e != hipSuccess) return e;
+    return klaunch(gemm_kernel<W>, grid, dim3(256), 0, st, nullptr, ev.stop, L, (const float*)inv_rms);
+  }
+  return klaunch(gemm_kernel<W>, grid, dim3(256), 0, st, ev.start, ev.stop, L, (const float*)inv_rms);
+}
+
+template <typename KV, int DH>
+hipError_t attn_decode_dh(const Attn& a, int max_kv, float* part, int64_t part_floats, hipStream_t st, const Ev& ev) {
   const int M = a.tok.M;
   int chunk = 256;
   int S = (max_kv + chunk - 1) / chunk;
-  if (S < 1) S = 1;
-  // keep the split scratch within bounds; fall back to fewer, longer splits
-  while (S > 1 && (int64_t)M * a.H * S * (a.dh + 2) > part_floats) {
+  while (S > 1 && (S > kMaxSplits || (int64_t)M * a.H * S * (DH + 2) > part_floats)) {
     chunk *= 2;
     S = (max_kv + chunk - 1) / chunk;
   }
-  if (S > 1 && (int64_t)M * a.H * S * (a.dh + 2) > part_floats) S = 1;
-  if (S == 1) chunk = max_kv > 0 ? max_kv : 1;
-  dim3 grid(S, a.H, M);
-  if (a.dh == 64) {
-    attn_split_kernel<KV, 64><<<grid, 64, 0, st>>>(a, chunk, S, part);
-    if (S > 1) attn_combine_kernel<64><<<dim3(a.H, M), 64, 0, st>>>(part, S, a.H, a.O, a.ldo);
-  } else {
-    attn_split_kernel<KV, 32><<<grid, 64, 0, st>>>(a, chunk, S, part);
-    if (S > 1) attn_combine_kernel<32><<<dim3(a.H, M), 64, 0, st>>>(part, S, a.H, a.O, a.ldo);
+  if (S <= 1) {
+    return klaunch(attn_decode_kernel<KV, DH>, dim3(1, a.H, M), dim3(256), 0, st, ev.start, ev.stop, a,
+                   max_kv > 0 ? max_kv : 1, 1, part);
   }
-  return hipGetLastError();
+  hipError_t e = klaunch(attn_decode_kernel<KV, DH>, dim3(S, a.H, M), dim3(256), 0, st, ev.start, nullptr, a, chunk, S,
+                         part);
+  if (e != hipSuccess) return e;
+  return klaunch(attn_merge_kernel<DH>, dim3(a.H, M), dim3(256), 0, st, nullptr, ev.stop, (const float*)part, S, a.H,
+                 a.O, a.ldo);
 }
 
 template <typename KV>
-hipError_t attn_prefill_t(const Attn& a, const int32_t* tiles, int ntiles, hipStream_t st) {
-  dim3 grid(ntiles, a.H);
-  if (a.dh == 64) attn_prefill_kernel<KV, 64><<<grid, 256, 0, st>>>(a, tiles);
-  else attn_prefill_kernel<KV, 32><<<grid, 256, 0, st>>>(a, tiles);
-  return hipGetLastError();
+hipError_t attn_decode_t(const Attn& a, int max_kv, float* part, int64_t part_floats, hipStream_t st, const Ev& ev) {
+  if (a.dh == 64) return attn_decode_dh<KV, 64>(a, max_kv, part, part_floats, st, ev);
+  return attn_decode_dh<KV, 32>(a, max_kv, part, part_floats, st, ev);
+}
+
+template <typename KV>
+hipError_t attn_prefill_t(const Attn& a, const int32_t* tiles, int ntiles, hipStream_t st, const Ev& ev) {
+  const dim3 grid(ntiles, a.H);
+  if (a.dh == 64) return klaunch(attn_prefill_kernel<KV, 64>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
+  return klaunch(attn_prefill_kernel<KV, 32>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
 }
 
 }  // namespace
 
-hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms, hipStream_t st) {
+bool linear_is_gemv(const Linear& L, int wdt) { return wdt ? gemv_fits<uint16_t>(L) : gemv_fits<float>(L); }
+
+hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms, hipStream_t st, const Ev& ev) {
   if (L.M <= 0) return hipSuccess;
-  return wdt ? linear_t<uint16_t>(L, inv_rms, st) : linear_t<float>(L, inv_rms, st);
+  return wdt ? linear_t<uint16_t>(L, inv_rms, st, ev) : linear_t<float>(L, inv_rms, st, ev);
 }
 
-hipError_t launch_attn_split(const Attn& a, int kvt, int max_kv, float* part, int64_t part_floats, hipStream_t st) {
+hipError_t launch_attn_decode(const Attn& a, int kvt, int max_kv, float* part, int64_t part_floats, hipStream_t st,
+                              const Ev& ev) {
   if (a.tok.M <= 0) return hipSuccess;
-  if (kvt == 2) return attn_split_t<_Float16>(a, max_kv, part, part_floats, st);
-  if (kvt == 1) return attn_split_t<uint16_t>(a, max_kv, part, part_floats, st);
-  return attn_split_t<float>(a, max_kv, part, part_floats, st);
+  if (kvt == 2) return attn_decode_t<_Float16>(a, max_kv, part, part_floats, st, ev);
+  if (kvt == 1) return attn_decode_t<uint16_t>(a, max_kv, part, part_floats, st, ev);
+  return attn_decode_t<float>(a, max_kv, part, part_floats, st, ev);
 }
 
-hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int ntiles, hipStream_t st) {
+hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int ntiles, hipStream_t st,
+                               const Ev& ev) {
   if (ntiles <= 0) return hipSuccess;
-  if (kvt == 2) return attn_prefill_t<_Float16>(a, tiles, ntiles, st);
-  if (kvt == 1) return attn_prefill_t<uint16_t>(a, tiles, ntiles, st);
-  return attn_prefill_t<float>(a, tiles, ntiles, st);
+  if (kvt == 2) return attn_prefill_t<_Float16>(a, tiles, ntiles, st, ev);
+  if (kvt == 1) return attn_prefill_t<uint16_t>(a, tiles, ntiles, st, ev);
+  return attn_prefill_t<float>(a, tiles, ntiles, st, ev);
 }
 
-hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st) {
+hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st,
+                        const Ev& ev) {
   if (M <= 0) return hipSuccess;
-  if (wdt) embed_kernel<uint16_t><<<M, 256, 0, st>>>(reinterpret_cast<const uint16_t*>(emb), bytes, X, d);
-  else embed_kernel<float><<<M, 256, 0, st>>>(reinterpret_cast<const float*>(emb), bytes, X, d);
-  return hipGetLastError();
+  if (wdt)
+    return klaunch(embed_kernel<uint16_t>, dim3(M), dim3(256), 0, st, ev.start, ev.stop,
+                   reinterpret_cast<const uint16_t*>(emb), bytes, X, d);
+  return klaunch(embed_kernel<float>, dim3(M), dim3(256), 0, st, ev.start, ev.stop, reinterpret_cast<const float*>(emb),
+                 bytes, X, d);
 }
 
 hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const float* src2, const int32_t* src2_idx,
-                            float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st) {
+                            float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
-  copy_rows_kernel<<<M, 256, 0, st>>>(src, src_idx, src2, src2_idx, dst, dst_idx, d);
-  return hipGetLastError();
+  return klaunch(copy_rows_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, src_idx, src2, src2_idx, dst,
+                 dst_idx, d);
 }
 
 hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, const float* bos, float* dst,
-                       const int32_t* dst_idx, int d, int M, hipStream_t st) {
+                       const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
-  pool_kernel<<<M, 256, 0, st>>>(src, lo, cnt, bos, dst, dst_idx, d);
-  return hipGetLastError();
+  return klaunch(pool_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, lo, cnt, bos, dst, dst_idx, d);
 }
 
 hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps, float* out,
-                            const int32_t* dst_idx, int d, int M, hipStream_t st) {
+                            const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
-  norm_rows_kernel<<<M, 256, 0, st>>>(src, src_idx, gain, eps, out, dst_idx, d);
-  return hipGetLastError();
+  return klaunch(norm_rows_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, src_idx, gain, eps, out,
+                 dst_idx, d);
 }
 
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active, uint8_t* cand,
-                         float* prob, int32_t* accept_len, int write_len, hipStream_t st) {
+                         float* prob, int32_t* accept_len, int write_len, hipStream_t st, const Ev& ev) {
   if (B <= 0) return hipSuccess;
-  accept_kernel<<<B, 64 * n, 0, st>>>(logits, n, tau, active, cand, prob, accept_len, write_len);
-  return hipGetLastError();
+  return klaunch(accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau, active, cand, prob,
+                 accept_len, write_len);
 }
 
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
-                         int32_t* accept_len, hipStream_t st) {
+                         int32_t* accept_len, hipStream_t st, const Ev& ev) {
   if (B <= 0) return hipSuccess;
-  verify_kernel<<<B, 64 * (n > 1 ? n - 1 : 1), 0, st>>>(nt_logits, cand, n, active, accept_len);
-  return hipGetLastError();
+  return klaunch(verify_kernel, dim3(B), dim3(64 * (n > 1 ? n - 1 : 1)), 0, st, ev.start, ev.stop, nt_logits, cand, n,
+                 active, accept_len);
 }
 
 hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st) {
   if (n <= 0) return hipSuccess;
-  const int64_t blocks = (n + 255) / 256;
-  if (wdt) to_f32_kernel<uint16_t><<<blocks, 256, 0, st>>>(reinterpret_cast<const uint16_t*>(src), dst, n);
-  else to_f32_kernel<float><<<blocks, 256, 0, st>>>(reinterpret_cast<const float*>(src), dst, n);
-  return hipGetLastError();
+  const dim3 grid((unsigned)((n + 255) / 256));
+  if (wdt) return klaunch(to_f32_kernel<uint16_t>, grid, dim3(256), 0, st, nullptr, nullptr,
+                          reinterpret_cast<const uint16_t*>(src), dst, n);
+  return klaunch(to_f32_kernel<float>, grid, dim3(256), 0, st, nullptr, nullptr, reinterpret_cast<const float*>(src),
+                 dst, n);
 }
 
 hipError_t launch_rope_table(float2* tab, int npos, int dh, double base, hipStream_t st) {
   const int half = dh / 2;
   const int64_t tot = (int64_t)npos * half;
-  rope_table_kernel<<<(tot + 255) / 256, 256, 0, st>>>(tab, npos, half, base);
-  return hipGetLastError();
+  return klaunch(rope_table_kernel, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, st, nullptr, nullptr, tab, npos,
+                 half, base);
+}
+
+hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t st) {
+  if (n <= 0) return hipSuccess;
+  return klaunch(fill_i32_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, nullptr, nullptr, p, v, n);
 }
 
 }  // namespace mbp

@@ -60,9 +60,12 @@ struct Sizes {
 };
 
 struct Regions {
-  size_t gains, rope, enc_k, enc_v, lm_k, lm_v, nt_k, nt_v, mb_k, mb_v, he, lat_in, lat_out, mbh, h1, h1_save,
-      mlp_out, head_in, logits, vlogits, X, Xl, Q, O, Hid, inv, part, plan0, plan1, active, total;
+  size_t gains, rope, enc_k, enc_v, lm_k, lm_v, nt_k, nt_v, mb_k, mb_v, he, lat_in, lat_out, rows, logits, vlogits,
+      X, Xl, Q, O, Hid, inv, part, plan0, plan1, active, total;
   size_t plan_ints;
+  // row offsets inside `rows` ([n_rows, d] floats): h1 [B], h1_save [B],
+  // MB window outputs [B, Wcap], MLP head outputs [B, nmax]
+  int32_t row_h1, row_h1s, row_mbh, row_mlp, n_rows;
 };
 
 bool valid_cfg(const mbp_config* c, std::string* why) {
@@ -148,11 +151,12 @@ Regions layout(const mbp_config& c) {
   r.he = take((size_t)s.B * s.Tcap * s.d * 4);
   r.lat_in = take((size_t)s.B * s.Kcap * s.d * 4);
   r.lat_out = take((size_t)s.B * s.Kcap * s.d * 4);
-  r.mbh = take((size_t)s.B * s.Wcap * s.d * 4);
-  r.h1 = take((size_t)s.B * s.d * 4);
-  r.h1_save = take((size_t)s.B * s.d * 4);
-  r.mlp_out = take((size_t)s.B * s.nmax * s.d * 4);
-  r.head_in = take((size_t)s.B * s.nmax * s.d * 4);
+  r.row_h1 = 0;
+  r.row_h1s = s.B;
+  r.row_mbh = 2 * s.B;
+  r.row_mlp = 2 * s.B + s.B * s.Wcap;
+  r.n_rows = r.row_mlp + s.B * s.nmax;
+  r.rows = take((size_t)r.n_rows * s.d * 4);
   r.logits = take((size_t)s.B * s.nmax * 256 * 4);
   r.vlogits = take((size_t)s.B * s.nmax * 256 * 4);
   // every per-pass buffer holds Ml = Mc + B rows: a chunk of Mc bytes can close
@@ -275,6 +279,17 @@ struct mbp_handle {
   std::vector<int32_t> pre_len;
   Plan plan[2];
 
+  // launch timing (mbp_set_timing)
+  struct TimeRec {
+    int cls, e0, e1;
+    double bytes;
+  };
+  bool timing = false;
+  std::vector<hipEvent_t> events;
+  int ev_used = 0;
+  std::vector<TimeRec> trecs;
+  mbp_kernel_time ttot[MBP_KCLASS_COUNT];
+
   template <typename T>
   T* R(size_t off) { return reinterpret_cast<T*>(ws + off); }
 };
@@ -296,6 +311,78 @@ int fail_hip(mbp_handle* h, hipError_t e, const char* what) {
   do {                                               \
     hipError_t e_ = (x);                             \
     if (e_ != hipSuccess) return fail_hip(h, e_, #x); \
+  } while (0)
+
+// Launch timing: each timed launch gets an event pair that the kernels themselves
+// stamp (start of the first kernel, end of the last one).
+int t_new(mbp_handle* h, int* idx) {
+  if ((size_t)h->ev_used >= h->events.size()) {
+    hipEvent_t e;
+    HIPCK(h, hipEventCreate(&e));
+    h->events.push_back(e);
+  }
+  *idx = h->ev_used++;
+  return MBP_OK;
+}
+
+int t_pair(mbp_handle* h, int cls, double bytes, Ev* ev) {
+  *ev = Ev();
+  if (!h->timing) return MBP_OK;
+  int e0, e1, rc;
+  if ((rc = t_new(h, &e0)) || (rc = t_new(h, &e1))) return rc;
+  ev->start = h->events[e0];
+  ev->stop = h->events[e1];
+  h->trecs.push_back({cls, e0, e1, bytes});
+  return MBP_OK;
+}
+
+// Fold finished records into the totals; only called right after a stream sync.
+int t_drain(mbp_handle* h) {
+  for (const auto& r : h->trecs) {
+    float ms = 0.f;
+    HIPCK(h, hipEventElapsedTime(&ms, h->events[r.e0], h->events[r.e1]));
+    h->ttot[r.cls].launches += 1;
+    h->ttot[r.cls].ms += ms;
+    h->ttot[r.cls].bytes += r.bytes;
+  }
+  h->trecs.clear();
+  h->ev_used = 0;
+  return MBP_OK;
+}
+
+#define TIMED(h, cls, bytes, fn, ...)               \
+  do {                                              \
+    Ev ev_;                                         \
+    int rc_ = t_pair(h, cls, bytes, &ev_);          \
+    if (rc_) return rc_;                            \
+    HIPCK(h, fn(__VA_ARGS__, ev_));                 \
+  } while (0)
+
+#define OTHER(h, fn, ...) TIMED(h, MBP_KCLASS_OTHER, 0.0, fn, __VA_ARGS__)
+
+// Algorithmic bytes of one linear layer: weights once, inputs, outputs.
+double linear_bytes(const mbp_handle* h, const Linear& L) {
+  const double wb = h->wdt ? 2.0 : 4.0, M = L.M, N = L.N, K = L.K;
+  double out;
+  switch (L.epi.kind) {
+    case EPI_STORE: out = M * N * 4; break;
+    case EPI_RESID: out = 2 * M * N * 4; break;
+    case EPI_SWIGLU: out = M * (N / 2) * 4; break;
+    default: out = M * (N / 3) * 4 + 2 * M * (N / 3) * (double)h->sz.es; break;
+  }
+  return N * K * wb + M * K * 4 + out;
+}
+
+int run_linear(mbp_handle* h, const Linear& L) {
+  const int cls = linear_is_gemv(L, h->wdt) ? MBP_KCLASS_GEMV : MBP_KCLASS_GEMM;
+  TIMED(h, cls, linear_bytes(h, L), launch_linear, L, h->wdt, h->R<float>(h->rg.inv), h->st);
+  return MBP_OK;
+}
+
+#define LINEAR(h, L)              \
+  do {                            \
+    int rcl_ = run_linear(h, L);  \
+    if (rcl_) return rcl_;        \
   } while (0)
 
 int upload(mbp_handle* h, Plan& p) {
@@ -342,15 +429,16 @@ std::vector<int32_t> make_tiles(const Toks& t) {
 }
 
 // Run one transformer stack over the token rows in X (residual stream, [M, d]).
+// kv_rows: total visible cache rows over the pass's queries (attention reads K and V
+// of each for every head).
 int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
-              const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv) {
+              const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows) {
   const Sizes& s = h->sz;
   const int M = tok.M;
   if (M == 0) return MBP_OK;
   float* Q = h->R<float>(h->rg.Q);
   float* O = h->R<float>(h->rg.O);
   float* Hid = h->R<float>(h->rg.Hid);
-  float* inv = h->R<float>(h->rg.inv);
   float* part = h->R<float>(h->rg.part);
   const float scale = h->cfg.attn_scale / std::sqrt((float)s.dh);
   for (size_t l = 0; l < layers.size(); ++l) {
@@ -365,32 +453,36 @@ int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, fl
     qkv.epi.kind = EPI_QKV; qkv.epi.Q = Q; qkv.epi.kc = kc; qkv.epi.vc = vc;
     qkv.epi.b_stride = kv.b_stride; qkv.epi.cap = kv.cap; qkv.epi.H = s.H; qkv.epi.dh = s.dh; qkv.epi.d = s.d;
     qkv.epi.rope = h->rope; qkv.epi.tok = tok; qkv.epi.kvt = h->cfg.kv_dtype;
-    HIPCK(h, launch_linear(qkv, h->wdt, inv, h->st));
+    LINEAR(h, qkv);
 
     Attn a{};
     a.Q = Q; a.ldq = s.d; a.kc = kc; a.vc = vc; a.b_stride = kv.b_stride; a.cap = kv.cap;
     a.H = s.H; a.dh = s.dh; a.tok = tok; a.grp_tab = grp_tab; a.scale = scale; a.O = O; a.ldo = s.d;
-    if (tiled) HIPCK(h, launch_attn_prefill(a, h->cfg.kv_dtype, tiles, ntiles, h->st));
-    else HIPCK(h, launch_attn_split(a, h->cfg.kv_dtype, max_kv, part, s.part_floats, h->st));
+    const double abytes = kv_rows * 2.0 * s.d * (double)s.es + 2.0 * M * s.d * 4;
+    if (tiled) {
+      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_prefill, a, h->cfg.kv_dtype, tiles, ntiles, h->st);
+    } else {
+      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_decode, a, h->cfg.kv_dtype, max_kv, part, s.part_floats, h->st);
+    }
 
     Linear o{};
     o.X = O; o.ldx = s.d; o.M = M; o.K = s.d; o.N = s.d; o.gain = nullptr;
     o.mats.m[0] = w.wo; o.mats.rows = s.d; o.mats.mode = MAT_SINGLE;
     o.epi.kind = EPI_RESID; o.epi.Y = X; o.epi.ldy = s.d;
-    HIPCK(h, launch_linear(o, h->wdt, inv, h->st));
+    LINEAR(h, o);
 
     Linear gu{};
     gu.X = X; gu.ldx = s.d; gu.M = M; gu.K = s.d; gu.N = 2 * s.dff;
     gu.gain = w.ffn_norm; gu.eps = h->cfg.rms_eps;
     gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
     gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
-    HIPCK(h, launch_linear(gu, h->wdt, inv, h->st));
+    LINEAR(h, gu);
 
     Linear dn{};
     dn.X = Hid; dn.ldx = s.dff; dn.M = M; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
     dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
     dn.epi.kind = EPI_RESID; dn.epi.Y = X; dn.epi.ldy = s.d;
-    HIPCK(h, launch_linear(dn, h->wdt, inv, h->st));
+    LINEAR(h, dn);
   }
   return MBP_OK;
 }
@@ -452,7 +544,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
   float* he = h->R<float>(h->rg.he);
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
-  float* h1 = h->R<float>(h->rg.h1);
+  float* h1 = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1 * s.d;
   size_t first = 0;
   bool first_chunk = true;
   while (first < items.size()) {
@@ -462,6 +554,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
     Toks te, tl;
     std::vector<int32_t> bytes, he_row, nt_src, lo_row, cnt, lat_row, last_src, last_dst;
     int max_kv_e = 0, max_kv_l = 0;
+    double kvr_e = 0, kvr_l = 0;
     std::vector<int> rows_in_chunk;
     for (size_t it = first; it < last; ++it) {
       const int b = items[it].b;
@@ -476,6 +569,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
           r.lm_rows = 1;
           r.epoch++;
           max_kv_l = std::max(max_kv_l, 1);
+          kvr_l += 1;
         }
       }
       const uint8_t byte = add[b][items[it].idx];
@@ -492,6 +586,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
         r.lm_rows = j + 1;
         r.epoch++;
         max_kv_l = std::max(max_kv_l, j + 1);
+        kvr_l += j + 1;
       }
       const int32_t L = (int32_t)r.q.size();  // group of this byte
       te.push(b, pos, pos, pos + 1, 0);
@@ -499,6 +594,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
       he_row.push_back(b * s.Tcap + pos);
       nt_src.push_back(b * s.Kcap + L);
       max_kv_e = std::max(max_kv_e, pos + 1);
+      kvr_e += pos + 1;
       if (it + 1 == last || items[it + 1].b != b) {
         last_src.push_back(te.size() - 1);
         last_dst.push_back(b);
@@ -518,21 +614,24 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
     if (rc) return rc;
     const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
 
-    HIPCK(h, launch_embed(h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st));
-    rc = run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e);
+    OTHER(h, launch_embed, h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st);
+    rc = run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
+                   kvr_e);
     if (rc) return rc;
-    HIPCK(h, launch_copy_rows(X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st));
+    OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st);
     if (Ml > 0) {
-      HIPCK(h, launch_pool(he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st));
-      HIPCK(h, launch_copy_rows(lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st));
-      rc = run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l);
+      OTHER(h, launch_pool, he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st);
+      OTHER(h, launch_copy_rows, lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st);
+      rc = run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l,
+                     kvr_l);
       if (rc) return rc;
-      HIPCK(h, launch_copy_rows(Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st));
+      OTHER(h, launch_copy_rows, Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st);
     }
-    HIPCK(h, launch_copy_rows(lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st));
-    rc = run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e);
+    OTHER(h, launch_copy_rows, lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st);
+    rc = run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
+                   kvr_e);
     if (rc) return rc;
-    HIPCK(h, launch_copy_rows(X, p.at(o_ls), nullptr, nullptr, h1, p.at(o_ld), s.d, (int)last_src.size(), h->st));
+    OTHER(h, launch_copy_rows, X, p.at(o_ls), nullptr, nullptr, h1, p.at(o_ld), s.d, (int)last_src.size(), h->st);
     first = last;
   }
   return MBP_OK;
@@ -704,112 +803,105 @@ namespace {
 int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len) {
   const Sizes& s = h->sz;
   const mbp_config& c = h->cfg;
+  const Regions& rg = h->rg;
   const int B = h->batch;
   Plan& p = h->plan[1];
   p.buf.clear();
-  float* h1 = h->R<float>(h->rg.h1);
-  float* head_in = h->R<float>(h->rg.head_in);
-  float* logits = h->R<float>(h->rg.logits);
-  float* lat_in = h->R<float>(h->rg.lat_in);
-  float* lat_out = h->R<float>(h->rg.lat_out);
-  float* mbh = h->R<float>(h->rg.mbh);
-  float* Xm = h->R<float>(h->rg.X);
-  float* Hid = h->R<float>(h->rg.Hid);
-  float* inv = h->R<float>(h->rg.inv);
+  float* rows = h->R<float>(rg.rows);
+  float* h1 = rows + (size_t)rg.row_h1 * s.d;
+  float* mbh = rows + (size_t)rg.row_mbh * s.d;
+  float* mlp_out = rows + (size_t)rg.row_mlp * s.d;
+  float* logits = h->R<float>(rg.logits);
+  float* lat_in = h->R<float>(rg.lat_in);
+  float* lat_out = h->R<float>(rg.lat_out);
+  float* Xm = h->R<float>(rg.X);
+  float* Hid = h->R<float>(rg.Hid);
 
-  std::vector<int32_t> nt_src, nt_dst, mb_src, mb_dst;
-  for (int b = 0; b < B; ++b) {
-    nt_src.push_back(b);
-    nt_dst.push_back(b * n);
-  }
+  // head_rows[b*n + m]: row of `rows` holding the hidden state of candidate m of row b
+  std::vector<int32_t> head_rows((size_t)B * n), mlp_dst;
   Toks tm;
   std::vector<int32_t> zrow, wrow, grp_tab;
   int max_w = 0;
+  double kvr_m = 0;
   const bool lca = c.head == MBP_HEAD_LCA;
-  if (lca && n >= 2) {
-    grp_tab.assign((size_t)B * s.Wcap, 0);
-    for (int b = 0; b < B; ++b) {
-      Row& r = h->rows[b];
-      const int32_t t = (int32_t)r.x.size() - 1;
-      const int32_t g = (int32_t)r.q.size();
-      const int32_t sw = g >= 1 ? (g - 1 == 0 ? 0 : r.q[g - 2]) : 0;
-      const int32_t W = t + n - 1 - sw;
-      if (W > s.Wcap) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
-      if (r.win_epoch != r.epoch || r.win_s != sw) {
-        r.win_epoch = r.epoch;
-        r.win_s = sw;
-        r.win_valid = 0;
-      }
-      for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
-        const int32_t pos = sw + w;
-        grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
-      }
-      for (int32_t w = r.win_valid; w < W; ++w) {
-        const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
-        tm.push(b, sw + w, w, w + 1, G);
-        zrow.push_back(b * s.Kcap + G);
-        wrow.push_back(b * s.Wcap + w);
-        max_w = std::max(max_w, w + 1);
-      }
-      r.win_valid = std::max(r.win_valid, W);
-      for (int m = 1; m < n; ++m) {
-        mb_src.push_back(b * s.Wcap + (t - sw) + m - 1);
-        mb_dst.push_back(b * n + m);
-      }
+  if (lca && n >= 2) grp_tab.assign((size_t)B * s.Wcap, 0);
+  for (int b = 0; b < B; ++b) {
+    head_rows[(size_t)b * n] = rg.row_h1 + b;
+    if (n < 2) continue;
+    if (!lca) {
+      for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mlp + b * s.nmax + m;
+      continue;
     }
-  } else if (!lca && n >= 2) {
-    for (int b = 0; b < B; ++b)
-      for (int m = 1; m < n; ++m) {
-        mb_src.push_back(b * s.nmax + m);
-        mb_dst.push_back(b * n + m);
-      }
+    Row& r = h->rows[b];
+    const int32_t t = (int32_t)r.x.size() - 1;
+    const int32_t g = (int32_t)r.q.size();
+    const int32_t sw = g >= 1 ? (g - 1 == 0 ? 0 : r.q[g - 2]) : 0;
+    const int32_t W = t + n - 1 - sw;
+    if (W > s.Wcap) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
+    if (r.win_epoch != r.epoch || r.win_s != sw) {
+      r.win_epoch = r.epoch;
+      r.win_s = sw;
+      r.win_valid = 0;
+    }
+    for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
+      const int32_t pos = sw + w;
+      grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
+    }
+    for (int32_t w = r.win_valid; w < W; ++w) {
+      const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
+      tm.push(b, sw + w, w, w + 1, G);
+      zrow.push_back(b * s.Kcap + G);
+      wrow.push_back(b * s.Wcap + w);
+      max_w = std::max(max_w, w + 1);
+      kvr_m += w + 1;
+    }
+    r.win_valid = std::max(r.win_valid, W);
+    for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mbh + b * s.Wcap + (t - sw) + m - 1;
   }
+  if (!lca)
+    for (int m = 1; m < n; ++m)
+      for (int b = 0; b < B; ++b) mlp_dst.push_back(b * s.nmax + m);
   const TokOffs om = add_toks(p, tm);
-  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab), o_ns = p.add(nt_src),
-               o_nd = p.add(nt_dst), o_ms = p.add(mb_src), o_md = p.add(mb_dst);
+  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab), o_hr = p.add(head_rows),
+               o_md = p.add(mlp_dst);
   int rc = upload(h, p);
   if (rc) return rc;
 
   if (lca && tm.size() > 0) {
     const Tok tok = dev_tok(p, om, tm.size());
-    HIPCK(h, launch_copy_rows(lat_out, p.at(o_z), lat_in, p.at(o_z), Xm, nullptr, s.d, tm.size(), h->st));
-    rc = run_stack(h, h->mb, h->kv_mb, Xm, tok, p.at(o_g), false, nullptr, 0, max_w);
+    OTHER(h, launch_copy_rows, lat_out, p.at(o_z), lat_in, p.at(o_z), Xm, nullptr, s.d, tm.size(), h->st);
+    rc = run_stack(h, h->mb, h->kv_mb, Xm, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m);
     if (rc) return rc;
-    HIPCK(h, launch_copy_rows(Xm, nullptr, nullptr, nullptr, mbh, p.at(o_w), s.d, tm.size(), h->st));
+    OTHER(h, launch_copy_rows, Xm, nullptr, nullptr, nullptr, mbh, p.at(o_w), s.d, tm.size(), h->st);
   }
-  float* mlp_out = h->R<float>(h->rg.mlp_out);
-  if (!lca && n >= 2) {
+  if (!lca) {
     for (int m = 1; m < n; ++m) {
       const MlpW& w = h->mlp[m - 1];
-      // residual base: mlp_out[b, m] = h1[b]
-      HIPCK(h, hipMemcpy2DAsync(mlp_out + (size_t)m * s.d, (size_t)s.nmax * s.d * 4, h1, (size_t)s.d * 4,
-                                (size_t)s.d * 4, B, hipMemcpyDeviceToDevice, h->st));
+      // head m-1: mlp_out[b, m] = h1[b] + FFN_{m-1}(RMSNorm(h1[b]))
+      OTHER(h, launch_copy_rows, h1, nullptr, nullptr, nullptr, mlp_out, p.at(o_md) + (size_t)(m - 1) * B, s.d, B,
+            h->st);
       Linear gu{};
       gu.X = h1; gu.ldx = s.d; gu.M = B; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.norm; gu.eps = c.rms_eps;
       gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
       gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
-      HIPCK(h, launch_linear(gu, h->wdt, inv, h->st));
+      LINEAR(h, gu);
       Linear dn{};
       dn.X = Hid; dn.ldx = s.dff; dn.M = B; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
       dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
       dn.epi.kind = EPI_RESID; dn.epi.Y = mlp_out + (size_t)m * s.d; dn.epi.ldy = s.nmax * s.d;
-      HIPCK(h, launch_linear(dn, h->wdt, inv, h->st));
+      LINEAR(h, dn);
     }
   }
-  // head inputs: RMSNorm * gain of each candidate row, then the shared unembedding
-  HIPCK(h, launch_norm_rows(h1, p.at(o_ns), h->g_nt, c.rms_eps, head_in, p.at(o_nd), s.d, B, h->st));
-  if (n >= 2) {
-    const float* src = lca ? mbh : mlp_out;
-    const float* g = lca ? h->g_mb : h->g_nt;
-    HIPCK(h, launch_norm_rows(src, p.at(o_ms), g, c.rms_eps, head_in, p.at(o_md), s.d, (int)mb_src.size(), h->st));
-  }
+  // head: RMSNorm with the head's gain (NT norm for candidate 1, MB norm for the LCA
+  // rows) fused into the shared unembedding
   Linear un{};
-  un.X = head_in; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = nullptr;
+  un.X = rows; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.xidx = p.at(o_hr);
+  un.gain = h->g_nt; un.gain2 = lca ? h->g_mb : nullptr; un.gain_period = n; un.eps = c.rms_eps;
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
-  HIPCK(h, launch_linear(un, h->wdt, inv, h->st));
-  HIPCK(h, launch_accept(logits, B, n, tau, h->R<int32_t>(h->rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
-                         h->st));
+  LINEAR(h, un);
+  OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
+        h->st);
   return MBP_OK;
 }
 
@@ -860,24 +952,23 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   for (int b = 0; b < B; ++b)
     if (simulate_latents(c, h->rows[b], add[b].data(), n) > c.max_latents)
       return fail(h, MBP_ECAPACITY, "verify drafts exceed max_latents");
-  float* h1 = h->R<float>(h->rg.h1);
-  float* h1s = h->R<float>(h->rg.h1_save);
+  float* h1 = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1 * s.d;
+  float* h1s = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1s * s.d;
   HIPCK(h, hipMemcpyAsync(h1s, h1, (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
   rc = commit(h, add);
   if (rc) return rc;
   // NT outputs of the B*n tentative rows are in X (row-major by batch row)
   float* X = h->R<float>(h->rg.X);
-  float* head_in = h->R<float>(h->rg.head_in);
   float* vlog = h->R<float>(h->rg.vlogits);
-  HIPCK(h, launch_norm_rows(X, nullptr, h->g_nt, c.rms_eps, head_in, nullptr, s.d, B * n, h->st));
   Linear un{};
-  un.X = head_in; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = nullptr;
+  un.X = X; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = h->g_nt; un.eps = c.rms_eps;
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
-  HIPCK(h, launch_linear(un, h->wdt, h->R<float>(h->rg.inv), h->st));
-  HIPCK(h, launch_verify(vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len, h->st));
+  LINEAR(h, un);
+  OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len, h->st);
   HIPCK(h, hipMemcpyAsync(h->h_len.data(), d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
+  if (h->timing && (rc = t_drain(h))) return rc;
   // roll back to the accepted prefix; h1 = NT row of the last accepted draft
   Plan& p = h->plan[1];
   p.buf.clear();
@@ -891,7 +982,7 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   const size_t os = p.add(src), od = p.add(dst);
   rc = upload(h, p);
   if (rc) return rc;
-  HIPCK(h, launch_copy_rows(X, p.at(os), nullptr, nullptr, h1, p.at(od), s.d, B, h->st));
+  OTHER(h, launch_copy_rows, X, p.at(os), nullptr, nullptr, h1, p.at(od), s.d, B, h->st);
   h->pending = true;
   h->last_n = n;
   h->last_mode = mode;
@@ -920,6 +1011,7 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
   if (!h_override && !h->pending) return fail(h, MBP_ESTATE, "no pending step to accept");
   if ((h_override == nullptr) != (h_override_len == nullptr)) return fail(h, MBP_EINVAL, "override needs both arrays");
   HIPCK(h, hipStreamSynchronize(h->st));
+  if (h->timing && (rc = t_drain(h))) return rc;
   const int B = h->batch;
   std::vector<std::vector<uint8_t>> add(B);
   if (h_override) {
@@ -936,8 +1028,9 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
     }
     if (rollback) {
       for (int b = 0; b < B; ++b) truncate_row(h->rows[b], h->pre_len[b]);
-      HIPCK(h, hipMemcpyAsync(h->R<float>(h->rg.h1), h->R<float>(h->rg.h1_save), (size_t)B * s.d * 4,
-                              hipMemcpyDeviceToDevice, h->st));
+      float* rows = h->R<float>(h->rg.rows);
+      HIPCK(h, hipMemcpyAsync(rows + (size_t)h->rg.row_h1 * s.d, rows + (size_t)h->rg.row_h1s * s.d,
+                              (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
     }
   } else if (h->last_mode == MBP_ACCEPT_THRESHOLD) {
     const int n = h->last_n;
@@ -973,9 +1066,36 @@ extern "C" int mbp_reset(mbp_handle* h) {
   h->last_n = 0;
   h->poisoned = false;
   h->err.clear();
+  h->trecs.clear();
+  h->ev_used = 0;
   return MBP_OK;
 }
 
-extern "C" void mbp_destroy(mbp_handle* h) { delete h; }
+extern "C" int mbp_set_timing(mbp_handle* h, int32_t on) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  HIPCK(h, hipStreamSynchronize(h->st));
+  h->trecs.clear();
+  h->ev_used = 0;
+  for (auto& t : h->ttot) t = mbp_kernel_time{0, 0.0, 0.0};
+  h->timing = on != 0;
+  return MBP_OK;
+}
+
+extern "C" int mbp_read_timing(mbp_handle* h, mbp_kernel_time* out) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  if (!out) return fail(h, MBP_EINVAL, "null pointer");
+  HIPCK(h, hipStreamSynchronize(h->st));
+  if ((rc = t_drain(h))) return rc;
+  for (int i = 0; i < MBP_KCLASS_COUNT; ++i) out[i] = h->ttot[i];
+  return MBP_OK;
+}
+
+extern "C" void mbp_destroy(mbp_handle* h) {
+  if (!h) return;
+  for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
+  delete h;
+}
 
 extern "C" const char* mbp_last_error(const mbp_handle* h) { return h ? h->err.c_str() : "null handle"; }
