@@ -18,7 +18,9 @@
  *     device; "host" pointers to ordinary host memory.
  *   - The caller owns all device memory: weights, the workspace and all output
  *     buffers.  The library never allocates or frees device memory; it carves the
- *     caller's workspace.  It keeps a small host-side state per handle.
+ *     caller's workspace.  It keeps a small host-side state per handle, including
+ *     pinned host staging buffers (hipHostMalloc) for its uploads and downloads, and
+ *     one stream of its own on which part of a step runs concurrently.
  *   - All device work is enqueued on the stream given to mbp_init.  Device outputs
  *     are valid once the caller synchronizes that stream.  Calls that need host-side
  *     values (mbp_accept, mbp_decode_step in verify mode) synchronize it themselves.

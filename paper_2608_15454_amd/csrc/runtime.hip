@@ -5,6 +5,11 @@
 // ("plans") that are uploaded in one copy and consumed by the gfx950 kernels in
 // kernels.hip.  All model state (KV caches, pooled latents, LM outputs, MB window
 // cache, last NT row) lives in the caller's device workspace.
+//
+// Two streams: the caller's stream carries the encoder, LM module, NT decoder, head
+// and acceptance; a second stream of the library's own runs the LCA window update of
+// the next step concurrently with the NT decoder (both depend only on the encoder and
+// LM outputs of the commit), joined by an event before the head.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -54,14 +59,29 @@ struct Row {
 };
 
 struct Sizes {
-  int d, H, dh, dff, B, Tcap, Kcap, Wcap, Mc, Ml, nmax, Smax;
-  int64_t part_floats;
+  int d, H, dh, dff, B, Tcap, Kcap, Wcap, Mc, Ml, Mm, nmax, Smax;
+  int64_t part_floats, part_floats_mb;
   size_t es;  // element size of the KV caches
 };
 
+// Per-pass scratch: residual stream X, queries, attention output, FFN hidden,
+// row norms of the tiled GEMM, split-attention partials.
+struct ScratchOff {
+  size_t X, Q, O, Hid, inv, part;
+};
+
+struct Scratch {
+  float *X, *Q, *O, *Hid, *inv, *part;
+  int64_t part_floats;
+};
+
+constexpr int kPlans = 4;  // 0 commit, 1 head, 2 forked MB update, 3 MB update in the step
+
 struct Regions {
   size_t gains, rope, enc_k, enc_v, lm_k, lm_v, nt_k, nt_v, mb_k, mb_v, he, lat_in, lat_out, rows, logits, vlogits,
-      X, Xl, Q, O, Hid, inv, part, plan0, plan1, active, total;
+      Xl, active, total;
+  ScratchOff main, mb;
+  size_t plan[kPlans];
   size_t plan_ints;
   // row offsets inside `rows` ([n_rows, d] floats): h1 [B], h1_save [B],
   // MB window outputs [B, Wcap], MLP head outputs [B, nmax]
@@ -111,8 +131,11 @@ Sizes sizes_of(const mbp_config& c) {
   const int chunk = c.max_chunk > 0 ? c.max_chunk : 4096;
   s.Mc = std::max({chunk, s.B * s.nmax, s.B * s.Wcap});
   s.Ml = s.Mc + s.B;
+  s.Mm = s.B * s.Wcap;
   s.Smax = (s.Tcap + 255) / 256;
   s.part_floats = (int64_t)s.B * (s.nmax + 1) * s.H * s.Smax * (s.dh + 2);
+  const int sw = (s.Wcap + 255) / 256;
+  s.part_floats_mb = sw > 1 ? (int64_t)s.Mm * s.H * sw * (s.dh + 2) : 0;
   s.es = c.kv_dtype == MBP_F32 ? 4 : 2;
   return s;
 }
@@ -159,18 +182,24 @@ Regions layout(const mbp_config& c) {
   r.rows = take((size_t)r.n_rows * s.d * 4);
   r.logits = take((size_t)s.B * s.nmax * 256 * 4);
   r.vlogits = take((size_t)s.B * s.nmax * 256 * 4);
-  // every per-pass buffer holds Ml = Mc + B rows: a chunk of Mc bytes can close
-  // up to Mc segments, plus one BOS latent per row
-  r.X = take((size_t)s.Ml * s.d * 4);
+  // main scratch: Ml = Mc + B rows (a chunk of Mc bytes can close up to Mc segments,
+  // plus one BOS latent per row)
+  r.main.X = take((size_t)s.Ml * s.d * 4);
   r.Xl = take((size_t)s.Ml * s.d * 4);
-  r.Q = take((size_t)s.Ml * s.d * 4);
-  r.O = take((size_t)s.Ml * s.d * 4);
-  r.Hid = take((size_t)s.Ml * s.dff * 4);
-  r.inv = take((size_t)s.Ml * 4);
-  r.part = take((size_t)s.part_floats * 4);
+  r.main.Q = take((size_t)s.Ml * s.d * 4);
+  r.main.O = take((size_t)s.Ml * s.d * 4);
+  r.main.Hid = take((size_t)s.Ml * s.dff * 4);
+  r.main.inv = take((size_t)s.Ml * 4);
+  r.main.part = take((size_t)s.part_floats * 4);
+  // MB-window scratch: B * Wcap rows
+  r.mb.X = take((size_t)s.Mm * s.d * 4);
+  r.mb.Q = take((size_t)s.Mm * s.d * 4);
+  r.mb.O = take((size_t)s.Mm * s.d * 4);
+  r.mb.Hid = take((size_t)s.Mm * s.dff * 4);
+  r.mb.inv = take((size_t)s.Mm * 4);
+  r.mb.part = take((size_t)std::max<int64_t>(s.part_floats_mb, 1) * 4);
   r.plan_ints = (size_t)20 * s.Ml + (size_t)s.B * s.Wcap + 64;
-  r.plan0 = take(r.plan_ints * 4);
-  r.plan1 = take(r.plan_ints * 4);
+  for (int i = 0; i < kPlans; ++i) r.plan[i] = take(r.plan_ints * 4);
   r.active = take((size_t)s.B * 4);
   r.total = off;
   return r;
@@ -218,15 +247,28 @@ std::vector<WInfo> manifest(const mbp_config& c) {
   return m;
 }
 
-// Host-side staging of one device plan (int32 arrays at recorded offsets).
+// Pinned host staging of one device plan (int32 arrays at recorded offsets); the
+// copy to the device is asynchronous, so a plan is only rewritten once the stream has
+// passed its previous upload.
 struct Plan {
-  std::vector<int32_t> buf;
+  int32_t* host = nullptr;
   int32_t* dev = nullptr;
-  size_t cap = 0;
+  size_t n = 0, cap = 0;
+  bool overflow = false;
+  void clear() {
+    n = 0;
+    overflow = false;
+  }
   size_t add(const std::vector<int32_t>& a) {
-    const size_t o = buf.size();
-    buf.insert(buf.end(), a.begin(), a.end());
-    while (buf.size() % 4) buf.push_back(0);
+    const size_t o = n;
+    const size_t padded = (a.size() + 3) / 4 * 4;
+    if (n + padded > cap) {
+      overflow = true;
+      return 0;
+    }
+    if (!a.empty()) std::memcpy(host + n, a.data(), a.size() * 4);
+    for (size_t i = a.size(); i < padded; ++i) host[n + i] = 0;
+    n += padded;
     return o;
   }
   const int32_t* at(size_t o) const { return dev + o; }
@@ -255,7 +297,12 @@ struct mbp_handle {
   Sizes sz;
   Regions rg;
   int wdt;
-  hipStream_t st;
+  hipStream_t st;             // the caller's stream
+  hipStream_t st2 = nullptr;  // the library's stream for the forked MB window update
+  hipEvent_t ev_fork = nullptr, ev_mb = nullptr;
+  bool mb_pending = false;   // the caller's stream has not yet waited for ev_mb
+  bool mb_recorded = false;  // ev_mb was recorded at least once
+  int n_hint = 3;
   char* ws;
   bool poisoned = false;
   std::string err;
@@ -269,15 +316,16 @@ struct mbp_handle {
   std::vector<MlpW> mlp;
   KV kv_enc, kv_lm, kv_nt, kv_mb;
   float2* rope;
+  Scratch sc_main, sc_mb;
 
   std::vector<Row> rows;
   int batch = 0;
   bool pending = false;
   int last_n = 0, last_mode = 0;
-  std::vector<uint8_t> h_cand;
-  std::vector<int32_t> h_len;
+  uint8_t* h_cand = nullptr;  // pinned [B, n] candidates of the last step
+  int32_t* h_len = nullptr;   // pinned [B] accepted counts of the last step
   std::vector<int32_t> pre_len;
-  Plan plan[2];
+  Plan plan[kPlans];
 
   // launch timing (mbp_set_timing)
   struct TimeRec {
@@ -292,6 +340,8 @@ struct mbp_handle {
 
   template <typename T>
   T* R(size_t off) { return reinterpret_cast<T*>(ws + off); }
+  float* rows_base() { return R<float>(rg.rows); }
+  float* row_ptr(int32_t row) { return rows_base() + (size_t)row * sz.d; }
 };
 
 namespace {
@@ -313,6 +363,12 @@ int fail_hip(mbp_handle* h, hipError_t e, const char* what) {
     if (e_ != hipSuccess) return fail_hip(h, e_, #x); \
   } while (0)
 
+#define RCK(x)           \
+  do {                   \
+    int rc_ = (x);       \
+    if (rc_) return rc_; \
+  } while (0)
+
 // Launch timing: each timed launch gets an event pair that the kernels themselves
 // stamp (start of the first kernel, end of the last one).
 int t_new(mbp_handle* h, int* idx) {
@@ -328,15 +384,16 @@ int t_new(mbp_handle* h, int* idx) {
 int t_pair(mbp_handle* h, int cls, double bytes, Ev* ev) {
   *ev = Ev();
   if (!h->timing) return MBP_OK;
-  int e0, e1, rc;
-  if ((rc = t_new(h, &e0)) || (rc = t_new(h, &e1))) return rc;
+  int e0, e1;
+  RCK(t_new(h, &e0));
+  RCK(t_new(h, &e1));
   ev->start = h->events[e0];
   ev->stop = h->events[e1];
   h->trecs.push_back({cls, e0, e1, bytes});
   return MBP_OK;
 }
 
-// Fold finished records into the totals; only called right after a stream sync.
+// Fold finished records into the totals; both streams must be idle.
 int t_drain(mbp_handle* h) {
   for (const auto& r : h->trecs) {
     float ms = 0.f;
@@ -350,12 +407,18 @@ int t_drain(mbp_handle* h) {
   return MBP_OK;
 }
 
-#define TIMED(h, cls, bytes, fn, ...)               \
-  do {                                              \
-    Ev ev_;                                         \
-    int rc_ = t_pair(h, cls, bytes, &ev_);          \
-    if (rc_) return rc_;                            \
-    HIPCK(h, fn(__VA_ARGS__, ev_));                 \
+int sync_all(mbp_handle* h) {
+  HIPCK(h, hipStreamSynchronize(h->st));
+  HIPCK(h, hipStreamSynchronize(h->st2));
+  h->mb_pending = false;
+  return MBP_OK;
+}
+
+#define TIMED(h, cls, bytes, fn, ...) \
+  do {                                \
+    Ev ev_;                           \
+    RCK(t_pair(h, cls, bytes, &ev_)); \
+    HIPCK(h, fn(__VA_ARGS__, ev_));   \
   } while (0)
 
 #define OTHER(h, fn, ...) TIMED(h, MBP_KCLASS_OTHER, 0.0, fn, __VA_ARGS__)
@@ -373,22 +436,15 @@ double linear_bytes(const mbp_handle* h, const Linear& L) {
   return N * K * wb + M * K * 4 + out;
 }
 
-int run_linear(mbp_handle* h, const Linear& L) {
+int run_linear(mbp_handle* h, const Linear& L, float* inv, hipStream_t st) {
   const int cls = linear_is_gemv(L, h->wdt) ? MBP_KCLASS_GEMV : MBP_KCLASS_GEMM;
-  TIMED(h, cls, linear_bytes(h, L), launch_linear, L, h->wdt, h->R<float>(h->rg.inv), h->st);
+  TIMED(h, cls, linear_bytes(h, L), launch_linear, L, h->wdt, inv, st);
   return MBP_OK;
 }
 
-#define LINEAR(h, L)              \
-  do {                            \
-    int rcl_ = run_linear(h, L);  \
-    if (rcl_) return rcl_;        \
-  } while (0)
-
-int upload(mbp_handle* h, Plan& p) {
-  if (p.buf.size() > p.cap) return fail(h, MBP_ECAPACITY, "internal plan exceeds its capacity");
-  if (!p.buf.empty())
-    HIPCK(h, hipMemcpyAsync(p.dev, p.buf.data(), p.buf.size() * 4, hipMemcpyHostToDevice, h->st));
+int upload(mbp_handle* h, Plan& p, hipStream_t st) {
+  if (p.overflow) return fail(h, MBP_ECAPACITY, "internal plan exceeds its capacity");
+  if (p.n) HIPCK(h, hipMemcpyAsync(p.dev, p.host, p.n * 4, hipMemcpyHostToDevice, st));
   return MBP_OK;
 }
 
@@ -428,18 +484,14 @@ std::vector<int32_t> make_tiles(const Toks& t) {
   return tiles;
 }
 
-// Run one transformer stack over the token rows in X (residual stream, [M, d]).
-// kv_rows: total visible cache rows over the pass's queries (attention reads K and V
-// of each for every head).
+// One transformer stack over the token rows in X (residual stream, [M, d]) on stream
+// st with scratch sc.  kv_rows: total visible cache rows over the pass's queries.
 int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
-              const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows) {
+              const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows,
+              const Scratch& sc, hipStream_t st) {
   const Sizes& s = h->sz;
   const int M = tok.M;
   if (M == 0) return MBP_OK;
-  float* Q = h->R<float>(h->rg.Q);
-  float* O = h->R<float>(h->rg.O);
-  float* Hid = h->R<float>(h->rg.Hid);
-  float* part = h->R<float>(h->rg.part);
   const float scale = h->cfg.attn_scale / std::sqrt((float)s.dh);
   for (size_t l = 0; l < layers.size(); ++l) {
     const BlockW& w = layers[l];
@@ -450,39 +502,39 @@ int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, fl
     qkv.gain = w.attn_norm; qkv.eps = h->cfg.rms_eps;
     qkv.mats.m[0] = w.wq; qkv.mats.m[1] = w.wk; qkv.mats.m[2] = w.wv;
     qkv.mats.rows = s.d; qkv.mats.mode = MAT_QKV;
-    qkv.epi.kind = EPI_QKV; qkv.epi.Q = Q; qkv.epi.kc = kc; qkv.epi.vc = vc;
+    qkv.epi.kind = EPI_QKV; qkv.epi.Q = sc.Q; qkv.epi.kc = kc; qkv.epi.vc = vc;
     qkv.epi.b_stride = kv.b_stride; qkv.epi.cap = kv.cap; qkv.epi.H = s.H; qkv.epi.dh = s.dh; qkv.epi.d = s.d;
     qkv.epi.rope = h->rope; qkv.epi.tok = tok; qkv.epi.kvt = h->cfg.kv_dtype;
-    LINEAR(h, qkv);
+    RCK(run_linear(h, qkv, sc.inv, st));
 
     Attn a{};
-    a.Q = Q; a.ldq = s.d; a.kc = kc; a.vc = vc; a.b_stride = kv.b_stride; a.cap = kv.cap;
-    a.H = s.H; a.dh = s.dh; a.tok = tok; a.grp_tab = grp_tab; a.scale = scale; a.O = O; a.ldo = s.d;
+    a.Q = sc.Q; a.ldq = s.d; a.kc = kc; a.vc = vc; a.b_stride = kv.b_stride; a.cap = kv.cap;
+    a.H = s.H; a.dh = s.dh; a.tok = tok; a.grp_tab = grp_tab; a.scale = scale; a.O = sc.O; a.ldo = s.d;
     const double abytes = kv_rows * 2.0 * s.d * (double)s.es + 2.0 * M * s.d * 4;
     if (tiled) {
-      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_prefill, a, h->cfg.kv_dtype, tiles, ntiles, h->st);
+      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_prefill, a, h->cfg.kv_dtype, tiles, ntiles, st);
     } else {
-      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_decode, a, h->cfg.kv_dtype, max_kv, part, s.part_floats, h->st);
+      TIMED(h, MBP_KCLASS_ATTN, abytes, launch_attn_decode, a, h->cfg.kv_dtype, max_kv, sc.part, sc.part_floats, st);
     }
 
     Linear o{};
-    o.X = O; o.ldx = s.d; o.M = M; o.K = s.d; o.N = s.d; o.gain = nullptr;
+    o.X = sc.O; o.ldx = s.d; o.M = M; o.K = s.d; o.N = s.d; o.gain = nullptr;
     o.mats.m[0] = w.wo; o.mats.rows = s.d; o.mats.mode = MAT_SINGLE;
     o.epi.kind = EPI_RESID; o.epi.Y = X; o.epi.ldy = s.d;
-    LINEAR(h, o);
+    RCK(run_linear(h, o, sc.inv, st));
 
     Linear gu{};
     gu.X = X; gu.ldx = s.d; gu.M = M; gu.K = s.d; gu.N = 2 * s.dff;
     gu.gain = w.ffn_norm; gu.eps = h->cfg.rms_eps;
     gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
-    gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
-    LINEAR(h, gu);
+    gu.epi.kind = EPI_SWIGLU; gu.epi.Y = sc.Hid; gu.epi.ldy = s.dff;
+    RCK(run_linear(h, gu, sc.inv, st));
 
     Linear dn{};
-    dn.X = Hid; dn.ldx = s.dff; dn.M = M; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
+    dn.X = sc.Hid; dn.ldx = s.dff; dn.M = M; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
     dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
     dn.epi.kind = EPI_RESID; dn.epi.Y = X; dn.epi.ldy = s.d;
-    LINEAR(h, dn);
+    RCK(run_linear(h, dn, sc.inv, st));
   }
   return MBP_OK;
 }
@@ -519,10 +571,84 @@ void truncate_row(Row& r, int32_t T) {
   }
 }
 
+// Window start of a row: first byte of the previous group (byte 0 for groups 0, 1).
+int32_t window_start(const Row& r) {
+  const int32_t g = (int32_t)r.q.size();
+  return g >= 2 ? r.q[g - 2] : 0;
+}
+
+// LCA window of the current state for n candidates: window rows s..t+n-2 (previous
+// group, current group, n-2 virtual rows).  Computes, on stream st, the rows not yet
+// cached (rows are prefix-stable while the latent list is unchanged) and writes
+// their outputs to the MB rows of `rows`.  With clamp, n is reduced to fit the
+// window capacity instead of failing.
+int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
+  const Sizes& s = h->sz;
+  const Regions& rg = h->rg;
+  const int B = h->batch;
+  if (n < 2) return MBP_OK;
+  p.clear();
+  Toks tm;
+  std::vector<int32_t> zrow, wrow, grp_tab((size_t)B * s.Wcap, 0);
+  int max_w = 0;
+  double kvr_m = 0;
+  for (int b = 0; b < B; ++b) {
+    Row& r = h->rows[b];
+    const int32_t t = (int32_t)r.x.size() - 1;
+    const int32_t g = (int32_t)r.q.size();
+    const int32_t sw = window_start(r);
+    int32_t W = t + n - 1 - sw;
+    if (W > s.Wcap) {
+      if (!clamp) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
+      W = s.Wcap;
+    }
+    if (r.win_epoch != r.epoch || r.win_s != sw) {
+      r.win_epoch = r.epoch;
+      r.win_s = sw;
+      r.win_valid = 0;
+    }
+    for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
+      const int32_t pos = sw + w;
+      grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
+    }
+    for (int32_t w = r.win_valid; w < W; ++w) {
+      const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
+      tm.push(b, sw + w, w, w + 1, G);
+      zrow.push_back(b * s.Kcap + G);
+      wrow.push_back(rg.row_mbh + b * s.Wcap + w);
+      max_w = std::max(max_w, w + 1);
+      kvr_m += w + 1;
+    }
+    r.win_valid = std::max(r.win_valid, W);
+  }
+  if (tm.size() == 0) return MBP_OK;
+  const TokOffs om = add_toks(p, tm);
+  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab);
+  RCK(upload(h, p, st));
+  const Tok tok = dev_tok(p, om, tm.size());
+  const Scratch& sc = h->sc_mb;
+  OTHER(h, launch_copy_rows, h->R<float>(rg.lat_out), p.at(o_z), h->R<float>(rg.lat_in), p.at(o_z), sc.X, nullptr,
+        s.d, tm.size(), st);
+  RCK(run_stack(h, h->mb, h->kv_mb, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st));
+  OTHER(h, launch_copy_rows, sc.X, nullptr, nullptr, nullptr, h->rows_base(), p.at(o_w), s.d, tm.size(), st);
+  return MBP_OK;
+}
+
+// Make the caller's stream wait for a forked MB update.
+int mb_join(mbp_handle* h) {
+  if (h->mb_pending) {
+    HIPCK(h, hipStreamWaitEvent(h->st, h->ev_mb, 0));
+    h->mb_pending = false;
+  }
+  return MBP_OK;
+}
+
 // Commit add[b] (bytes) to every row: encoder, segmentation + pooling, LM module on
-// the segments that close, NT decoder; the last NT row of each row goes to h1.
-// Rows keep the NT outputs of the final chunk in X (token order).
-int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
+// the segments that close, NT decoder; the last NT row of each row goes to h1.  The
+// NT outputs of the final chunk stay in the main scratch X (token order).  With
+// fork_mb (LCA head), the next step's window update runs on the second stream
+// between the LM module and the NT decoder.
+int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool fork_mb) {
   const Sizes& s = h->sz;
   const mbp_config& c = h->cfg;
   for (int b = 0; b < h->batch; ++b) {
@@ -533,18 +659,20 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
     if (simulate_latents(c, r, add[b].data(), n) > c.max_latents)
       return fail(h, MBP_ECAPACITY, "row would exceed max_latents");
   }
+  RCK(mb_join(h));  // nothing may still read the latents or scratch rewritten below
   struct Item {
     int b, idx;
   };
   std::vector<Item> items;
   for (int b = 0; b < h->batch; ++b)
     for (int i = 0; i < (int)add[b].size(); ++i) items.push_back({b, i});
-  float* X = h->R<float>(h->rg.X);
+  const Scratch& sc = h->sc_main;
+  float* X = sc.X;
   float* Xl = h->R<float>(h->rg.Xl);
   float* he = h->R<float>(h->rg.he);
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
-  float* h1 = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1 * s.d;
+  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty();
   size_t first = 0;
   bool first_chunk = true;
   while (first < items.size()) {
@@ -597,7 +725,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
       kvr_e += pos + 1;
       if (it + 1 == last || items[it + 1].b != b) {
         last_src.push_back(te.size() - 1);
-        last_dst.push_back(b);
+        last_dst.push_back(h->rg.row_h1 + b);
       }
     }
     const int Me = te.size(), Ml = tl.size();
@@ -605,33 +733,43 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
     const bool tiled_l = Ml >= 16 * (int)rows_in_chunk.size();
     std::vector<int32_t> tiles_e = make_tiles(te), tiles_l = make_tiles(tl);
     Plan& p = h->plan[0];
-    p.buf.clear();
+    p.clear();
     const TokOffs oe = add_toks(p, te), ol = add_toks(p, tl);
     const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_nts = p.add(nt_src), o_lo = p.add(lo_row),
                  o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_ls = p.add(last_src), o_ld = p.add(last_dst),
                  o_te = p.add(tiles_e), o_tl = p.add(tiles_l);
-    int rc = upload(h, p);
-    if (rc) return rc;
+    RCK(upload(h, p, h->st));
     const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
 
     OTHER(h, launch_embed, h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st);
-    rc = run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                   kvr_e);
-    if (rc) return rc;
+    RCK(run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
+                  kvr_e, sc, h->st));
     OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st);
     if (Ml > 0) {
       OTHER(h, launch_pool, he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st);
       OTHER(h, launch_copy_rows, lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st);
-      rc = run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l,
-                     kvr_l);
-      if (rc) return rc;
+      RCK(run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l,
+                    kvr_l, sc, h->st));
       OTHER(h, launch_copy_rows, Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st);
     }
+    const bool fork_here = fork && last == items.size();
+    if (fork_here) HIPCK(h, hipEventRecord(h->ev_fork, h->st));  // the latents are final here
     OTHER(h, launch_copy_rows, lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st);
-    rc = run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                   kvr_e);
-    if (rc) return rc;
-    OTHER(h, launch_copy_rows, X, p.at(o_ls), nullptr, nullptr, h1, p.at(o_ld), s.d, (int)last_src.size(), h->st);
+    RCK(run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
+                  kvr_e, sc, h->st));
+    OTHER(h, launch_copy_rows, X, p.at(o_ls), nullptr, nullptr, h->rows_base(), p.at(o_ld), s.d,
+          (int)last_src.size(), h->st);
+    if (fork_here) {
+      // the next step's window update, enqueued after the NT decoder (the critical
+      // path) but ordered only after the LM module; its plan reuses a host buffer
+      // whose previous upload must have been consumed
+      if (h->mb_recorded) HIPCK(h, hipEventSynchronize(h->ev_mb));
+      HIPCK(h, hipStreamWaitEvent(h->st2, h->ev_fork, 0));
+      RCK(mb_update(h, h->n_hint, h->plan[2], h->st2, true));
+      HIPCK(h, hipEventRecord(h->ev_mb, h->st2));
+      h->mb_pending = true;
+      h->mb_recorded = true;
+    }
     first = last;
   }
   return MBP_OK;
@@ -640,6 +778,76 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add) {
 int check_ready(mbp_handle* h) {
   if (!h) return MBP_EINVAL;
   if (h->poisoned) return fail(h, MBP_ESTATE, "handle poisoned by an earlier HIP error; call mbp_reset");
+  return MBP_OK;
+}
+
+// Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
+// per-row greedy bytes / probabilities (and accept_len in threshold mode).
+int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len) {
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  const Regions& rg = h->rg;
+  const int B = h->batch;
+  const bool lca = c.head == MBP_HEAD_LCA;
+  if (lca) {
+    RCK(mb_join(h));
+    RCK(mb_update(h, n, h->plan[3], h->st, false));  // rows the forked update did not cover
+  }
+  Plan& p = h->plan[1];
+  p.clear();
+  float* h1 = h->row_ptr(rg.row_h1);
+  float* mlp_out = h->row_ptr(rg.row_mlp);
+  float* logits = h->R<float>(rg.logits);
+  const Scratch& sc = h->sc_main;
+
+  // head_rows[b*n + m]: row of `rows` holding the hidden state of candidate m of row b
+  std::vector<int32_t> head_rows((size_t)B * n), mlp_dst;
+  for (int b = 0; b < B; ++b) {
+    head_rows[(size_t)b * n] = rg.row_h1 + b;
+    if (n < 2) continue;
+    if (!lca) {
+      for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mlp + b * s.nmax + m;
+      continue;
+    }
+    const Row& r = h->rows[b];
+    const int32_t t = (int32_t)r.x.size() - 1;
+    for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mbh + b * s.Wcap + (t - r.win_s) + m - 1;
+  }
+  if (!lca)
+    for (int m = 1; m < n; ++m)
+      for (int b = 0; b < B; ++b) mlp_dst.push_back(rg.row_mlp + b * s.nmax + m);
+  const size_t o_hr = p.add(head_rows), o_md = p.add(mlp_dst);
+  RCK(upload(h, p, h->st));
+
+  if (!lca) {
+    for (int m = 1; m < n; ++m) {
+      const MlpW& w = h->mlp[m - 1];
+      // head m-1: mlp_out[b, m] = h1[b] + FFN_{m-1}(RMSNorm(h1[b]))
+      OTHER(h, launch_copy_rows, h1, nullptr, nullptr, nullptr, h->rows_base(), p.at(o_md) + (size_t)(m - 1) * B,
+            s.d, B, h->st);
+      Linear gu{};
+      gu.X = h1; gu.ldx = s.d; gu.M = B; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.norm; gu.eps = c.rms_eps;
+      gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
+      gu.epi.kind = EPI_SWIGLU; gu.epi.Y = sc.Hid; gu.epi.ldy = s.dff;
+      RCK(run_linear(h, gu, sc.inv, h->st));
+      Linear dn{};
+      dn.X = sc.Hid; dn.ldx = s.dff; dn.M = B; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
+      dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
+      dn.epi.kind = EPI_RESID; dn.epi.Y = mlp_out + (size_t)m * s.d; dn.epi.ldy = s.nmax * s.d;
+      RCK(run_linear(h, dn, sc.inv, h->st));
+    }
+  }
+  // head: RMSNorm with the head's gain (NT norm for candidate 1, MB norm for the LCA
+  // rows) fused into the shared unembedding
+  Linear un{};
+  un.X = h->rows_base(); un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.xidx = p.at(o_hr);
+  un.gain = h->g_nt; un.gain2 = lca ? h->g_mb : nullptr; un.gain_period = n; un.eps = c.rms_eps;
+  un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
+  un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
+  RCK(run_linear(h, un, sc.inv, h->st));
+  OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
+        h->st);
+  h->n_hint = n;
   return MBP_OK;
 }
 
@@ -691,7 +899,23 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   h->wdt = cfg->dtype == MBP_BF16 ? 1 : 0;
   h->st = reinterpret_cast<hipStream_t>(hip_stream);
   h->ws = reinterpret_cast<char*>(d_workspace);
+  h->n_hint = std::min(3, cfg->max_n);
   const Sizes& s = h->sz;
+  auto bail = [&]() {
+    mbp_destroy(h);
+    return MBP_EHIP;
+  };
+  hipError_t e = hipStreamCreateWithFlags(&h->st2, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_mb, hipEventDisableTiming);
+  // pinned host staging (host memory only): plans, step results
+  for (int i = 0; i < kPlans && e == hipSuccess; ++i) {
+    e = hipHostMalloc((void**)&h->plan[i].host, rg.plan_ints * 4, hipHostMallocDefault);
+    h->plan[i].cap = rg.plan_ints;
+  }
+  if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_cand, (size_t)s.B * s.nmax, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_len, (size_t)s.B * 4, hipHostMallocDefault);
+  if (e != hipSuccess) return bail();
 
   // norm gains and BOS converted to float32 once
   float* gains = h->R<float>(rg.gains);
@@ -699,8 +923,8 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   auto gain = [&](int widx) -> const float* {
     float* dst = gains + (size_t)gi * s.d;
     ++gi;
-    hipError_t e = launch_to_f32(d_weights[widx], h->wdt, dst, s.d, h->st);
-    if (e != hipSuccess) h->poisoned = true;
+    hipError_t ge = launch_to_f32(d_weights[widx], h->wdt, dst, s.d, h->st);
+    if (ge != hipSuccess) h->poisoned = true;
     return dst;
   };
   int w = 0;
@@ -753,17 +977,24 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   h->kv_nt = kvof(rg.nt_k, rg.nt_v, s.Tcap);
   h->kv_lm = kvof(rg.lm_k, rg.lm_v, s.Kcap);
   h->kv_mb = kvof(rg.mb_k, rg.mb_v, s.Wcap);
+  auto scratch = [&](const ScratchOff& o, int64_t pf) {
+    Scratch x;
+    x.X = h->R<float>(o.X);
+    x.Q = h->R<float>(o.Q);
+    x.O = h->R<float>(o.O);
+    x.Hid = h->R<float>(o.Hid);
+    x.inv = h->R<float>(o.inv);
+    x.part = h->R<float>(o.part);
+    x.part_floats = pf;
+    return x;
+  };
+  h->sc_main = scratch(rg.main, s.part_floats);
+  h->sc_mb = scratch(rg.mb, s.part_floats_mb);
   h->rope = h->R<float2>(rg.rope);
   const int npos = std::max(s.Tcap + s.nmax, s.Kcap) + 1;
-  hipError_t e = launch_rope_table(h->rope, npos, s.dh, (double)cfg->rope_base, h->st);
-  if (e != hipSuccess || h->poisoned) {
-    delete h;
-    return MBP_EHIP;
-  }
-  for (int i = 0; i < 2; ++i) {
-    h->plan[i].dev = h->R<int32_t>(i == 0 ? rg.plan0 : rg.plan1);
-    h->plan[i].cap = rg.plan_ints;
-  }
+  e = launch_rope_table(h->rope, npos, s.dh, (double)cfg->rope_base, h->st);
+  if (e != hipSuccess || h->poisoned) return bail();
+  for (int i = 0; i < kPlans; ++i) h->plan[i].dev = h->R<int32_t>(rg.plan[i]);
   h->rows.assign(s.B, Row());
   *out = h;
   return MBP_OK;
@@ -785,6 +1016,7 @@ extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t*
     if (simulate_latents(h->cfg, empty, add[b].data(), h_lens[b]) > h->cfg.max_latents)
       return fail(h, MBP_ECAPACITY, "prompt exceeds max_latents");
   }
+  RCK(sync_all(h));  // earlier work may still read buffers rewritten now
   h->rows.assign(s.B, Row());
   for (int b = 0; b < batch; ++b) h->rows[b].active = true;
   h->batch = batch;
@@ -793,119 +1025,8 @@ extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t*
   for (int b = 0; b < batch; ++b) act[b] = 1;
   HIPCK(h, hipMemcpyAsync(h->R<int32_t>(h->rg.active), act.data(), s.B * 4, hipMemcpyHostToDevice, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
-  return commit(h, add);
+  return commit(h, add, true);
 }
-
-namespace {
-
-// Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
-// per-row greedy bytes / probabilities (and accept_len in threshold mode).
-int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len) {
-  const Sizes& s = h->sz;
-  const mbp_config& c = h->cfg;
-  const Regions& rg = h->rg;
-  const int B = h->batch;
-  Plan& p = h->plan[1];
-  p.buf.clear();
-  float* rows = h->R<float>(rg.rows);
-  float* h1 = rows + (size_t)rg.row_h1 * s.d;
-  float* mbh = rows + (size_t)rg.row_mbh * s.d;
-  float* mlp_out = rows + (size_t)rg.row_mlp * s.d;
-  float* logits = h->R<float>(rg.logits);
-  float* lat_in = h->R<float>(rg.lat_in);
-  float* lat_out = h->R<float>(rg.lat_out);
-  float* Xm = h->R<float>(rg.X);
-  float* Hid = h->R<float>(rg.Hid);
-
-  // head_rows[b*n + m]: row of `rows` holding the hidden state of candidate m of row b
-  std::vector<int32_t> head_rows((size_t)B * n), mlp_dst;
-  Toks tm;
-  std::vector<int32_t> zrow, wrow, grp_tab;
-  int max_w = 0;
-  double kvr_m = 0;
-  const bool lca = c.head == MBP_HEAD_LCA;
-  if (lca && n >= 2) grp_tab.assign((size_t)B * s.Wcap, 0);
-  for (int b = 0; b < B; ++b) {
-    head_rows[(size_t)b * n] = rg.row_h1 + b;
-    if (n < 2) continue;
-    if (!lca) {
-      for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mlp + b * s.nmax + m;
-      continue;
-    }
-    Row& r = h->rows[b];
-    const int32_t t = (int32_t)r.x.size() - 1;
-    const int32_t g = (int32_t)r.q.size();
-    const int32_t sw = g >= 1 ? (g - 1 == 0 ? 0 : r.q[g - 2]) : 0;
-    const int32_t W = t + n - 1 - sw;
-    if (W > s.Wcap) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
-    if (r.win_epoch != r.epoch || r.win_s != sw) {
-      r.win_epoch = r.epoch;
-      r.win_s = sw;
-      r.win_valid = 0;
-    }
-    for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
-      const int32_t pos = sw + w;
-      grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
-    }
-    for (int32_t w = r.win_valid; w < W; ++w) {
-      const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
-      tm.push(b, sw + w, w, w + 1, G);
-      zrow.push_back(b * s.Kcap + G);
-      wrow.push_back(b * s.Wcap + w);
-      max_w = std::max(max_w, w + 1);
-      kvr_m += w + 1;
-    }
-    r.win_valid = std::max(r.win_valid, W);
-    for (int m = 1; m < n; ++m) head_rows[(size_t)b * n + m] = rg.row_mbh + b * s.Wcap + (t - sw) + m - 1;
-  }
-  if (!lca)
-    for (int m = 1; m < n; ++m)
-      for (int b = 0; b < B; ++b) mlp_dst.push_back(b * s.nmax + m);
-  const TokOffs om = add_toks(p, tm);
-  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab), o_hr = p.add(head_rows),
-               o_md = p.add(mlp_dst);
-  int rc = upload(h, p);
-  if (rc) return rc;
-
-  if (lca && tm.size() > 0) {
-    const Tok tok = dev_tok(p, om, tm.size());
-    OTHER(h, launch_copy_rows, lat_out, p.at(o_z), lat_in, p.at(o_z), Xm, nullptr, s.d, tm.size(), h->st);
-    rc = run_stack(h, h->mb, h->kv_mb, Xm, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m);
-    if (rc) return rc;
-    OTHER(h, launch_copy_rows, Xm, nullptr, nullptr, nullptr, mbh, p.at(o_w), s.d, tm.size(), h->st);
-  }
-  if (!lca) {
-    for (int m = 1; m < n; ++m) {
-      const MlpW& w = h->mlp[m - 1];
-      // head m-1: mlp_out[b, m] = h1[b] + FFN_{m-1}(RMSNorm(h1[b]))
-      OTHER(h, launch_copy_rows, h1, nullptr, nullptr, nullptr, mlp_out, p.at(o_md) + (size_t)(m - 1) * B, s.d, B,
-            h->st);
-      Linear gu{};
-      gu.X = h1; gu.ldx = s.d; gu.M = B; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.norm; gu.eps = c.rms_eps;
-      gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
-      gu.epi.kind = EPI_SWIGLU; gu.epi.Y = Hid; gu.epi.ldy = s.dff;
-      LINEAR(h, gu);
-      Linear dn{};
-      dn.X = Hid; dn.ldx = s.dff; dn.M = B; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
-      dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
-      dn.epi.kind = EPI_RESID; dn.epi.Y = mlp_out + (size_t)m * s.d; dn.epi.ldy = s.nmax * s.d;
-      LINEAR(h, dn);
-    }
-  }
-  // head: RMSNorm with the head's gain (NT norm for candidate 1, MB norm for the LCA
-  // rows) fused into the shared unembedding
-  Linear un{};
-  un.X = rows; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.xidx = p.at(o_hr);
-  un.gain = h->g_nt; un.gain2 = lca ? h->g_mb : nullptr; un.gain_period = n; un.eps = c.rms_eps;
-  un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
-  un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
-  LINEAR(h, un);
-  OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
-        h->st);
-  return MBP_OK;
-}
-
-}  // namespace
 
 extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, uint8_t* d_cand, float* d_prob,
                                int32_t* d_accept_len) {
@@ -920,69 +1041,71 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   if (!(tau >= 0.f && tau <= 1.f)) return fail(h, MBP_EINVAL, "tau must be in [0, 1]");
   if (mode != MBP_ACCEPT_THRESHOLD && mode != MBP_ACCEPT_SELF_VERIFY) return fail(h, MBP_EINVAL, "bad mode");
   if (!d_cand || !d_accept_len) return fail(h, MBP_EINVAL, "null output pointer");
+  const int B = h->batch;
+  if (c.head == MBP_HEAD_LCA && n >= 2) {
+    for (int b = 0; b < B; ++b) {
+      const Row& r = h->rows[b];
+      if ((int32_t)r.x.size() + n - 2 - window_start(r) > s.Wcap)
+        return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
+    }
+  }
   if (mode == MBP_ACCEPT_SELF_VERIFY) {
-    for (int b = 0; b < h->batch; ++b)
+    for (int b = 0; b < B; ++b)
       if ((int64_t)h->rows[b].x.size() + n > s.Tcap) return fail(h, MBP_ECAPACITY, "verify drafts exceed max_ctx");
   }
-  const int B = h->batch;
-  h->h_cand.assign((size_t)B * n, 0);
-  h->h_len.assign(B, 0);
+  std::memset(h->h_cand, 0, (size_t)B * n);
+  std::memset(h->h_len, 0, (size_t)B * 4);
   if (mode == MBP_ACCEPT_THRESHOLD) {
-    rc = draft(h, n, tau, true, d_cand, d_prob, d_accept_len);
-    if (rc) return rc;
-    HIPCK(h, hipMemcpyAsync(h->h_cand.data(), d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
-    HIPCK(h, hipMemcpyAsync(h->h_len.data(), d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+    RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len));
+    HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+    HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
     h->pending = true;
     h->last_n = n;
     h->last_mode = mode;
     return MBP_OK;
   }
   // self-verify: drafts, tentative commit of all n drafts, greedy check, rollback
-  rc = draft(h, n, tau, false, d_cand, d_prob, d_accept_len);
-  if (rc) return rc;
-  HIPCK(h, hipMemcpyAsync(h->h_cand.data(), d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+  RCK(draft(h, n, tau, false, d_cand, d_prob, d_accept_len));
+  HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
   std::vector<std::vector<uint8_t>> add(B);
   h->pre_len.assign(B, 0);
   for (int b = 0; b < B; ++b) {
     h->pre_len[b] = (int32_t)h->rows[b].x.size();
-    add[b].assign(h->h_cand.begin() + (size_t)b * n, h->h_cand.begin() + (size_t)(b + 1) * n);
+    add[b].assign(h->h_cand + (size_t)b * n, h->h_cand + (size_t)(b + 1) * n);
   }
   // capacity of the tentative commit
   for (int b = 0; b < B; ++b)
     if (simulate_latents(c, h->rows[b], add[b].data(), n) > c.max_latents)
       return fail(h, MBP_ECAPACITY, "verify drafts exceed max_latents");
-  float* h1 = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1 * s.d;
-  float* h1s = h->R<float>(h->rg.rows) + (size_t)h->rg.row_h1s * s.d;
+  float* h1 = h->row_ptr(h->rg.row_h1);
+  float* h1s = h->row_ptr(h->rg.row_h1s);
   HIPCK(h, hipMemcpyAsync(h1s, h1, (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
-  rc = commit(h, add);
-  if (rc) return rc;
+  RCK(commit(h, add, false));
   // NT outputs of the B*n tentative rows are in X (row-major by batch row)
-  float* X = h->R<float>(h->rg.X);
+  float* X = h->sc_main.X;
   float* vlog = h->R<float>(h->rg.vlogits);
   Linear un{};
   un.X = X; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = h->g_nt; un.eps = c.rms_eps;
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
-  LINEAR(h, un);
+  RCK(run_linear(h, un, h->sc_main.inv, h->st));
   OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len, h->st);
-  HIPCK(h, hipMemcpyAsync(h->h_len.data(), d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
-  if (h->timing && (rc = t_drain(h))) return rc;
   // roll back to the accepted prefix; h1 = NT row of the last accepted draft
   Plan& p = h->plan[1];
-  p.buf.clear();
+  p.clear();
   std::vector<int32_t> src, dst;
   for (int b = 0; b < B; ++b) {
     const int j = std::max(1, std::min(n, h->h_len[b]));
     truncate_row(h->rows[b], h->pre_len[b] + j);
     src.push_back(b * n + j - 1);
-    dst.push_back(b);
+    dst.push_back(h->rg.row_h1 + b);
   }
   const size_t os = p.add(src), od = p.add(dst);
-  rc = upload(h, p);
-  if (rc) return rc;
-  OTHER(h, launch_copy_rows, X, p.at(os), nullptr, nullptr, h1, p.at(od), s.d, B, h->st);
+  RCK(upload(h, p, h->st));
+  OTHER(h, launch_copy_rows, X, p.at(os), nullptr, nullptr, h->rows_base(), p.at(od), s.d, B, h->st);
   h->pending = true;
   h->last_n = n;
   h->last_mode = mode;
@@ -1011,7 +1134,10 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
   if (!h_override && !h->pending) return fail(h, MBP_ESTATE, "no pending step to accept");
   if ((h_override == nullptr) != (h_override_len == nullptr)) return fail(h, MBP_EINVAL, "override needs both arrays");
   HIPCK(h, hipStreamSynchronize(h->st));
-  if (h->timing && (rc = t_drain(h))) return rc;
+  if (h->timing) {
+    RCK(sync_all(h));
+    RCK(t_drain(h));
+  }
   const int B = h->batch;
   std::vector<std::vector<uint8_t>> add(B);
   if (h_override) {
@@ -1028,19 +1154,18 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
     }
     if (rollback) {
       for (int b = 0; b < B; ++b) truncate_row(h->rows[b], h->pre_len[b]);
-      float* rows = h->R<float>(h->rg.rows);
-      HIPCK(h, hipMemcpyAsync(rows + (size_t)h->rg.row_h1 * s.d, rows + (size_t)h->rg.row_h1s * s.d,
-                              (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
+      HIPCK(h, hipMemcpyAsync(h->row_ptr(h->rg.row_h1), h->row_ptr(h->rg.row_h1s), (size_t)B * s.d * 4,
+                              hipMemcpyDeviceToDevice, h->st));
     }
   } else if (h->last_mode == MBP_ACCEPT_THRESHOLD) {
     const int n = h->last_n;
     for (int b = 0; b < B; ++b) {
       const int k = std::max(0, std::min(n, h->h_len[b]));
-      add[b].assign(h->h_cand.begin() + (size_t)b * n, h->h_cand.begin() + (size_t)b * n + k);
+      add[b].assign(h->h_cand + (size_t)b * n, h->h_cand + (size_t)b * n + k);
     }
   }
   h->pending = false;
-  return commit(h, add);
+  return commit(h, add, true);
 }
 
 extern "C" int mbp_get_logits(mbp_handle* h, float* d_logits) {
@@ -1058,23 +1183,10 @@ extern "C" int32_t mbp_row_length(const mbp_handle* h, int32_t row) {
   return (int32_t)h->rows[row].x.size();
 }
 
-extern "C" int mbp_reset(mbp_handle* h) {
-  if (!h) return MBP_EINVAL;
-  h->rows.assign(h->sz.B, Row());
-  h->batch = 0;
-  h->pending = false;
-  h->last_n = 0;
-  h->poisoned = false;
-  h->err.clear();
-  h->trecs.clear();
-  h->ev_used = 0;
-  return MBP_OK;
-}
-
 extern "C" int mbp_set_timing(mbp_handle* h, int32_t on) {
   int rc = check_ready(h);
   if (rc) return rc;
-  HIPCK(h, hipStreamSynchronize(h->st));
+  RCK(sync_all(h));
   h->trecs.clear();
   h->ev_used = 0;
   for (auto& t : h->ttot) t = mbp_kernel_time{0, 0.0, 0.0};
@@ -1086,14 +1198,42 @@ extern "C" int mbp_read_timing(mbp_handle* h, mbp_kernel_time* out) {
   int rc = check_ready(h);
   if (rc) return rc;
   if (!out) return fail(h, MBP_EINVAL, "null pointer");
-  HIPCK(h, hipStreamSynchronize(h->st));
-  if ((rc = t_drain(h))) return rc;
+  RCK(sync_all(h));
+  RCK(t_drain(h));
   for (int i = 0; i < MBP_KCLASS_COUNT; ++i) out[i] = h->ttot[i];
+  return MBP_OK;
+}
+
+extern "C" int mbp_reset(mbp_handle* h) {
+  if (!h) return MBP_EINVAL;
+  // wait for enqueued work (errors are ignored: reset also recovers poisoned handles)
+  (void)hipStreamSynchronize(h->st);
+  (void)hipStreamSynchronize(h->st2);
+  h->mb_pending = false;
+  h->rows.assign(h->sz.B, Row());
+  h->batch = 0;
+  h->pending = false;
+  h->last_n = 0;
+  h->poisoned = false;
+  h->err.clear();
+  h->trecs.clear();
+  h->ev_used = 0;
   return MBP_OK;
 }
 
 extern "C" void mbp_destroy(mbp_handle* h) {
   if (!h) return;
+  (void)hipStreamSynchronize(h->st);  // pending copies may still read the pinned buffers
+  if (h->st2) {
+    (void)hipStreamSynchronize(h->st2);
+    (void)hipStreamDestroy(h->st2);
+  }
+  for (auto& p : h->plan)
+    if (p.host) (void)hipHostFree(p.host);
+  if (h->h_cand) (void)hipHostFree(h->h_cand);
+  if (h->h_len) (void)hipHostFree(h->h_len);
+  if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
+  if (h->ev_mb) (void)hipEventDestroy(h->ev_mb);
   for (hipEvent_t e : h->events) (void)hipEventDestroy(e);
   delete h;
 }
