@@ -80,6 +80,15 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *   kv_dtype                  storage type of every KV cache: MBP_F32, MBP_BF16 or
  *                             MBP_F16.  MBP_F16 stores the same bytes as bf16 with 3
  *                             more mantissa bits; values beyond +-65504 saturate.
+ *   no_engine                 0: passes of at most 16 token rows through a
+ *                             transformer stack run in the persistent engine (one
+ *                             cooperative launch per stack, layers chained through
+ *                             tagged device-coherent stores) when the dimensions
+ *                             allow it; 1: one kernel launch per layer operation.
+ *                             Both give the same results up to float32 rounding
+ *                             order.  The engine needs one resident block of 512
+ *                             threads per compute unit and the handle's stream to
+ *                             itself while a launch runs.
  */
 typedef struct {
   int32_t d_model, n_heads, d_ff;
@@ -89,6 +98,7 @@ typedef struct {
   float rope_base, rms_eps, attn_scale;
   int32_t window_mode;
   int32_t kv_dtype;
+  int32_t no_engine;
 } mbp_config;
 
 /* Number of weight tensors of the manifest for cfg, or a negative status. */
@@ -169,9 +179,11 @@ int mbp_get_logits(mbp_handle *h, float *d_logits);
  * the library enqueues is bracketed by a pair of HIP events on the handle's stream,
  * and the algorithmic bytes the launch must move are recorded with it (weights and
  * activations read and written by a linear layer; K/V rows read by attention).
- * Classes: weight-streaming GEMV (<= 8 rows), tiled GEMM, attention, other. */
+ * Classes: weight-streaming GEMV (<= 64 rows), tiled GEMM, attention, other, and
+ * persistent-engine launches (a whole transformer stack; their bytes are the
+ * weights, activations and K/V rows of every layer they run). */
 enum { MBP_KCLASS_GEMV = 0, MBP_KCLASS_GEMM = 1, MBP_KCLASS_ATTN = 2, MBP_KCLASS_OTHER = 3,
-       MBP_KCLASS_COUNT = 4 };
+       MBP_KCLASS_ENGINE = 4, MBP_KCLASS_COUNT = 5 };
 typedef struct {
   int64_t launches;
   double ms;     /* summed event-to-event durations */
@@ -187,8 +199,8 @@ int mbp_read_timing(mbp_handle *h, mbp_kernel_time *out);
 /* Current committed length of row r (host value), or a negative status. */
 int32_t mbp_row_length(const mbp_handle *h, int32_t row);
 
-/* Forget all rows (no device work); the handle becomes usable again after a HIP
- * error. */
+/* Forget all rows and clear an engine timeout (waits for the stream); the handle
+ * becomes usable again after a HIP error. */
 int mbp_reset(mbp_handle *h);
 
 /* Free the host-side handle.  Device memory stays the caller's. */

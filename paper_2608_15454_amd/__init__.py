@@ -38,7 +38,7 @@ class MbpConfig(ctypes.Structure):
         ("max_n", ctypes.c_int32), ("max_patch", ctypes.c_int32), ("max_window", ctypes.c_int32),
         ("max_chunk", ctypes.c_int32),
         ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("attn_scale", ctypes.c_float),
-        ("window_mode", ctypes.c_int32), ("kv_dtype", ctypes.c_int32),
+        ("window_mode", ctypes.c_int32), ("kv_dtype", ctypes.c_int32), ("no_engine", ctypes.c_int32),
     ]
 
 
@@ -46,7 +46,7 @@ class KernelTime(ctypes.Structure):
     _fields_ = [("launches", ctypes.c_int64), ("ms", ctypes.c_double), ("bytes", ctypes.c_double)]
 
 
-KCLASSES = ("gemv", "gemm", "attention", "other")
+KCLASSES = ("gemv", "gemm", "attention", "other", "engine")
 
 _lib = None
 
@@ -104,7 +104,7 @@ class MbpError(RuntimeError):
 
 
 def make_config(model, *, max_batch, max_ctx, max_latents=None, max_n=8, max_window=0, max_chunk=0,
-                kv_dtype=None) -> MbpConfig:
+                kv_dtype=None, engine=True) -> MbpConfig:
     """Fill an MbpConfig from any object with the model attributes (d_model, n_heads,
     d_ff, n_enc, n_lm, n_nb, n_mb, head 'lca'|'mlp', dtype 'f32'|'bf16', rope_base,
     rms_eps, attn_scale, max_patch, window_mode).  KV caches default to float16 for
@@ -122,6 +122,7 @@ def make_config(model, *, max_batch, max_ctx, max_latents=None, max_n=8, max_win
     if kv_dtype is None:
         kv_dtype = F16 if model.dtype == "bf16" else F32
     c.kv_dtype = kv_dtype
+    c.no_engine = 0 if engine else 1
     return c
 
 

@@ -11,7 +11,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmbp.so")
-SOURCES = ["kernels.hip", "runtime.hip"]
+SOURCES = ["kernels.hip", "engine.hip", "runtime.hip"]
 ARCH = os.environ.get("MBP_OFFLOAD_ARCH", "gfx950")
 
 # Packed-FP32 instructions are disabled for all device code: hipcc would otherwise

@@ -116,12 +116,13 @@ hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const floa
                             float* out, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());
 // Per batch row b < B: greedy byte and probability of each of the n logit rows,
 // then accept_len (threshold mode; write_len = 0 leaves accept_len untouched).
+// accept_len is -1 for every row when *fault != 0 (a failed engine wait).
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active,
-                         uint8_t* cand, float* prob, int32_t* accept_len, int write_len, hipStream_t st,
-                         const Ev& ev = Ev());
+                         uint8_t* cand, float* prob, int32_t* accept_len, int write_len, const int32_t* fault,
+                         hipStream_t st, const Ev& ev = Ev());
 // Greedy verification: NT logits of the n tentative rows vs the drafts.
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
-                         int32_t* accept_len, hipStream_t st, const Ev& ev = Ev());
+                         int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev = Ev());
 hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st);
 hipError_t launch_rope_table(float2* tab, int npos, int dh, double base, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t st);

@@ -11,89 +11,13 @@
 
 #include <math.h>
 
+#include "dev.h"
 #include "kernels.h"
 
 namespace mbp {
 namespace {
 
-__device__ __forceinline__ float bf2f(uint32_t h) { return __uint_as_float(h << 16); }
-
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7fffu + ((u >> 16) & 1u);  // round to nearest, ties to even
-  return (uint16_t)(u >> 16);
-}
-
-template <typename W>
-struct WT;
-
-template <>
-struct WT<uint16_t> {  // bfloat16 bits
-  static constexpr int VEC = 8;  // elements per 16-byte load
-  __device__ static float ld(const uint16_t* p, size_t i) { return bf2f(p[i]); }
-  __device__ static void st(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
-  __device__ static void unpack(const uint4& u, float* f) {
-    f[0] = bf2f(u.x & 0xffffu); f[1] = bf2f(u.x >> 16);
-    f[2] = bf2f(u.y & 0xffffu); f[3] = bf2f(u.y >> 16);
-    f[4] = bf2f(u.z & 0xffffu); f[5] = bf2f(u.z >> 16);
-    f[6] = bf2f(u.w & 0xffffu); f[7] = bf2f(u.w >> 16);
-  }
-};
-
-template <>
-struct WT<_Float16> {
-  static constexpr int VEC = 8;
-  __device__ static float ld(const _Float16* p, size_t i) { return (float)p[i]; }
-  __device__ static void st(_Float16* p, size_t i, float v) {
-    p[i] = (_Float16)fminf(fmaxf(v, -65504.0f), 65504.0f);  // saturate instead of overflowing to inf
-  }
-  __device__ static void unpack(const uint4& u, float* f) {
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      f[2 * j] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[j] & 0xffffu));
-      f[2 * j + 1] = (float)__builtin_bit_cast(_Float16, (uint16_t)(w[j] >> 16));
-    }
-  }
-};
-
-template <>
-struct WT<float> {
-  static constexpr int VEC = 4;
-  __device__ static float ld(const float* p, size_t i) { return p[i]; }
-  __device__ static void st(float* p, size_t i, float v) { p[i] = v; }
-  __device__ static void unpack(const uint4& u, float* f) {
-    f[0] = __uint_as_float(u.x); f[1] = __uint_as_float(u.y);
-    f[2] = __uint_as_float(u.z); f[3] = __uint_as_float(u.w);
-  }
-};
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-
-__device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
-
-template <typename W>
-__device__ __forceinline__ const W* mat_row(const Mats& mt, int n, int K) {
-  int which, r;
-  if (mt.mode == MAT_SINGLE) {
-    which = 0; r = n;
-  } else if (mt.mode == MAT_QKV) {
-    which = n / mt.rows; r = n - which * mt.rows;
-  } else {
-    which = n & 1; r = n >> 1;
-  }
-  return reinterpret_cast<const W*>(mt.m[which]) + (size_t)r * K;
-}
+using namespace dev;
 
 __device__ __forceinline__ const float* row_gain(const Linear& L, int m) {
   return (L.gain2 != nullptr && (m % L.gain_period) != 0) ? L.gain2 : L.gain;
@@ -152,30 +76,6 @@ hipError_t klaunch(Kern kernel, dim3 grid, dim3 block, size_t shm, hipStream_t s
 }
 
 // ------------------------------------------------------------------ GEMV ------
-// Wave total of V = 2^k values per lane by recursive halving (V - 1 exchanges
-// instead of 6V): afterwards lane l holds the total of value l / (64 / V).
-template <int V>
-__device__ __forceinline__ float multi_sum(float (&v)[V]) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int n = V, o = 32; n > 1; n >>= 1, o >>= 1) {
-    const bool upper = (lane & o) != 0;
-#pragma unroll
-    for (int j = 0; j < n / 2; ++j) {
-      // the lower lane keeps value j, the upper lane value j + n/2; selecting between
-      // the two finished sums (not between array slots) keeps v[] in registers
-      const float lo = v[j], hi = v[j + n / 2];
-      const float lo_sum = lo + __shfl_xor(lo, o);
-      const float hi_sum = hi + __shfl_xor(hi, o);
-      v[j] = upper ? hi_sum : lo_sum;
-    }
-  }
-  float t = v[0];
-#pragma unroll
-  for (int o = 32 / V; o > 0; o >>= 1) t += __shfl_xor(t, o);
-  return t;
-}
-
 // Wave w of block g owns output rows [(4g+w)*R, +R) and loads its whole R x K weight
 // slice into registers first (lane l holds 16 bytes of every 64*VEC-column chunk),
 // so each weight byte leaves HBM once.  Input rows are processed MR at a time; each
@@ -663,7 +563,7 @@ __device__ __forceinline__ float row_top1(const float* row, int lane, int* idx_o
 }
 
 __global__ void accept_kernel(const float* logits, int n, float tau, const int32_t* active, uint8_t* cand,
-                              float* prob, int32_t* accept_len, int write_len) {
+                              float* prob, int32_t* accept_len, int write_len, const int32_t* fault) {
   __shared__ float ps[8];
   const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (wave < n) {
@@ -679,12 +579,12 @@ __global__ void accept_kernel(const float* logits, int n, float tau, const int32
   if (tid == 0 && write_len) {
     int k = 1;
     while (k < n && ps[k] >= tau) ++k;
-    accept_len[b] = active[b] ? k : 0;
+    accept_len[b] = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
   }
 }
 
 __global__ void verify_kernel(const float* nt_logits, const uint8_t* cand, int n, const int32_t* active,
-                              int32_t* accept_len) {
+                              int32_t* accept_len, const int32_t* fault) {
   __shared__ int gam[8];
   const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (wave < n - 1) {
@@ -699,7 +599,7 @@ __global__ void verify_kernel(const float* nt_logits, const uint8_t* cand, int n
       if (gam[m] == (int)cand[b * n + m + 1]) ++j;
       else break;
     }
-    accept_len[b] = active[b] ? j : 0;
+    accept_len[b] = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? j : 0);
   }
 }
 
@@ -864,17 +764,18 @@ hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const floa
 }
 
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active, uint8_t* cand,
-                         float* prob, int32_t* accept_len, int write_len, hipStream_t st, const Ev& ev) {
+                         float* prob, int32_t* accept_len, int write_len, const int32_t* fault, hipStream_t st,
+                         const Ev& ev) {
   if (B <= 0) return hipSuccess;
   return klaunch(accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau, active, cand, prob,
-                 accept_len, write_len);
+                 accept_len, write_len, fault);
 }
 
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
-                         int32_t* accept_len, hipStream_t st, const Ev& ev) {
+                         int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev) {
   if (B <= 0) return hipSuccess;
   return klaunch(verify_kernel, dim3(B), dim3(64 * (n > 1 ? n - 1 : 1)), 0, st, ev.start, ev.stop, nt_logits, cand, n,
-                 active, accept_len);
+                 active, accept_len, fault);
 }
 
 hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st) {

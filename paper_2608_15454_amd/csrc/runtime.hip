@@ -6,10 +6,13 @@
 // kernels.hip.  All model state (KV caches, pooled latents, LM outputs, MB window
 // cache, last NT row) lives in the caller's device workspace.
 //
-// Two streams: the caller's stream carries the encoder, LM module, NT decoder, head
-// and acceptance; a second stream of the library's own runs the LCA window update of
-// the next step concurrently with the NT decoder (both depend only on the encoder and
-// LM outputs of the commit), joined by an event before the head.
+// Passes of a few token rows through a transformer stack (decode steps) run in the
+// persistent engine of engine.hip, one cooperative launch per stack; long passes
+// (prefill) use the per-kernel path.  Without the engine, a second stream of the
+// library's own runs the LCA window update of the next step concurrently with the NT
+// decoder (both depend only on the encoder and LM outputs of the commit), joined by an
+// event before the head; with it, every launch stays on the caller's stream, since a
+// cooperative launch needs the compute units to itself.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -19,6 +22,7 @@
 #include <string>
 #include <vector>
 
+#include "engine.h"
 #include "kernels.h"
 #include "mbp.h"
 
@@ -62,6 +66,9 @@ struct Sizes {
   int d, H, dh, dff, B, Tcap, Kcap, Wcap, Mc, Ml, Mm, nmax, Smax;
   int64_t part_floats, part_floats_mb;
   size_t es;  // element size of the KV caches
+  int Esplit;          // attention splits per (row, head) the engine buffers hold
+  int64_t ll_entries;  // tagged 8-byte entries of the engine buffers
+  int eng_ops;         // engine operations of all stacks
 };
 
 // Per-pass scratch: residual stream X, queries, attention output, FFN hidden,
@@ -86,6 +93,7 @@ struct Regions {
   // row offsets inside `rows` ([n_rows, d] floats): h1 [B], h1_save [B],
   // MB window outputs [B, Wcap], MLP head outputs [B, nmax]
   int32_t row_h1, row_h1s, row_mbh, row_mlp, n_rows;
+  size_t ll, eng_err, eng_ops;  // engine: tagged buffers, timeout flag, operation lists
 };
 
 bool valid_cfg(const mbp_config* c, std::string* why) {
@@ -113,6 +121,7 @@ bool valid_cfg(const mbp_config* c, std::string* why) {
   if (c->max_chunk < 0) return bad("max_chunk must be >= 0");
   if (c->window_mode != 0) return bad("only window_mode 0 is implemented");
   if (c->kv_dtype != MBP_F32 && c->kv_dtype != MBP_BF16 && c->kv_dtype != MBP_F16) return bad("bad kv_dtype");
+  if (c->no_engine != 0 && c->no_engine != 1) return bad("no_engine must be 0 or 1");
   if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f) || !std::isfinite(c->attn_scale)) return bad("bad rope_base/rms_eps/attn_scale");
   return true;
 }
@@ -137,6 +146,10 @@ Sizes sizes_of(const mbp_config& c) {
   const int sw = (s.Wcap + 255) / 256;
   s.part_floats_mb = sw > 1 ? (int64_t)s.Mm * s.H * sw * (s.dh + 2) : 0;
   s.es = c.kv_dtype == MBP_F32 ? 4 : 2;
+  const int ex = kEngineMaxRows;
+  s.Esplit = std::min(64, (s.Tcap + kEngineChunk - 1) / kEngineChunk + 1);
+  s.ll_entries = (int64_t)ex * s.d * 7 + (int64_t)ex * s.dff + (int64_t)ex * s.H * s.Esplit * (s.dh + 2);
+  s.eng_ops = 6 * (c.n_enc + c.n_lm + c.n_nb + (c.head == MBP_HEAD_LCA ? c.n_mb : 0));
   return s;
 }
 
@@ -201,6 +214,9 @@ Regions layout(const mbp_config& c) {
   r.plan_ints = (size_t)20 * s.Ml + (size_t)s.B * s.Wcap + 64;
   for (int i = 0; i < kPlans; ++i) r.plan[i] = take(r.plan_ints * 4);
   r.active = take((size_t)s.B * 4);
+  r.ll = take((size_t)s.ll_entries * 8);
+  r.eng_err = take(4);
+  r.eng_ops = take((size_t)std::max(s.eng_ops, 1) * sizeof(EOp));
   r.total = off;
   return r;
 }
@@ -286,8 +302,17 @@ struct Toks {  // host token list of one module pass
   int size() const { return (int)b.size(); }
 };
 
+// Operations of one transformer stack in the engine's device list.
+struct EngStack {
+  int first = 0;  // index of the first operation in the list
+  int nops = 0;   // 0: the stack does not fit the engine
+};
+
 struct TokOffs {
   size_t b, pos, slot, kvlen, grp;
+  size_t first;       // index of the first token of the same batch row (rows are contiguous)
+  size_t first_slot;  // slot of that token
+  int32_t max_ns;     // largest such slot
 };
 
 }  // namespace
@@ -337,6 +362,14 @@ struct mbp_handle {
   int ev_used = 0;
   std::vector<TimeRec> trecs;
   mbp_kernel_time ttot[MBP_KCLASS_COUNT];
+
+  // persistent engine
+  bool engine = false;
+  int eng_shape = -1;
+  EngStack es_enc, es_lm, es_nt, es_mb;
+  uint32_t tag_base = 1;
+  EOp* d_ops = nullptr;
+  int32_t* d_err = nullptr;
 
   template <typename T>
   T* R(size_t off) { return reinterpret_cast<T*>(ws + off); }
@@ -455,6 +488,15 @@ TokOffs add_toks(Plan& p, const Toks& t) {
   o.slot = p.add(t.slot);
   o.kvlen = p.add(t.kvlen);
   o.grp = p.add(t.grp);
+  std::vector<int32_t> first(t.size()), first_slot(t.size());
+  o.max_ns = 0;
+  for (int i = 0; i < t.size(); ++i) {
+    first[i] = (i > 0 && t.b[i] == t.b[i - 1]) ? first[i - 1] : i;
+    first_slot[i] = t.slot[first[i]];
+    o.max_ns = std::max(o.max_ns, first_slot[i]);
+  }
+  o.first = p.add(first);
+  o.first_slot = p.add(first_slot);
   return o;
 }
 
@@ -484,14 +526,55 @@ std::vector<int32_t> make_tiles(const Toks& t) {
   return tiles;
 }
 
+// Algorithmic bytes of one pass of M rows through a stack: every linear layer's
+// weights, inputs and outputs, and the K/V rows the queries read.
+double stack_bytes(const mbp_handle* h, int nlayers, int M, double kv_rows) {
+  const Sizes& s = h->sz;
+  const double wb = h->wdt ? 2.0 : 4.0, d = s.d, f = s.dff;
+  const double per_layer = (4.0 * d * d + 3.0 * d * f) * wb        // weights
+                           + M * (d * 4 + d * 4 + d * 4 + f * 4) * 4.0  // linear inputs
+                           + M * (3 * d + 2 * d + f + 2 * d) * 4.0       // outputs and residual reads
+                           + kv_rows * 2.0 * d * (double)s.es;           // attention K/V
+  return per_layer * nlayers;
+}
+
+// One pass through a stack in the persistent engine (see engine.hip).
+int run_engine(mbp_handle* h, const EngStack& es, int nlayers, float* X, const Tok& tok, const int32_t* first,
+               const int32_t* first_slot, int S, const int32_t* grp_tab, double kv_rows, hipStream_t st) {
+  ECall c;
+  c.x = X;
+  c.M = tok.M;
+  c.tok = tok;
+  c.first = first;
+  c.first_slot = first_slot;
+  c.grp_tab = grp_tab;
+  c.S = S;
+  if (h->tag_base > 0xF0000000u) {  // restart the tags before they wrap: clear the tagged buffers
+    HIPCK(h, hipMemsetAsync(h->R<uint64_t>(h->rg.ll), 0, (size_t)h->sz.ll_entries * 8, st));
+    h->tag_base = 1;
+  }
+  const uint32_t base = h->tag_base;
+  h->tag_base += (uint32_t)es.nops + 1;
+  TIMED(h, MBP_KCLASS_ENGINE, stack_bytes(h, nlayers, tok.M, kv_rows), launch_engine, h->eng_shape,
+        h->d_ops + es.first, es.nops / 6, c, base, h->d_err, st);
+  return MBP_OK;
+}
+
 // One transformer stack over the token rows in X (residual stream, [M, d]) on stream
 // st with scratch sc.  kv_rows: total visible cache rows over the pass's queries.
+// Short passes go to the engine when the stack has an operation list (es).
 int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
               const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows,
-              const Scratch& sc, hipStream_t st) {
+              const Scratch& sc, hipStream_t st, const EngStack* es = nullptr, const int32_t* first = nullptr,
+              const int32_t* first_slot = nullptr, int32_t max_ns = 0) {
   const Sizes& s = h->sz;
   const int M = tok.M;
   if (M == 0) return MBP_OK;
+  if (h->engine && es != nullptr && es->nops > 0 && !tiled && M <= kEngineMaxRows) {
+    const int S = (max_ns + kEngineChunk - 1) / kEngineChunk + 1;
+    if (S <= s.Esplit)
+      return run_engine(h, *es, (int)layers.size(), X, tok, first, first_slot, S, grp_tab, kv_rows, st);
+  }
   const float scale = h->cfg.attn_scale / std::sqrt((float)s.dh);
   for (size_t l = 0; l < layers.size(); ++l) {
     const BlockW& w = layers[l];
@@ -629,7 +712,8 @@ int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
   const Scratch& sc = h->sc_mb;
   OTHER(h, launch_copy_rows, h->R<float>(rg.lat_out), p.at(o_z), h->R<float>(rg.lat_in), p.at(o_z), sc.X, nullptr,
         s.d, tm.size(), st);
-  RCK(run_stack(h, h->mb, h->kv_mb, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st));
+  RCK(run_stack(h, h->mb, h->kv_mb, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st, &h->es_mb,
+                p.at(om.first), p.at(om.first_slot), om.max_ns));
   OTHER(h, launch_copy_rows, sc.X, nullptr, nullptr, nullptr, h->rows_base(), p.at(o_w), s.d, tm.size(), st);
   return MBP_OK;
 }
@@ -672,7 +756,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
   float* he = h->R<float>(h->rg.he);
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
-  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty();
+  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty() && !h->engine;
   size_t first = 0;
   bool first_chunk = true;
   while (first < items.size()) {
@@ -743,20 +827,20 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
 
     OTHER(h, launch_embed, h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st);
     RCK(run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                  kvr_e, sc, h->st));
+                  kvr_e, sc, h->st, &h->es_enc, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
     OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st);
     if (Ml > 0) {
       OTHER(h, launch_pool, he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st);
       OTHER(h, launch_copy_rows, lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st);
       RCK(run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l,
-                    kvr_l, sc, h->st));
+                    kvr_l, sc, h->st, &h->es_lm, p.at(ol.first), p.at(ol.first_slot), ol.max_ns));
       OTHER(h, launch_copy_rows, Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st);
     }
     const bool fork_here = fork && last == items.size();
     if (fork_here) HIPCK(h, hipEventRecord(h->ev_fork, h->st));  // the latents are final here
     OTHER(h, launch_copy_rows, lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st);
     RCK(run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                  kvr_e, sc, h->st));
+                  kvr_e, sc, h->st, &h->es_nt, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
     OTHER(h, launch_copy_rows, X, p.at(o_ls), nullptr, nullptr, h->rows_base(), p.at(o_ld), s.d,
           (int)last_src.size(), h->st);
     if (fork_here) {
@@ -772,6 +856,16 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     }
     first = last;
   }
+  return MBP_OK;
+}
+
+// accept_len < 0 marks a step in which an engine wait timed out (see launch_accept).
+int check_fault(mbp_handle* h) {
+  for (int b = 0; b < h->batch; ++b)
+    if (h->h_len[b] < 0) {
+      h->poisoned = true;
+      return fail(h, MBP_EHIP, "persistent engine: a wait for another block's data timed out");
+    }
   return MBP_OK;
 }
 
@@ -846,8 +940,110 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
   un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
   RCK(run_linear(h, un, sc.inv, h->st));
   OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
-        h->st);
+        h->engine ? h->d_err : nullptr, h->st);
   h->n_hint = n;
+  return MBP_OK;
+}
+
+// Operation lists of the persistent engine for every stack, uploaded once.  A stack
+// whose shapes do not fit the engine's register layout keeps nops = 0 (per-kernel
+// path); so does every stack when the device cannot host the engine's grid.
+int build_engine(mbp_handle* h) {
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  if (c.no_engine) return MBP_OK;
+  const int shape = engine_shape(h->wdt, c.kv_dtype, s.dh, s.d, s.dff);
+  if (shape < 0 || engine_grid(shape) <= 0) return MBP_OK;
+  h->eng_shape = shape;
+  const int ex = kEngineMaxRows;
+  uint64_t* x0 = h->R<uint64_t>(h->rg.ll);
+  uint64_t* x1 = x0 + (size_t)ex * s.d;
+  uint64_t* rr = x1 + (size_t)ex * s.d;
+  uint64_t* q = rr + (size_t)ex * s.d;
+  uint64_t* kvn = q + (size_t)ex * s.d;
+  uint64_t* a = kvn + (size_t)2 * ex * s.d;
+  uint64_t* hid = a + (size_t)ex * s.d;
+  uint64_t* part = hid + (size_t)ex * s.dff;
+  uint64_t* xb[2] = {x0, x1};
+  const float scale = c.attn_scale / std::sqrt((float)s.dh);
+  std::vector<EOp> ops;
+  auto stack = [&](const std::vector<BlockW>& layers, const KV& kv, EngStack& es) {
+    es.first = (int)ops.size();
+    const int L = (int)layers.size();
+    for (int l = 0; l < L; ++l) {
+      const BlockW& w = layers[l];
+      const uint32_t t = 6u * l;  // operation 6l + j writes tag 6l + j + 1
+      char* kc = reinterpret_cast<char*>(kv.k) + l * kv.layer_stride * s.es;
+      char* vc = reinterpret_cast<char*>(kv.v) + l * kv.layer_stride * s.es;
+      const EIn xl = l == 0 ? EIn{nullptr, nullptr, s.d, 0} : EIn{nullptr, xb[l % 2], s.d, t};
+      EOp op{};
+      op.kind = EOP_LINEAR;
+      op.tag = t + 1;
+      ELinear& qk = op.lin;
+      qk.x = xl; qk.K = s.d; qk.N = 3 * s.d; qk.gain = w.attn_norm; qk.eps = c.rms_eps;
+      qk.mats.m[0] = w.wq; qk.mats.m[1] = w.wk; qk.mats.m[2] = w.wv; qk.mats.rows = s.d; qk.mats.mode = MAT_QKV;
+      qk.epi = EPI_QKV; qk.y = q; qk.ldy = s.d;
+      qk.kvn = kvn; qk.kc = kc; qk.vc = vc; qk.b_stride = kv.b_stride; qk.cap = kv.cap;
+      qk.H = s.H; qk.dh = s.dh; qk.d = s.d; qk.rope = h->rope; qk.kvt = c.kv_dtype;
+      ops.push_back(op);
+
+      op = EOp{};
+      op.kind = EOP_ATTN;
+      op.tag = t + 2;
+      EAttn& at = op.at;
+      at.q = EIn{nullptr, q, s.d, t + 1};
+      at.kvn = kvn; at.kvn_tag = t + 1; at.kvn_ld = 2 * s.d; at.kc = kc; at.vc = vc;
+      at.b_stride = kv.b_stride; at.cap = kv.cap; at.H = s.H; at.dh = s.dh; at.d = s.d;
+      at.scale = scale; at.kvt = c.kv_dtype; at.part = part;
+      ops.push_back(op);
+
+      op = EOp{};
+      op.kind = EOP_MERGE;
+      op.tag = t + 3;
+      op.mg.part = part; op.mg.part_tag = t + 2; op.mg.H = s.H; op.mg.dh = s.dh; op.mg.out = a;
+      ops.push_back(op);
+
+      op = EOp{};
+      op.kind = EOP_LINEAR;
+      op.tag = t + 4;
+      ELinear& o = op.lin;
+      o.x = EIn{nullptr, a, s.d, t + 3}; o.K = s.d; o.N = s.d; o.gain = nullptr;
+      o.mats.m[0] = w.wo; o.mats.rows = s.d; o.mats.mode = MAT_SINGLE;
+      o.epi = EPI_RESID; o.resid = xl; o.y = rr; o.ldy = s.d;
+      ops.push_back(op);
+
+      op = EOp{};
+      op.kind = EOP_LINEAR;
+      op.tag = t + 5;
+      ELinear& gu = op.lin;
+      gu.x = EIn{nullptr, rr, s.d, t + 4}; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.ffn_norm; gu.eps = c.rms_eps;
+      gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
+      gu.epi = EPI_SWIGLU; gu.y = hid; gu.ldy = s.dff;
+      ops.push_back(op);
+
+      op = EOp{};
+      op.kind = EOP_LINEAR;
+      op.tag = t + 6;
+      ELinear& dn = op.lin;
+      dn.x = EIn{nullptr, hid, s.dff, t + 5}; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
+      dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
+      dn.epi = EPI_RESID; dn.resid = EIn{nullptr, rr, s.d, t + 4};
+      dn.y = l + 1 == L ? nullptr : xb[(l + 1) % 2];  // the last layer writes the caller's rows
+      dn.ldy = s.d;
+      ops.push_back(op);
+    }
+    es.nops = (int)ops.size() - es.first;
+  };
+  stack(h->enc, h->kv_enc, h->es_enc);
+  stack(h->lm, h->kv_lm, h->es_lm);
+  stack(h->nt, h->kv_nt, h->es_nt);
+  if (c.head == MBP_HEAD_LCA) stack(h->mb, h->kv_mb, h->es_mb);
+  if ((int)ops.size() > s.eng_ops) return fail(h, MBP_ECAPACITY, "engine operation list exceeds its region");
+  if (!ops.empty()) {
+    HIPCK(h, hipMemcpyAsync(h->d_ops, ops.data(), ops.size() * sizeof(EOp), hipMemcpyHostToDevice, h->st));
+    HIPCK(h, hipStreamSynchronize(h->st));
+  }
+  h->engine = true;
   return MBP_OK;
 }
 
@@ -996,6 +1192,11 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   if (e != hipSuccess || h->poisoned) return bail();
   for (int i = 0; i < kPlans; ++i) h->plan[i].dev = h->R<int32_t>(rg.plan[i]);
   h->rows.assign(s.B, Row());
+  h->d_err = h->R<int32_t>(rg.eng_err);
+  h->d_ops = h->R<EOp>(rg.eng_ops);
+  e = hipMemsetAsync(h->d_err, 0, 4, h->st);
+  if (e == hipSuccess) e = hipMemsetAsync(h->R<uint64_t>(rg.ll), 0, (size_t)s.ll_entries * 8, h->st);
+  if (e != hipSuccess || build_engine(h) != MBP_OK) return bail();
   *out = h;
   return MBP_OK;
 }
@@ -1090,9 +1291,11 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
   RCK(run_linear(h, un, h->sc_main.inv, h->st));
-  OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len, h->st);
+  OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len,
+        h->engine ? h->d_err : nullptr, h->st);
   HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
+  RCK(check_fault(h));
   // roll back to the accepted prefix; h1 = NT row of the last accepted draft
   Plan& p = h->plan[1];
   p.clear();
@@ -1118,6 +1321,7 @@ extern "C" int mbp_last_accepted(mbp_handle* h, uint8_t* h_bytes, int32_t* h_len
   if (!h->pending) return fail(h, MBP_ESTATE, "no pending step");
   if (!h_bytes || !h_lens) return fail(h, MBP_EINVAL, "null pointer");
   HIPCK(h, hipStreamSynchronize(h->st));
+  RCK(check_fault(h));
   const int n = h->last_n, mx = h->sz.nmax;
   for (int b = 0; b < h->batch; ++b) {
     h_lens[b] = h->h_len[b];
@@ -1158,6 +1362,7 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
                               hipMemcpyDeviceToDevice, h->st));
     }
   } else if (h->last_mode == MBP_ACCEPT_THRESHOLD) {
+    RCK(check_fault(h));
     const int n = h->last_n;
     for (int b = 0; b < B; ++b) {
       const int k = std::max(0, std::min(n, h->h_len[b]));
@@ -1209,6 +1414,10 @@ extern "C" int mbp_reset(mbp_handle* h) {
   // wait for enqueued work (errors are ignored: reset also recovers poisoned handles)
   (void)hipStreamSynchronize(h->st);
   (void)hipStreamSynchronize(h->st2);
+  if (h->d_err) {  // forget an engine timeout
+    (void)hipMemsetAsync(h->d_err, 0, 4, h->st);
+    (void)hipStreamSynchronize(h->st);
+  }
   h->mb_pending = false;
   h->rows.assign(h->sz.B, Row());
   h->batch = 0;

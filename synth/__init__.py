@@ -28,6 +28,7 @@ __all__ = [
     "ModelConfig",
     "Workload",
     "WORKLOADS",
+    "SMALL_F32",
     "manifest",
     "head_manifest_start",
     "make_weights",
@@ -88,6 +89,9 @@ _TINY = ModelConfig(d_model=128, n_heads=4, n_enc=1, n_lm=2, n_nb=1, n_mb=1, hea
 _D1024_LCA = ModelConfig(d_model=1024, n_heads=16, n_enc=2, n_lm=16, n_nb=2, n_mb=2, head="lca", dtype="bf16")
 _D1024_MLP = _D1024_LCA.replace(head="mlp", n_mb=3)
 _D2048 = ModelConfig(d_model=2048, n_heads=32, n_enc=2, n_lm=16, n_nb=2, n_mb=2, head="lca", dtype="bf16")
+# float32 model at the smallest width the persistent engine's register tiles take
+# (d_model 256, head size 64): parity of that path at the float32 tolerance
+SMALL_F32 = ModelConfig(d_model=256, n_heads=4, n_enc=2, n_lm=2, n_nb=2, n_mb=2, head="lca", dtype="f32")
 
 WORKLOADS = {
     "tiny_f32": Workload("tiny_f32", _TINY, batch=1, prompt_len=256, gen_len=128, n=3, tau=0.75),
