@@ -41,6 +41,7 @@ def parse():
     ap.add_argument("--logit-gain", type=float, default=1.0)
     ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for cpu_baseline (0 = skip)")
     ap.add_argument("--no-timing-pass", action="store_true")
+    ap.add_argument("--no-engine", action="store_true", help="one kernel launch per layer operation")
     return ap.parse_args()
 
 
@@ -117,7 +118,7 @@ def main():
     weights = synth.make_weights(model, seed=0, logit_gain=args.logit_gain)
     prompts = [synth.make_prompt(r, wl.prompt_len) for r in range(B)]
     max_ctx = wl.prompt_len + (max(K, W) + 2) * n + 16
-    dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max(n, 8)), weights)
+    dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max(n, 8), engine=not args.no_engine), weights)
     log(f"[bench] weights + init {time.time() - t0:.1f}s")
 
     t0 = time.time()

@@ -584,13 +584,15 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
       }
     } else {
       // keys of this pass: slot j is row f + (j - ns) of kvn (float32, tagged); each
-      // round requests its key and value entries together before waiting
-      for (int j0 = lo + wave * KW; j0 < hi; j0 += EW * KW) {
-        float sc[NR];
+      // round requests its key and value entries together before waiting.  A pass
+      // has at most kEngineMaxRows keys, so NRF rounds cover them.
+      constexpr int NRF = (kEngineMaxRows + KPR - 1) / KPR;
+      for (int j0 = lo + wave * NRF * KPR; j0 < hi; j0 += EW * NRF * KPR) {
+        float sc[NRF];
         float mx = -INFINITY;
-        float vrow[NR][VEC];
+        float vrow[NRF][VEC];
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
+        for (int r = 0; r < NRF; ++r) {
           const int j = j0 + r * KPR + g;
           const bool in = j < hi && f + j - ns < c.M;  // pass rows only
           float dot = 0.f;
@@ -636,7 +638,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
         for (int v = 0; v < VEC; ++v) o[v] *= alpha;
         float ps = 0.f;
 #pragma unroll
-        for (int r = 0; r < NR; ++r) {
+        for (int r = 0; r < NRF; ++r) {
           const float p = (sc[r] == -INFINITY) ? 0.f : expf(sc[r] - m_new);
           ps += p;
 #pragma unroll
@@ -744,10 +746,12 @@ struct Shape {
 };
 
 // Input rows per pass: one for single-row passes, else as many as keep R * MR <= 16
-// accumulators per lane.
-template <int R, bool MULTI>
+// accumulators and MR * KCW <= 4 staged input slices per lane.
+template <int R, int KCW, bool MULTI>
 constexpr int mr_of() {
-  return MULTI ? (R >= 16 ? 1 : (R >= 8 ? 2 : 4)) : 1;
+  int mr = 4;
+  while (mr > 1 && (R * mr > 16 || mr * KCW > 4)) mr /= 2;
+  return MULTI ? mr : 1;
 }
 
 // Every layer of a stack: QKV (RMSNorm, RoPE, KV append) -> split attention ->
@@ -762,18 +766,18 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
 #pragma unroll 1
   for (int l = 0; l < nlayers; ++l) {
     const EOp* o = ops + 6 * l;
-    op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, MULTI>()>(o[0].lin, c, base, base + o[0].tag, err, lds);
+    op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>()>(o[0].lin, c, base, base + o[0].tag, err, lds);
     lds_barrier();
     WPre<W, SH::KCD, SH::NSO, SH::RO> po;
     op_attn<KV, SH::DH>(o[1].at, c, base, base + o[1].tag, err, lds,
                         [&] { weights_ahead<W, SH::KCD, SH::NSO, SH::RO>(o[3].lin, po); });
     lds_barrier();
     op_merge<SH::DH>(o[2].mg, c, base, base + o[2].tag, err);
-    op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, MULTI>()>(o[3].lin, c, base, base + o[3].tag, err, lds, &po);
+    op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>()>(o[3].lin, c, base, base + o[3].tag, err, lds, &po);
     lds_barrier();
-    op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, MULTI>()>(o[4].lin, c, base, base + o[4].tag, err, lds);
+    op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>()>(o[4].lin, c, base, base + o[4].tag, err, lds);
     lds_barrier();
-    op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, MULTI>()>(o[5].lin, c, base, base + o[5].tag, err, lds);
+    op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>()>(o[5].lin, c, base, base + o[5].tag, err, lds);
     lds_barrier();
   }
 }
@@ -781,7 +785,7 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
 // The shapes compiled in (index = EngineShape id).
 // Tiles: 256 tiles (one per block of a 256-CU grid) wherever the row count allows.
 using Shape0 = Shape<uint16_t, _Float16, 64, 1024, 4096, 2, 3, 2, 1, 2, 8, 8, 4>;    // bf16, d 1024
-using Shape1 = Shape<uint16_t, _Float16, 64, 2048, 8192, 4, 6, 4, 4, 4, 8, 8, 8>;    // bf16, d 2048
+using Shape1 = Shape<uint16_t, _Float16, 64, 2048, 8192, 4, 6, 4, 4, 4, 8, 8, 4>;    // bf16, d 2048
 using Shape2 = Shape<float, float, 64, 256, 1024, 1, 1, 1, 1, 1, 1, 4, 1>;           // float32, d 256
 
 template <class SH, bool MULTI>
