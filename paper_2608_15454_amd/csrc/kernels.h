@@ -53,7 +53,8 @@ struct Epi {
 
 // y = W x over M rows.  Input row m is X + (xidx ? xidx[m] : m) * ldx.  With a gain,
 // the row is RMS-normalized and scaled by gain, or by gain2 when gain2 is set and
-// m % gain_period != 0.
+// m % gain_period != 0.  part / part_floats: scratch for split-K partial sums of the
+// matrix-core path (kGemmPartFloats floats; nullptr disables splitting).
 struct Linear {
   const float* X;
   int32_t ldx, M, K, N;
@@ -64,7 +65,11 @@ struct Linear {
   float eps;
   Mats mats;
   Epi epi;
+  float* part;
 };
+
+// Split-K scratch of the matrix-core linear path, in floats.
+constexpr int64_t kGemmPartFloats = (int64_t)1 << 20;
 
 // Attention of M query rows (Q [M, ldq], head h at columns h*dh) over a KV cache.
 struct Attn {

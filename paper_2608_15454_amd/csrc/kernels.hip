@@ -11,6 +11,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 #include "dev.h"
 #include "kernels.h"
 
@@ -238,6 +240,143 @@ __global__ __launch_bounds__(256) void gemm_kernel(Linear L, const float* inv_rm
       for (int j = 0; j < 4; ++j) epi_single(L.epi, m, n + j, acc[i][j]);
     }
   }
+}
+
+// --------------------------------------------------------------- MFMA GEMM ----
+// Y = epi(RMSNorm(X) W^T) for bfloat16 weights on the matrix cores: a 64x64 output
+// tile per block of four waves, each wave one 32x32 tile of
+// v_mfma_f32_32x32x16_bf16 (operand A: row l%32, k (l/32)*8..+8 of the lane's 16-byte
+// fragment; B likewise by column; result lane l, register r = column l%32, row
+// 8(r/4) + 4(l/32) + r%4).  K advances 64 at a time; the next step's X rows and weight
+// rows are loaded into registers while the current step's MFMAs run.  X is float32:
+// each normalized value is split into bfloat16 hi + lo (hi = bf16(x), lo = bf16(x -
+// hi), 16 significant bits together) and both halves go through the matrix cores, so
+// the product keeps float32-like accuracy (weights are bfloat16 already).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kMfmaBK = 64, kMfmaLD = kMfmaBK + 8;  // LDS row pitch in bf16 elements (pad against bank conflicts)
+
+// With ksplit > 1, block z covers K steps [z*nk/ksplit, (z+1)*nk/ksplit) and writes its
+// raw sums to L.part[z][m][n]; gemm_finish_kernel adds the splits and applies the
+// epilogue.
+__global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, const float* inv_rms, int ksplit) {
+  constexpr int BM = 64, BN = 64, BK = kMfmaBK, LD = kMfmaLD;
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LD];  // hi halves of X
+  __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LD];  // lo halves of X
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LD];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // loads: thread t stages 16 consecutive k of row t/4 of both tiles
+  const int lr = tid >> 2, lk = (tid & 3) * 16;
+  const int am = m0 + lr;
+  const bool aok = am < L.M;
+  const float* arow = L.X + (size_t)(aok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx;
+  const bool norm = L.gain != nullptr;
+  const float ascale = (norm && aok) ? inv_rms[am] : 1.0f;
+  const float* ag = norm ? row_gain(L, aok ? am : 0) : nullptr;
+  const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K);
+  float a[16];
+  uint4 b0, b1;
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int v = 0; v < 16; v += 4) {
+      float4 t = aok ? *reinterpret_cast<const float4*>(arow + k0 + lk + v) : make_float4(0.f, 0.f, 0.f, 0.f);
+      if (norm && aok) {
+        const float4 g = *reinterpret_cast<const float4*>(ag + k0 + lk + v);
+        t.x *= ascale * g.x; t.y *= ascale * g.y; t.z *= ascale * g.z; t.w *= ascale * g.w;
+      }
+      a[v] = t.x; a[v + 1] = t.y; a[v + 2] = t.z; a[v + 3] = t.w;
+    }
+    b0 = *reinterpret_cast<const uint4*>(brow + k0 + lk);
+    b1 = *reinterpret_cast<const uint4*>(brow + k0 + lk + 8);
+  };
+  auto stage = [&](int buf) {
+    uint32_t p[8], q[8];
+#pragma unroll
+    for (int v = 0; v < 8; ++v) {
+      const uint16_t h0 = f2bf(a[2 * v]), h1 = f2bf(a[2 * v + 1]);
+      const uint16_t l0 = f2bf(a[2 * v] - bf2f(h0)), l1 = f2bf(a[2 * v + 1] - bf2f(h1));
+      p[v] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+      q[v] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+    }
+    uint4* ad = reinterpret_cast<uint4*>(&As[buf][lr * LD + lk]);
+    ad[0] = make_uint4(p[0], p[1], p[2], p[3]);
+    ad[1] = make_uint4(p[4], p[5], p[6], p[7]);
+    uint4* al = reinterpret_cast<uint4*>(&Al[buf][lr * LD + lk]);
+    al[0] = make_uint4(q[0], q[1], q[2], q[3]);
+    al[1] = make_uint4(q[4], q[5], q[6], q[7]);
+    uint4* bd = reinterpret_cast<uint4*>(&Bs[buf][lr * LD + lk]);
+    bd[0] = b0;
+    bd[1] = b1;
+  };
+  const int wm = wave >> 1, wn = wave & 1;
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  const int nk_all = L.K / BK;
+  const int kt0 = (int)((int64_t)blockIdx.z * nk_all / ksplit), kt1 = (int)((int64_t)(blockIdx.z + 1) * nk_all / ksplit);
+  fetch(kt0 * BK);
+  stage(0);
+  __syncthreads();
+  for (int kt = kt0; kt < kt1; ++kt) {
+    const int cur = (kt - kt0) & 1;
+    if (kt + 1 < kt1) fetch((kt + 1) * BK);  // in flight during this step's MFMAs
+    const int aoff = (wm * 32 + (lane & 31)) * LD + (lane >> 5) * 8;
+    const uint16_t* ab = &As[cur][aoff];
+    const uint16_t* alo = &Al[cur][aoff];
+    const uint16_t* bb = &Bs[cur][(wn * 32 + (lane & 31)) * LD + (lane >> 5) * 8];
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 16) {
+      const bf16x8 fa = *reinterpret_cast<const bf16x8*>(ab + ks);
+      const bf16x8 fl = *reinterpret_cast<const bf16x8*>(alo + ks);
+      const bf16x8 fb = *reinterpret_cast<const bf16x8*>(bb + ks);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fl, fb, acc, 0, 0, 0);
+    }
+    if (kt + 1 < kt1) stage(cur ^ 1);
+    __syncthreads();
+  }
+  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+  const int j = lane & 31;
+  const int n = n0 + wn * 32 + j;
+  if (ksplit > 1) {
+    float* pp = L.part + (size_t)blockIdx.z * L.M * L.N;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      if (m < L.M) pp[(size_t)m * L.N + n] = acc[r];
+    }
+    return;
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+    const float val = acc[r];
+    const float partner = __shfl_down(val, 1);  // column n + 1, same row
+    if (m >= L.M) continue;
+    if (!pair) epi_single(L.epi, m, n, val);
+    else if ((j & 1) == 0) epi_pair(L.epi, m, n, val, partner);
+  }
+}
+
+// Sum of the ksplit partials of gemm_mfma_kernel and the epilogue, one thread per
+// output (or output pair for SwiGLU / QKV).
+__global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) {
+  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+  const int per_row = pair ? L.N / 2 : L.N;
+  const int64_t idx = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)L.M * per_row) return;
+  const int m = (int)(idx / per_row);
+  const int n = (int)(idx - (int64_t)m * per_row) * (pair ? 2 : 1);
+  float a0 = 0.f, a1 = 0.f;
+  for (int z = 0; z < ksplit; ++z) {
+    const float* pp = L.part + ((size_t)z * L.M + m) * L.N + n;
+    a0 += pp[0];
+    if (pair) a1 += pp[1];
+  }
+  if (pair) epi_pair(L.epi, m, n, a0, a1);
+  else epi_single(L.epi, m, n, a0);
 }
 
 // ------------------------------------------------------------- attention ------
@@ -655,8 +794,37 @@ hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
   return klaunch(gemv_kernel<W, 1, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
 }
 
+// Linears of more rows than this use the matrix cores (bfloat16 weights).
+constexpr int kMfmaMinRows = 16;
+
+template <typename W>
+bool mfma_fits(const Linear& L) {
+  return std::is_same<W, uint16_t>::value && L.M > kMfmaMinRows && L.N % 64 == 0 && L.K % kMfmaBK == 0;
+}
+
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
+  if (mfma_fits<W>(L)) {
+    // split K until about 256 blocks stream the weights (the partials must fit)
+    const int tiles = (L.N / 64) * ((L.M + 63) / 64);
+    const int nk = L.K / kMfmaBK;
+    int ks = 1;
+    while (L.part != nullptr && tiles * ks * 2 <= 256 && ks * 2 <= nk &&
+           (int64_t)ks * 2 * L.M * L.N <= kGemmPartFloats)
+      ks *= 2;
+    const dim3 grid(L.N / 64, (L.M + 63) / 64, ks);
+    const bool first_is_rms = L.gain != nullptr;
+    if (first_is_rms) {
+      hipError_t e = klaunch(rms_kernel, dim3((L.M + 3) / 4), dim3(256), 0, st, ev.start, nullptr, L, inv_rms);
+      if (e != hipSuccess) return e;
+    }
+    hipError_t e = klaunch(gemm_mfma_kernel, grid, dim3(256), 0, st, first_is_rms ? nullptr : ev.start,
+                           ks > 1 ? nullptr : ev.stop, L, (const float*)inv_rms, ks);
+    if (e != hipSuccess || ks == 1) return e;
+    const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+    const int64_t items = (int64_t)L.M * (pair ? L.N / 2 : L.N);
+    return klaunch(gemm_finish_kernel, dim3((unsigned)((items + 255) / 256)), dim3(256), 0, st, nullptr, ev.stop, L, ks);
+  }
   if (gemv_fits<W>(L)) {
     switch (L.K / (64 * WT<W>::VEC)) {
       case 1: return gemv_launch<W, 1>(L, st, ev);
@@ -710,7 +878,9 @@ hipError_t attn_prefill_t(const Attn& a, const int32_t* tiles, int ntiles, hipSt
 
 }  // namespace
 
-bool linear_is_gemv(const Linear& L, int wdt) { return wdt ? gemv_fits<uint16_t>(L) : gemv_fits<float>(L); }
+bool linear_is_gemv(const Linear& L, int wdt) {
+  return wdt ? (!mfma_fits<uint16_t>(L) && gemv_fits<uint16_t>(L)) : gemv_fits<float>(L);
+}
 
 hipError_t launch_linear(const Linear& L, int wdt, float* inv_rms, hipStream_t st, const Ev& ev) {
   if (L.M <= 0) return hipSuccess;

@@ -74,11 +74,11 @@ struct Sizes {
 // Per-pass scratch: residual stream X, queries, attention output, FFN hidden,
 // row norms of the tiled GEMM, split-attention partials.
 struct ScratchOff {
-  size_t X, Q, O, Hid, inv, part;
+  size_t X, Q, O, Hid, inv, part, gpart;
 };
 
 struct Scratch {
-  float *X, *Q, *O, *Hid, *inv, *part;
+  float *X, *Q, *O, *Hid, *inv, *part, *gpart;  // gpart: split-K partials of the GEMM
   int64_t part_floats;
 };
 
@@ -204,6 +204,7 @@ Regions layout(const mbp_config& c) {
   r.main.Hid = take((size_t)s.Ml * s.dff * 4);
   r.main.inv = take((size_t)s.Ml * 4);
   r.main.part = take((size_t)s.part_floats * 4);
+  r.main.gpart = take((size_t)kGemmPartFloats * 4);
   // MB-window scratch: B * Wcap rows
   r.mb.X = take((size_t)s.Mm * s.d * 4);
   r.mb.Q = take((size_t)s.Mm * s.d * 4);
@@ -211,6 +212,7 @@ Regions layout(const mbp_config& c) {
   r.mb.Hid = take((size_t)s.Mm * s.dff * 4);
   r.mb.inv = take((size_t)s.Mm * 4);
   r.mb.part = take((size_t)std::max<int64_t>(s.part_floats_mb, 1) * 4);
+  r.mb.gpart = take((size_t)kGemmPartFloats * 4);
   r.plan_ints = (size_t)20 * s.Ml + (size_t)s.B * s.Wcap + 64;
   for (int i = 0; i < kPlans; ++i) r.plan[i] = take(r.plan_ints * 4);
   r.active = take((size_t)s.B * 4);
@@ -469,7 +471,9 @@ double linear_bytes(const mbp_handle* h, const Linear& L) {
   return N * K * wb + M * K * 4 + out;
 }
 
-int run_linear(mbp_handle* h, const Linear& L, float* inv, hipStream_t st) {
+int run_linear(mbp_handle* h, Linear L, const Scratch& sc, hipStream_t st) {
+  L.part = sc.gpart;
+  float* inv = sc.inv;
   const int cls = linear_is_gemv(L, h->wdt) ? MBP_KCLASS_GEMV : MBP_KCLASS_GEMM;
   TIMED(h, cls, linear_bytes(h, L), launch_linear, L, h->wdt, inv, st);
   return MBP_OK;
@@ -588,7 +592,7 @@ int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, fl
     qkv.epi.kind = EPI_QKV; qkv.epi.Q = sc.Q; qkv.epi.kc = kc; qkv.epi.vc = vc;
     qkv.epi.b_stride = kv.b_stride; qkv.epi.cap = kv.cap; qkv.epi.H = s.H; qkv.epi.dh = s.dh; qkv.epi.d = s.d;
     qkv.epi.rope = h->rope; qkv.epi.tok = tok; qkv.epi.kvt = h->cfg.kv_dtype;
-    RCK(run_linear(h, qkv, sc.inv, st));
+    RCK(run_linear(h, qkv, sc, st));
 
     Attn a{};
     a.Q = sc.Q; a.ldq = s.d; a.kc = kc; a.vc = vc; a.b_stride = kv.b_stride; a.cap = kv.cap;
@@ -604,20 +608,20 @@ int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, fl
     o.X = sc.O; o.ldx = s.d; o.M = M; o.K = s.d; o.N = s.d; o.gain = nullptr;
     o.mats.m[0] = w.wo; o.mats.rows = s.d; o.mats.mode = MAT_SINGLE;
     o.epi.kind = EPI_RESID; o.epi.Y = X; o.epi.ldy = s.d;
-    RCK(run_linear(h, o, sc.inv, st));
+    RCK(run_linear(h, o, sc, st));
 
     Linear gu{};
     gu.X = X; gu.ldx = s.d; gu.M = M; gu.K = s.d; gu.N = 2 * s.dff;
     gu.gain = w.ffn_norm; gu.eps = h->cfg.rms_eps;
     gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
     gu.epi.kind = EPI_SWIGLU; gu.epi.Y = sc.Hid; gu.epi.ldy = s.dff;
-    RCK(run_linear(h, gu, sc.inv, st));
+    RCK(run_linear(h, gu, sc, st));
 
     Linear dn{};
     dn.X = sc.Hid; dn.ldx = s.dff; dn.M = M; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
     dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
     dn.epi.kind = EPI_RESID; dn.epi.Y = X; dn.epi.ldy = s.d;
-    RCK(run_linear(h, dn, sc.inv, st));
+    RCK(run_linear(h, dn, sc, st));
   }
   return MBP_OK;
 }
@@ -923,12 +927,12 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
       gu.X = h1; gu.ldx = s.d; gu.M = B; gu.K = s.d; gu.N = 2 * s.dff; gu.gain = w.norm; gu.eps = c.rms_eps;
       gu.mats.m[0] = w.wg; gu.mats.m[1] = w.wu; gu.mats.rows = s.dff; gu.mats.mode = MAT_GATEUP;
       gu.epi.kind = EPI_SWIGLU; gu.epi.Y = sc.Hid; gu.epi.ldy = s.dff;
-      RCK(run_linear(h, gu, sc.inv, h->st));
+      RCK(run_linear(h, gu, sc, h->st));
       Linear dn{};
       dn.X = sc.Hid; dn.ldx = s.dff; dn.M = B; dn.K = s.dff; dn.N = s.d; dn.gain = nullptr;
       dn.mats.m[0] = w.wd; dn.mats.rows = s.d; dn.mats.mode = MAT_SINGLE;
       dn.epi.kind = EPI_RESID; dn.epi.Y = mlp_out + (size_t)m * s.d; dn.epi.ldy = s.nmax * s.d;
-      RCK(run_linear(h, dn, sc.inv, h->st));
+      RCK(run_linear(h, dn, sc, h->st));
     }
   }
   // head: RMSNorm with the head's gain (NT norm for candidate 1, MB norm for the LCA
@@ -938,7 +942,7 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
   un.gain = h->g_nt; un.gain2 = lca ? h->g_mb : nullptr; un.gain_period = n; un.eps = c.rms_eps;
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
-  RCK(run_linear(h, un, sc.inv, h->st));
+  RCK(run_linear(h, un, sc, h->st));
   OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
         h->engine ? h->d_err : nullptr, h->st);
   h->n_hint = n;
@@ -1181,6 +1185,7 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
     x.Hid = h->R<float>(o.Hid);
     x.inv = h->R<float>(o.inv);
     x.part = h->R<float>(o.part);
+    x.gpart = h->R<float>(o.gpart);
     x.part_floats = pf;
     return x;
   };
@@ -1290,7 +1295,7 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   un.X = X; un.ldx = s.d; un.M = B * n; un.K = s.d; un.N = 256; un.gain = h->g_nt; un.eps = c.rms_eps;
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
-  RCK(run_linear(h, un, h->sc_main.inv, h->st));
+  RCK(run_linear(h, un, h->sc_main, h->st));
   OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len,
         h->engine ? h->d_err : nullptr, h->st);
   HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
