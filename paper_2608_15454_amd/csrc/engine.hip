@@ -28,13 +28,18 @@ using namespace dev;
 constexpr int EB = 512;            // threads per block
 constexpr int EW = EB / 64;        // waves per block
 constexpr int kLdsFloats = 16384;  // 64 KiB of LDS per block
-constexpr int kStage = kLdsFloats - 64;  // staged input rows; the last 64 floats hold row scalars
+constexpr int kSsFloats = kEngineMaxRows * EW;  // per-wave sums of squares of staged rows
+constexpr int kStage = kLdsFloats - kSsFloats;   // staged input rows; the rest holds the sums
 constexpr uint64_t kWaitTicks = 20000000ull;  // 200 ms of the 100 MHz real-time counter
 
 // Device-memory accesses go through global address-space pointers: the operands
 // come from descriptors in memory, and generic (flat) accesses would also count in
 // the counter the scalar descriptor loads wait on, serializing the weight stream.
 #define GLOBAL __attribute__((address_space(1)))
+// The operation descriptors are read through the constant address space: they do
+// not change during a launch, so every field read is a scalar load (a generic or
+// global read would be a vector load, queued behind the wave's weight requests).
+#define CONST_AS __attribute__((address_space(4)))
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
@@ -115,63 +120,111 @@ __device__ __forceinline__ float ein_get(const EIn& x, const ECall& c, int m, in
   return gld(f + (size_t)m * x.ld + k);
 }
 
-// out[v] = entries p[0..N) carrying tag: all N loads are in flight before the first wait.
-template <int N>
-__device__ __forceinline__ void ll_get_n(const uint64_t* p, uint32_t tag, int* err, float* out) {
-  uint64_t v[N];
+// Waits until every entry v[j] with bit j of live set carries tag; addr(j) is the
+// address v[j] was loaded from.  The stale entries of the batch are requested again
+// together, so waiting costs one round trip per retry rather than one per entry.
+// After a timeout anywhere in the launch (err set) it returns at once, so the
+// launch still finishes.
+template <int N, class Addr>
+__device__ __forceinline__ void ll_settle(uint64_t (&v)[N], Addr&& addr, uint32_t live, uint32_t tag, int* err) {
+  auto any_stale = [&] {
+    bool st = false;
 #pragma unroll
-  for (int j = 0; j < N; ++j) v[j] = ll_load(p + j);
+    for (int j = 0; j < N; ++j) st |= ((live >> j) & 1u) && (uint32_t)(v[j] >> 32) != tag;
+    return st;
+  };
+  if (__builtin_amdgcn_ballot_w64(any_stale()) == 0) return;
+  const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  for (int it = 1;; ++it) {
+    if ((it & 15) == 0) {
+      if (err_get(err) != 0) return;
+      if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
+        __hip_atomic_store((GLOBAL int*)err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
+      }
+    }
+    __builtin_amdgcn_s_sleep(1);
 #pragma unroll
-  for (int j = 0; j < N; ++j) out[j] = ll_take(v[j], p + j, tag, err);
+    for (int j = 0; j < N; ++j)
+      if ((live >> j) & 1u) v[j] = ll_load(addr(j));
+    if (__builtin_amdgcn_ballot_w64(any_stale()) == 0) return;
+  }
 }
 
 // lds[(m - m0) * K + k] = x[m][k] for rows m0 .. m0+mc-1.  Tagged rows are requested
-// eight entries per thread at a time; only entries whose tag is stale are polled.
+// eight entries per thread at a time.  With ssw, wave w adds the squares of the
+// entries it staged to ssw[(m - m0) * EW + w]: the 64 entries of one tagged load
+// (256 of a plain one) lie in one row because K is a multiple of 256.
 __device__ __forceinline__ void stage_rows(const EIn& x, const ECall& c, int m0, int mc, int K, float* lds, uint32_t base,
-                           int* err) {
+                                           int* err, float* ssw) {
   const int n = mc * K;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  float acc = 0.f;
+  int row = -1;  // the row acc belongs to (wave-uniform)
+  auto flush = [&] {
+    if (row >= 0) {
+      const float t = wave_sum(acc);
+      if (lane == 0) ssw[row * EW + wave] += t;
+    }
+  };
+  auto add = [&](int m, float sq) {
+    if (m != row) {
+      flush();
+      row = m;
+      acc = 0.f;
+    }
+    acc += sq;
+  };
   if (x.ll == nullptr) {
     const float* f = x.f != nullptr ? x.f : c.x;
-    for (int e = threadIdx.x * 4; e < n; e += EB * 4) {
-      const int m = e / K, k = e - m * K;
-      *reinterpret_cast<float4*>(lds + e) = ld16f(f + (size_t)(m0 + m) * x.ld + k);
+    for (int eb = wave * 256; eb < n; eb += EB * 4) {
+      const int m = eb / K;
+      const int e = eb + lane * 4;
+      const float4 t = ld16f(f + (size_t)(m0 + m) * x.ld + (e - m * K));
+      *reinterpret_cast<float4*>(lds + e) = t;
+      if (ssw != nullptr) add(m, t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w);
     }
-    return;
-  }
-  const uint32_t tag = base + x.tag;
-  constexpr int U = 8;
-  for (int e0 = threadIdx.x; e0 < n; e0 += EB * U) {
-    uint64_t v[U];
-    const uint64_t* p[U];
+  } else {
+    const uint32_t tag = base + x.tag;
+    constexpr int U = 8;
+    for (int eb = wave * 64; eb < n; eb += EB * U) {
+      // entry j of the batch: the wave's 64 entries from ej = eb + j*EB (uniform)
+      auto addr = [&](int j) {
+        const int ej = min(eb + j * EB, n - 64);
+        const int m = ej / K;
+        return x.ll + (size_t)(m0 + m) * x.ld + (ej - m * K) + lane;
+      };
+      uint64_t v[U];
+      uint32_t live = 0;
 #pragma unroll
-    for (int j = 0; j < U; ++j) {
-      const int e = e0 + j * EB;
-      const int m = e / K, k = e - m * K;
-      p[j] = x.ll + (size_t)(m0 + m) * x.ld + k;
-      v[j] = e < n ? ll_load(p[j]) : 0ull;
-    }
+      for (int j = 0; j < U; ++j) {
+        const bool in = eb + j * EB < n;
+        v[j] = in ? ll_load(addr(j)) : 0ull;
+        live |= in ? 1u << j : 0u;
+      }
+      ll_settle<U>(v, addr, live, tag, err);
 #pragma unroll
-    for (int j = 0; j < U; ++j) {
-      const int e = e0 + j * EB;
-      if (e < n) lds[e] = ll_take(v[j], p[j], tag, err);
+      for (int j = 0; j < U; ++j) {
+        const int ej = eb + j * EB;
+        if (ej < n) {
+          const float val = __uint_as_float((uint32_t)v[j]);
+          lds[ej + lane] = val;
+          if (ssw != nullptr) add(ej / K, val * val);
+        }
+      }
     }
   }
+  if (ssw != nullptr) flush();
 }
 
-// inv[m] = 1 / sqrt(mean(x[m]^2) + eps) for the staged rows.
-__device__ __forceinline__ void stage_inv(const float* lds, int mc, int K, float eps, float* inv) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int m = wave; m < mc; m += EW) {
-    float ss = 0.f;
-    for (int k = lane; k < K; k += 64) {
-      const float v = lds[m * K + k];
-      ss += v * v;
-    }
-    ss = wave_sum(ss);
-    if (lane == 0) inv[m] = 1.0f / sqrtf(ss / (float)K + eps);
-  }
+// 1 / RMS of staged row m from the per-wave sums of squares.
+__device__ __forceinline__ float row_scale(const float* ssw, int m, int K, float eps) {
+  float ss = 0.f;
+#pragma unroll
+  for (int w = 0; w < EW; ++w) ss += ssw[m * EW + w];
+  return 1.0f / sqrtf(ss / (float)K + eps);
 }
-
 // ------------------------------------------------------------------ linear ----
 // A block computes tiles of RB = (EW / NS) * R consecutive output rows.  The waves of
 // a block form EW / NS row groups of NS waves; wave (group g, slice s) holds rows
@@ -236,9 +289,10 @@ __device__ __forceinline__ void cache_put2(void* cache, int kvt, size_t off, flo
 }
 
 // Output columns (n, n+1), n even: SwiGLU of a (gate, up) pair, or a rotated q / k
-// pair or a v pair of the fused QKV projection (k and v also go to the cache).
+// pair or a v pair of the fused QKV projection (k and v also go to the cache).  csp:
+// the rotation of the pair when already loaded, else read from the table.
 __device__ __forceinline__ void epi_pair(const ELinear& L, const ECall& c, int m, int n, float a0, float a1,
-                                         uint32_t tag, int pos, int b, int slot) {
+                                         uint32_t tag, int pos, int b, int slot, const float2* csp) {
   if (L.epi == EPI_SWIGLU) {
     out_store(L, c, m, n >> 1, silu(a0) * a1, tag);
     return;
@@ -247,7 +301,13 @@ __device__ __forceinline__ void epi_pair(const ELinear& L, const ECall& c, int m
   const int which = n / d, col = n - which * d;
   const int h = col / L.dh, ee = col - h * L.dh;
   if (which < 2) {
-    const v2f cs = *(const GLOBAL v2f*)(L.rope + (size_t)pos * (L.dh >> 1) + (ee >> 1));
+    v2f cs;
+    if (csp != nullptr) {
+      cs.x = csp->x;
+      cs.y = csp->y;
+    } else {
+      cs = *(const GLOBAL v2f*)(L.rope + (size_t)pos * (L.dh >> 1) + (ee >> 1));
+    }
     const float r0 = a0 * cs.x - a1 * cs.y;
     const float r1 = a0 * cs.y + a1 * cs.x;
     a0 = r0;
@@ -276,15 +336,15 @@ struct Pow2<1> {
 };
 
 // Partial dot products of the wave's R rows (K-slice from kc0) with the staged
-// input rows 0..mc-1, MR rows at a time, into part[slice][row in tile][m].
-template <typename W, int R, int KCW, int MR>
-__device__ __forceinline__ void slice_dots(const ELinear& L, const uint4 (&wv)[R][KCW],
-                                           const float4 (&gv)[KCW][WT<W>::VEC / 4], int kc0, const float* x, int K,
-                                           int mc, float* part_s, int r0) {
+// input rows 0..mc-1, MR rows at a time, into part[slice][row in tile][m].  NORM:
+// the inputs are scaled by the norm gain gv of the same columns (the per-row RMS
+// factor is applied in the epilogue).
+template <typename W, int R, int KCW, int MR, bool NORM, int GD>
+__device__ __forceinline__ void slice_dots(const uint4 (&wv)[R][KCW], const float4 (&gv)[GD][WT<W>::VEC / 4], int kc0,
+                                           const float* x, int K, int mc, float* part_s, int r0) {
   constexpr int VEC = WT<W>::VEC;
   constexpr int V = Pow2<R * MR>::value, LPV = 64 / V;
   const int lane = threadIdx.x & 63;
-  const bool norm = L.gain != nullptr;
   for (int mm = 0; mm < mc; mm += MR) {
     float acc[V];
 #pragma unroll
@@ -295,7 +355,7 @@ __device__ __forceinline__ void slice_dots(const ELinear& L, const uint4 (&wv)[R
       float g[VEC];
 #pragma unroll
       for (int v = 0; v < VEC; v += 4) {
-        const float4 t = norm ? gv[cc][v / 4] : make_float4(1.f, 1.f, 1.f, 1.f);
+        const float4 t = NORM ? gv[NORM ? cc : 0][v / 4] : make_float4(1.f, 1.f, 1.f, 1.f);
         g[v] = t.x; g[v + 1] = t.y; g[v + 2] = t.z; g[v + 3] = t.w;
       }
 #pragma unroll
@@ -328,96 +388,126 @@ struct NoHook {
   __device__ __forceinline__ void operator()() const {}
 };
 
-// Weight slice of a wave for the first tile of a linear layer, requested by the
-// operation before it (see the kernel loop).
-template <typename W, int KC, int NS, int R>
+// A wave's weight slice (and norm gain slice) for the first tile of a linear layer,
+// requested ahead of the layer by an earlier operation.
+template <typename W, int KC, int NS, int R, bool NORM>
 struct WPre {
-  uint4 wv[R][KC / NS];
+  static constexpr int KCW = KC / NS, GD = NORM ? KC / NS : 1;
+  uint4 wv[R][KCW];
+  float4 gv[GD][WT<W>::VEC / 4];
 };
 
-template <typename W, int KC, int NS, int R>
-__device__ __forceinline__ void weights_ahead(const ELinear& L, WPre<W, KC, NS, R>& p) {
-  constexpr int RB = (EW / NS) * R;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  load_w<W, R, KC / NS>(L, blockIdx.x * RB + (wave / NS) * R, (wave % NS) * (KC / NS), p.wv);
+template <typename W, int KCW, int GD>
+__device__ __forceinline__ void load_g(const ELinear& L, int kc0, float4 (&gv)[GD][WT<W>::VEC / 4]) {
+  constexpr int VEC = WT<W>::VEC;
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int cc = 0; cc < GD; ++cc)
+#pragma unroll
+    for (int v = 0; v < VEC / 4; ++v) gv[cc][v] = ld16f(L.gain + (kc0 + cc) * 64 * VEC + lane * VEC + 4 * v);
 }
 
-// pre: the first tile's weight slice when the previous operation requested it
-// (nullptr: requested here).  late: runs right after this operation's input poll
-// (the next operation's requests, in flight while this one computes).
-template <typename W, int KC, int NS, int R, int MR, class Late = NoHook>
+template <typename W, int KC, int NS, int R, bool NORM>
+__device__ __forceinline__ void weights_ahead(const ELinear& L, WPre<W, KC, NS, R, NORM>& p) {
+  constexpr int RB = (EW / NS) * R, KCW = KC / NS;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int kc0 = (wave % NS) * KCW;
+  load_w<W, R, KCW>(L, blockIdx.x * RB + (wave / NS) * R, kc0, p.wv);
+  if (NORM) load_g<W, KCW>(L, kc0, p.gv);
+}
+
+// A thread's first output item of a linear layer (first tile, first input chunk):
+// row m and offset rr of its column (pair) in the tile.
+struct Item0 {
+  int m, rr;
+  bool live;
+};
+
+template <int RB>
+__device__ __forceinline__ Item0 item0(int M, int K, int N, bool pair) {
+  const int mcap = min(min(M, kEngineMaxRows), (kStage - kPartFloats) / K);
+  const int mc0 = min(mcap, M);
+  Item0 it;
+  it.m = threadIdx.x % mc0;
+  it.rr = (threadIdx.x / mc0) * (pair ? 2 : 1);
+  it.live = (int)threadIdx.x < (pair ? RB / 2 : RB) * mc0 && (int)blockIdx.x * RB + it.rr < N;
+  return it;
+}
+
+// Epilogue operands of a thread's first item of the fused QKV projection.  They
+// are the same in every layer of a launch: the row's position, batch row and cache
+// slot, and the rotation of the item's column pair.
+struct QkvItem {
+  int pos, b, slot;
+  float2 cs;
+};
+
+// pre: the first tile's weight slice, requested by an earlier operation.  qi: the
+// QKV epilogue operands (EPI_QKV).  next: runs once, after this operation's output
+// stores are issued (it requests a later operation's weights, which are then in
+// flight during the next input poll).
+template <typename W, int KC, int NS, int R, int MR, bool NORM, class Next = NoHook>
 __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint32_t base, uint32_t tag, int* err,
-                                          float* lds, const WPre<W, KC, NS, R>* pre = nullptr, Late&& late = Late()) {
-  constexpr int KCW = KC / NS;
+                                          float* lds, const WPre<W, KC, NS, R, NORM>& pre, const QkvItem* qi,
+                                          Next&& next = Next()) {
+  constexpr int KCW = KC / NS, GD = NORM ? KCW : 1;
   constexpr int RB = (EW / NS) * R;
   static_assert(KC % NS == 0 && EW % NS == 0 && NS * RB * 16 <= kPartFloats, "linear tiling");
   float* x = lds;
   float* part = lds + kStage - kPartFloats;
-  float* inv = lds + kStage;
+  float* ssw = lds + kStage;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int slice = wave % NS, rgrp = wave / NS;
   const int kc0 = slice * KCW;
   const int M = c.M;
-  const int mcap = min(min(M, 16), (kStage - kPartFloats) / L.K);
+  const int mcap = min(min(M, kEngineMaxRows), (kStage - kPartFloats) / L.K);
   const int nch = (M + mcap - 1) / mcap;
   const int ntiles = (L.N + RB - 1) / RB;
   const int rounds = (ntiles + gridDim.x - 1) / gridDim.x;
   const bool pair = L.epi == EPI_SWIGLU || L.epi == EPI_QKV;
-  // epilogue operands of this thread's item in the first tile and chunk (at most one:
-  // RB * 16 <= EB), requested with the weights, before the input poll
-  const int mc0 = min(mcap, M);
-  const int e0_m = threadIdx.x % mc0, e0_rr = (threadIdx.x / mc0) * (pair ? 2 : 1);
-  const bool e0_live = (int)threadIdx.x < (pair ? RB / 2 : RB) * mc0 && (int)blockIdx.x * RB + e0_rr < L.N;
+  // the residual operand of this thread's first item (at most one item per thread
+  // and chunk: RB * 16 <= EB), requested before the input poll
+  const Item0 i0 = item0<RB>(M, L.K, L.N, pair);
   uint64_t e0_res = 0;
-  int e0_pos = 0, e0_b = 0, e0_slot = 0;
-  if (e0_live) {
-    if (L.epi == EPI_RESID) {
-      const int n = blockIdx.x * RB + e0_rr;
-      if (L.resid.ll != nullptr) {
-        e0_res = ll_load(L.resid.ll + (size_t)e0_m * L.resid.ld + n);
-      } else {
-        const float* f = L.resid.f != nullptr ? L.resid.f : c.x;
-        e0_res = __float_as_uint(gld(f + (size_t)e0_m * L.resid.ld + n));
-      }
-    } else if (L.epi == EPI_QKV) {
-      e0_pos = gld(c.tok.pos + e0_m);
-      e0_b = gld(c.tok.b + e0_m);
-      e0_slot = gld(c.tok.slot + e0_m);
+  if (i0.live && L.epi == EPI_RESID) {
+    const int n = blockIdx.x * RB + i0.rr;
+    if (L.resid.ll != nullptr) {
+      e0_res = ll_load(L.resid.ll + (size_t)i0.m * L.resid.ld + n);
+    } else {
+      const float* f = L.resid.f != nullptr ? L.resid.f : c.x;
+      e0_res = __float_as_uint(gld(f + (size_t)i0.m * L.resid.ld + n));
     }
   }
-  for (int t = 0; t < rounds; ++t) {
+  // one round: a tile of RB output rows over all input chunks.  fast: the common
+  // case of one round and one chunk, where next() runs right after the dot products
+  // (otherwise after the last round, so that no weights stay live across the loops)
+  auto round = [&](int t, bool fast) {
     const int tile = blockIdx.x + t * gridDim.x;
     const int nt0 = tile * RB;  // first row of the tile (>= N: no rows)
     uint4 wv[R][KCW];
-    if (t == 0 && pre != nullptr) {
+    float4 gv[GD][WT<W>::VEC / 4];
+    if (t == 0) {
 #pragma unroll
       for (int r = 0; r < R; ++r)
 #pragma unroll
-        for (int cc = 0; cc < KCW; ++cc) wv[r][cc] = pre->wv[r][cc];
+        for (int cc = 0; cc < KCW; ++cc) wv[r][cc] = pre.wv[r][cc];
+#pragma unroll
+      for (int cc = 0; cc < GD; ++cc)
+#pragma unroll
+        for (int v = 0; v < WT<W>::VEC / 4; ++v) gv[cc][v] = pre.gv[cc][v];
     } else {
       load_w<W, R, KCW>(L, nt0 + rgrp * R, kc0, wv);  // issued before the input poll
-    }
-    float4 gv[KCW][WT<W>::VEC / 4];                  // the norm gain of the same columns
-    if (L.gain != nullptr) {
-      constexpr int VEC = WT<W>::VEC;
-      const int lane = threadIdx.x & 63;
-#pragma unroll
-      for (int cc = 0; cc < KCW; ++cc)
-#pragma unroll
-        for (int v = 0; v < VEC / 4; ++v) gv[cc][v] = ld16f(L.gain + (kc0 + cc) * 64 * VEC + lane * VEC + 4 * v);
+      if (NORM) load_g<W, KCW>(L, kc0, gv);
     }
     // one chunk of staged input rows: stage (unless reused), dot products, epilogue
-    auto chunk = [&](int m0, int mc, bool stage) {
+    auto chunk = [&](int m0, int mc, bool stage, bool last) {
       if (stage) {
+        if (NORM)
+          for (int i = threadIdx.x; i < kSsFloats; i += EB) ssw[i] = 0.f;
         lds_barrier();
-        stage_rows(L.x, c, m0, mc, L.K, x, base, err);
+        stage_rows(L.x, c, m0, mc, L.K, x, base, err, NORM ? ssw : nullptr);
         lds_barrier();
-        if (L.gain != nullptr) {
-          stage_inv(x, mc, L.K, L.eps, inv);
-          lds_barrier();
-        }
       }
-      if (t == 0 && m0 == 0) late();
       // first use of the weights here, after the input poll: without this anchor the
       // compiler hoists their unpacking above the poll and waits for them first
 #pragma unroll
@@ -425,7 +515,7 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
 #pragma unroll
         for (int cc = 0; cc < KCW; ++cc)
           asm volatile("" : "+v"(wv[r][cc].x), "+v"(wv[r][cc].y), "+v"(wv[r][cc].z), "+v"(wv[r][cc].w));
-      if (nt0 < L.N) slice_dots<W, R, KCW, MR>(L, wv, gv, kc0, x, L.K, mc, part + slice * RB * 16, rgrp * R);
+      if (nt0 < L.N) slice_dots<W, R, KCW, MR, NORM, GD>(wv, gv, kc0, x, L.K, mc, part + slice * RB * 16, rgrp * R);
       lds_barrier();
       if (nt0 < L.N) {
         const int items = (pair ? RB / 2 : RB) * mc;
@@ -434,7 +524,7 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
           const int rr = (e / mc) * (pair ? 2 : 1);
           const int n = nt0 + rr;
           if (n >= L.N) continue;
-          const float sc = L.gain != nullptr ? inv[m] : 1.0f;
+          const float sc = NORM ? row_scale(ssw, m, L.K, L.eps) : 1.0f;
           float a0 = 0.f, a1 = 0.f;
 #pragma unroll
           for (int s = 0; s < NS; ++s) {
@@ -444,13 +534,17 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
           a0 *= sc;
           a1 *= sc;
           const int row = m0 + m;
-          const bool pf = t == 0 && m0 == 0 && e == (int)threadIdx.x;  // operands prefetched above
+          const bool pf = t == 0 && m0 == 0 && e == (int)threadIdx.x;  // operands requested above
           if (pair) {
             if (L.epi == EPI_QKV) {
-              epi_pair(L, c, row, n, a0, a1, tag, pf ? e0_pos : gld(c.tok.pos + row),
-                       pf ? e0_b : gld(c.tok.b + row), pf ? e0_slot : gld(c.tok.slot + row));
+              if (pf && qi != nullptr) {
+                epi_pair(L, c, row, n, a0, a1, tag, qi->pos, qi->b, qi->slot, &qi->cs);
+              } else {
+                epi_pair(L, c, row, n, a0, a1, tag, gld(c.tok.pos + row), gld(c.tok.b + row), gld(c.tok.slot + row),
+                         nullptr);
+              }
             } else {
-              epi_pair(L, c, row, n, a0, a1, tag, 0, 0, 0);
+              epi_pair(L, c, row, n, a0, a1, tag, 0, 0, 0, nullptr);
             }
           } else {
             float out = a0;
@@ -467,10 +561,20 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
           }
         }
       }
-      lds_barrier();  // the partials are rewritten by the next chunk or round
+      if (last) next();  // after the stores: requests queued ahead of them would delay them
+      lds_barrier();     // the partials are rewritten by the next chunk or round
     };
-    chunk(0, min(mcap, M), t == 0 || nch > 1);  // the common case: all rows in one chunk
-    for (int ch = 1; ch < nch; ++ch) chunk(ch * mcap, min(mcap, M - ch * mcap), true);
+    if (fast) {
+      chunk(0, M, true, true);
+    } else {
+      for (int ch = 0; ch < nch; ++ch) chunk(ch * mcap, min(mcap, M - ch * mcap), t == 0 || nch > 1, false);
+    }
+  };
+  if (rounds == 1 && nch == 1) {
+    round(0, true);
+  } else {
+    for (int t = 0; t < rounds; ++t) round(t, false);
+    next();
   }
 }
 
@@ -521,9 +625,10 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
 #pragma unroll
       for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, max(hi - 1, 0)) * DH);
     }
+    ll_settle<VEC>(qraw, [&](int v) { return qp + v; }, (1u << VEC) - 1u, base + a.q.tag, err);
     float q[VEC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) q[v] = ll_take(qraw[v], qp + v, base + a.q.tag, err) * a.scale;
+    for (int v = 0; v < VEC; ++v) q[v] = __uint_as_float((uint32_t)qraw[v]) * a.scale;
     if (!hooked) {  // the query has arrived: the next operation's requests go out now
       late();
       hooked = true;
@@ -600,16 +705,12 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
             const uint64_t* kp = a.kvn + (size_t)(f + j - ns) * a.kvn_ld + h * DH + cq * VEC;
             float kf[2 * VEC];
             uint64_t e[2 * VEC];
+            auto ep = [&](int v) { return kp + (v < VEC ? v : a.d + v - VEC); };
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) {
-              e[v] = ll_load(kp + v);
-              e[VEC + v] = ll_load(kp + a.d + v);
-            }
+            for (int v = 0; v < 2 * VEC; ++v) e[v] = ll_load(ep(v));
+            ll_settle<2 * VEC>(e, ep, (1u << (2 * VEC)) - 1u, ktag, err);
 #pragma unroll
-            for (int v = 0; v < VEC; ++v) {
-              kf[v] = ll_take(e[v], kp + v, ktag, err);
-              kf[VEC + v] = ll_take(e[VEC + v], kp + a.d + v, ktag, err);
-            }
+            for (int v = 0; v < 2 * VEC; ++v) kf[v] = __uint_as_float((uint32_t)e[v]);
 #pragma unroll
             for (int v = 0; v < VEC; ++v) {
               dot += q[v] * kf[v];
@@ -700,11 +801,16 @@ __device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32
     const int i = it / g.H, h = it - i * g.H;
     const uint64_t* pb = g.part + ((size_t)i * g.H + h) * S * (DH + 2);
     float ms = -INFINITY, ds = 0.f;
-    if (lane < S) {
-      const uint64_t* pm = pb + (size_t)lane * (DH + 2) + DH;
-      const uint64_t v0 = ll_load(pm), v1 = ll_load(pm + 1);
-      ms = ll_take(v0, pm, ptag, err);
-      ds = ll_take(v1, pm + 1, ptag, err);
+    {
+      const uint64_t* pm = pb + (size_t)min(lane, S - 1) * (DH + 2) + DH;
+      uint64_t v[2];
+      v[0] = lane < S ? ll_load(pm) : 0ull;
+      v[1] = lane < S ? ll_load(pm + 1) : 0ull;
+      ll_settle<2>(v, [&](int j) { return pm + j; }, lane < S ? 3u : 0u, ptag, err);
+      if (lane < S) {
+        ms = __uint_as_float((uint32_t)v[0]);
+        ds = __uint_as_float((uint32_t)v[1]);
+      }
     }
     const float mg = wave_max(ms);
     const float w = (lane < S && ms != -INFINITY) ? expf(ms - mg) : 0.f;
@@ -712,19 +818,20 @@ __device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32
     float num = 0.f;
     for (int s0 = 0; s0 < S; s0 += 8) {
       uint64_t v[8];
+      uint32_t live = 0;
+      auto pe = [&](int j) { return pb + (size_t)min(s0 + j, S - 1) * (DH + 2) + min(lane, DH - 1); };
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const int s = s0 + j;
-        v[j] = (s < S && lane < DH) ? ll_load(pb + (size_t)s * (DH + 2) + lane) : 0ull;
+        const bool in = s0 + j < S && lane < DH;
+        v[j] = in ? ll_load(pe(j)) : 0ull;
+        live |= in ? 1u << j : 0u;
       }
+      ll_settle<8>(v, pe, live, ptag, err);
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int s = s0 + j;
-        const float ws = __shfl(w, s);
-        if (s < S && lane < DH && ws != 0.f) {
-          const uint64_t* pe = pb + (size_t)s * (DH + 2) + lane;
-          num += ws * ll_take(v[j], pe, ptag, err);
-        }
+        const float ws = __shfl(w, min(s, 63));
+        if (s < S && lane < DH && ws != 0.f) num += ws * __uint_as_float((uint32_t)v[j]);
       }
     }
     if (lane < DH) ll_store(g.out + (size_t)i * (g.H * DH) + h * DH + lane, den > 0.f ? num / den : 0.f, tag);
@@ -754,30 +861,69 @@ constexpr int mr_of() {
   return MULTI ? mr : 1;
 }
 
+// Epilogue operands of the thread's first QKV item (see QkvItem); the weight slice
+// of the first layer's QKV projection is requested between the two loads.
+template <class SH, class PQ>
+__device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ& pq) {
+  constexpr int RB = (EW / SH::NSQ) * SH::RQ;
+  const Item0 it = item0<RB>(c.M, SH::D, 3 * SH::D, true);
+  QkvItem q{0, 0, 0, make_float2(1.f, 0.f)};
+  if (it.live) {
+    q.pos = gld(c.tok.pos + it.m);
+    q.b = gld(c.tok.b + it.m);
+    q.slot = gld(c.tok.slot + it.m);
+  }
+  weights_ahead(L, pq);
+  const int n = blockIdx.x * RB + it.rr;
+  if (it.live && n < 2 * SH::D) {
+    const int ee = (n % SH::D) % SH::DH;
+    const v2f cs = *(const GLOBAL v2f*)(L.rope + (size_t)q.pos * (SH::DH / 2) + (ee >> 1));
+    q.cs = make_float2(cs.x, cs.y);
+  }
+  return q;
+}
+
 // Every layer of a stack: QKV (RMSNorm, RoPE, KV append) -> split attention ->
 // merge -> output projection + residual -> gate/up (RMSNorm, SwiGLU) -> down
-// projection + residual.  ops holds six operations per layer.
+// projection + residual.  ops holds six operations per layer.  Each linear layer's
+// first weight slice is requested ahead: the output projection's once the query has
+// arrived in the attention, gate/up's and down's right after the previous linear
+// layer's dot products, and QKV's as the layer starts (a request from the previous
+// layer would keep those registers live across the whole loop).
 template <class SH, bool MULTI>
 __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops, int nlayers, ECall c, uint32_t base,
                                                     int* err) {
   using W = typename SH::W;
   using KV = typename SH::KV;
+  static_assert(SH::D % 256 == 0 && SH::F % 256 == 0, "a staged load must not straddle two rows");
   __shared__ float lds[kLdsFloats];
+  WPre<W, SH::KCD, SH::NSQ, SH::RQ, true> pq;
+  WPre<W, SH::KCD, SH::NSO, SH::RO, false> po;
+  WPre<W, SH::KCD, SH::NSG, SH::RG, true> pg;
+  WPre<W, SH::KCF, SH::NSD, SH::RD, false> pd;
+  const CONST_AS EOp* const cops = (const CONST_AS EOp*)ops;
+  auto lin = [&](int i) -> const ELinear& { return *(const ELinear*)&cops[i].lin; };
+  auto att = [&](int i) -> const EAttn& { return *(const EAttn*)&cops[i].at; };
+  auto mrg = [&](int i) -> const EMerge& { return *(const EMerge*)&cops[i].mg; };
+  const QkvItem qi = qkv_item<SH>(lin(0), c, pq);
 #pragma unroll 1
   for (int l = 0; l < nlayers; ++l) {
-    const EOp* o = ops + 6 * l;
-    op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>()>(o[0].lin, c, base, base + o[0].tag, err, lds);
+    const int o = 6 * l;
+    if (l > 0) weights_ahead(lin(o), pq);
+    op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>(), true>(
+        lin(o), c, base, base + cops[o].tag, err, lds, pq, &qi);
     lds_barrier();
-    WPre<W, SH::KCD, SH::NSO, SH::RO> po;
-    op_attn<KV, SH::DH>(o[1].at, c, base, base + o[1].tag, err, lds,
-                        [&] { weights_ahead<W, SH::KCD, SH::NSO, SH::RO>(o[3].lin, po); });
+    op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, [&] { weights_ahead(lin(o + 3), po); });
     lds_barrier();
-    op_merge<SH::DH>(o[2].mg, c, base, base + o[2].tag, err);
-    op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>()>(o[3].lin, c, base, base + o[3].tag, err, lds, &po);
+    op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err);
+    op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>(), false>(
+        lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr, [&] { weights_ahead(lin(o + 4), pg); });
     lds_barrier();
-    op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>()>(o[4].lin, c, base, base + o[4].tag, err, lds);
+    op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>(), true>(
+        lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr, [&] { weights_ahead(lin(o + 5), pd); });
     lds_barrier();
-    op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>()>(o[5].lin, c, base, base + o[5].tag, err, lds);
+    op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>(), false>(
+        lin(o + 5), c, base, base + cops[o + 5].tag, err, lds, pd, nullptr);
     lds_barrier();
   }
 }
