@@ -19,7 +19,7 @@ constexpr int kEngineChunk = 512;
 
 // An operand of [M, ld] elements: tagged entries (ll != nullptr; valid once the tag
 // equals launch base + tag), plain float32 rows written before the launch (f), or,
-// with both null, the launch's own input rows (ECall::x).
+// with both null, the launch's own input rows (ECall::io).
 struct EIn {
   const float* f;
   const uint64_t* ll;
@@ -38,7 +38,7 @@ struct ELinear {
   int32_t epi;  // EPI_STORE, EPI_RESID, EPI_SWIGLU or EPI_QKV (kernels.h)
   EIn resid;    // EPI_RESID: output = resid + W x
   uint64_t* y;  // tagged output rows (ld ldy); for EPI_QKV the queries [M, d];
-                // nullptr: plain rows written to ECall::x (last operation)
+                // nullptr: the launch's output rows (ECall::io, last operation)
   int32_t ldy;
   // EPI_QKV: rotated keys and values of the pass rows, tagged [M, 2d] (k | v), plus
   // the KV cache append
@@ -51,9 +51,28 @@ struct ELinear {
   int32_t kvt;
 };
 
+// Input rows of a stack pass (read by the first layer) and where its output rows
+// go (written by the last layer); every row is d floats.  Input row m is the
+// embedding row emb[ie[m]] (a bfloat16 table when emb_bf16, else float32) when emb
+// is set, else xa[ia ? ia[m] : m]; plus xb[ib[m]] when xb is set.  Output row m goes
+// to xo[oi ? oi[m] : m] and, when oi2 is set and oi2[m] >= 0, also to xo2[oi2[m]].
+struct EIo {
+  const void* emb;
+  int32_t emb_bf16;
+  const int32_t* ie;
+  const float* xa;
+  const int32_t* ia;
+  const float* xb;
+  const int32_t* ib;
+  float* xo;
+  const int32_t* oi;
+  float* xo2;
+  const int32_t* oi2;
+};
+
 // Per-launch values shared by the operations of one stack pass.
 struct ECall {
-  float* x;  // [M, d] plain residual rows: input of the first layer, output of the last
+  EIo io;
   int32_t M;
   Tok tok;
   const int32_t* first;       // [M] index of the first pass row of the same batch row

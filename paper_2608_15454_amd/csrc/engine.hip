@@ -43,6 +43,7 @@ constexpr uint64_t kWaitTicks = 20000000ull;  // 200 ms of the 100 MHz real-time
 typedef uint32_t v4u __attribute__((ext_vector_type(4)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v2f __attribute__((ext_vector_type(2)));
+typedef uint32_t v2u __attribute__((ext_vector_type(2)));
 
 template <typename T>
 __device__ __forceinline__ T gld(const T* p) {
@@ -111,13 +112,58 @@ __device__ __forceinline__ float ll_take(uint64_t v, const uint64_t* p, uint32_t
   return (uint32_t)(v >> 32) == tag ? __uint_as_float((uint32_t)v) : ll_wait(p, tag, err);
 }
 
+// Element (m, k) and four elements (m, k..k+3) of a launch's input rows (EIo).
+__device__ __forceinline__ float in1(const EIo& io, int m, int d, int k) {
+  float v;
+  if (io.emb != nullptr) {
+    const size_t r = (size_t)gld(io.ie + m) * d + k;
+    v = io.emb_bf16 ? bf2f(gld(reinterpret_cast<const uint16_t*>(io.emb) + r))
+                    : gld(reinterpret_cast<const float*>(io.emb) + r);
+  } else {
+    v = gld(io.xa + (size_t)(io.ia != nullptr ? gld(io.ia + m) : m) * d + k);
+  }
+  if (io.xb != nullptr) v += gld(io.xb + (size_t)gld(io.ib + m) * d + k);
+  return v;
+}
+
+__device__ __forceinline__ float4 in4(const EIo& io, int m, int d, int k) {
+  float4 v;
+  if (io.emb != nullptr) {
+    const size_t r = (size_t)gld(io.ie + m) * d + k;
+    if (io.emb_bf16) {
+      const v2u u = *(const GLOBAL v2u*)(reinterpret_cast<const uint16_t*>(io.emb) + r);
+      v = make_float4(bf2f(u.x & 0xffffu), bf2f(u.x >> 16), bf2f(u.y & 0xffffu), bf2f(u.y >> 16));
+    } else {
+      v = ld16f(reinterpret_cast<const float*>(io.emb) + r);
+    }
+  } else {
+    v = ld16f(io.xa + (size_t)(io.ia != nullptr ? gld(io.ia + m) : m) * d + k);
+  }
+  if (io.xb != nullptr) {
+    const float4 w = ld16f(io.xb + (size_t)gld(io.ib + m) * d + k);
+    v.x += w.x;
+    v.y += w.y;
+    v.z += w.z;
+    v.w += w.w;
+  }
+  return v;
+}
+
+// Output element (m, n) of a launch (EIo).
+__device__ __forceinline__ void out1(const EIo& io, int m, int d, int n, float v) {
+  gst(io.xo + (size_t)(io.oi != nullptr ? gld(io.oi + m) : m) * d + n, v);
+  if (io.oi2 != nullptr) {
+    const int r = gld(io.oi2 + m);
+    if (r >= 0) gst(io.xo2 + (size_t)r * d + n, v);
+  }
+}
+
 __device__ __forceinline__ float ein_get(const EIn& x, const ECall& c, int m, int k, uint32_t base, int* err) {
   if (x.ll != nullptr) {
     const uint64_t* p = x.ll + (size_t)m * x.ld + k;
     return ll_take(ll_load(p), p, base + x.tag, err);
   }
-  const float* f = x.f != nullptr ? x.f : c.x;
-  return gld(f + (size_t)m * x.ld + k);
+  return x.f != nullptr ? gld(x.f + (size_t)m * x.ld + k) : in1(c.io, m, x.ld, k);
 }
 
 // Waits until every entry v[j] with bit j of live set carries tag; addr(j) is the
@@ -177,11 +223,11 @@ __device__ __forceinline__ void stage_rows(const EIn& x, const ECall& c, int m0,
     acc += sq;
   };
   if (x.ll == nullptr) {
-    const float* f = x.f != nullptr ? x.f : c.x;
     for (int eb = wave * 256; eb < n; eb += EB * 4) {
       const int m = eb / K;
       const int e = eb + lane * 4;
-      const float4 t = ld16f(f + (size_t)(m0 + m) * x.ld + (e - m * K));
+      const float4 t = x.f != nullptr ? ld16f(x.f + (size_t)(m0 + m) * x.ld + (e - m * K))
+                                      : in4(c.io, m0 + m, x.ld, e - m * K);
       *reinterpret_cast<float4*>(lds + e) = t;
       if (ssw != nullptr) add(m, t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w);
     }
@@ -265,7 +311,7 @@ __device__ __forceinline__ void load_w(const ELinear& L, int n0, int kc0, uint4 
 
 __device__ __forceinline__ void out_store(const ELinear& L, const ECall& c, int m, int n, float v, uint32_t tag) {
   if (L.y != nullptr) ll_store(L.y + (size_t)m * L.ldy + n, v, tag);
-  else gst(c.x + (size_t)m * L.ldy + n, v);
+  else out1(c.io, m, L.ldy, n, v);
 }
 
 // Cache elements off, off+1 (off even, so the pair is one aligned word).
@@ -474,8 +520,8 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
     if (L.resid.ll != nullptr) {
       e0_res = ll_load(L.resid.ll + (size_t)i0.m * L.resid.ld + n);
     } else {
-      const float* f = L.resid.f != nullptr ? L.resid.f : c.x;
-      e0_res = __float_as_uint(gld(f + (size_t)i0.m * L.resid.ld + n));
+      e0_res = __float_as_uint(L.resid.f != nullptr ? gld(L.resid.f + (size_t)i0.m * L.resid.ld + n)
+                                                     : in1(c.io, i0.m, L.resid.ld, n));
     }
   }
   // one round: a tile of RB output rows over all input chunks.  fast: the common

@@ -109,7 +109,8 @@ hipError_t launch_attn_prefill(const Attn& a, int kvt, const int32_t* tiles, int
 
 hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X, int d, int M, hipStream_t st,
                         const Ev& ev = Ev());
-// dst[dst_idx[i]] = src[src_idx[i]] (+ src2[src2_idx[i]]); null index arrays mean i.
+// dst[dst_idx[i]] = src[src_idx[i]] (+ src2[src2_idx[i]]); null index arrays mean i;
+// rows with dst_idx[i] < 0 are skipped.
 hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const float* src2,
                             const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d, int M,
                             hipStream_t st, const Ev& ev = Ev());

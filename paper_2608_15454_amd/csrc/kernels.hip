@@ -633,6 +633,7 @@ __global__ void embed_kernel(const W* emb, const int32_t* bytes, float* X, int d
 __global__ void copy_rows_kernel(const float* src, const int32_t* src_idx, const float* src2,
                                  const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d) {
   const int i = blockIdx.x;
+  if (dst_idx != nullptr && dst_idx[i] < 0) return;  // row not copied
   const size_t si = (size_t)(src_idx ? src_idx[i] : i) * d;
   const size_t di = (size_t)(dst_idx ? dst_idx[i] : i) * d;
   const size_t s2 = src2 ? (size_t)(src2_idx ? src2_idx[i] : i) * d : 0;

@@ -543,10 +543,10 @@ double stack_bytes(const mbp_handle* h, int nlayers, int M, double kv_rows) {
 }
 
 // One pass through a stack in the persistent engine (see engine.hip).
-int run_engine(mbp_handle* h, const EngStack& es, int nlayers, float* X, const Tok& tok, const int32_t* first,
+int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, const Tok& tok, const int32_t* first,
                const int32_t* first_slot, int S, const int32_t* grp_tab, double kv_rows, hipStream_t st) {
   ECall c;
-  c.x = X;
+  c.io = io;
   c.M = tok.M;
   c.tok = tok;
   c.first = first;
@@ -565,20 +565,14 @@ int run_engine(mbp_handle* h, const EngStack& es, int nlayers, float* X, const T
 }
 
 // One transformer stack over the token rows in X (residual stream, [M, d]) on stream
-// st with scratch sc.  kv_rows: total visible cache rows over the pass's queries.
-// Short passes go to the engine when the stack has an operation list (es).
+// st with scratch sc, one kernel per operation.  kv_rows: total visible cache rows
+// over the pass's queries.
 int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
               const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows,
-              const Scratch& sc, hipStream_t st, const EngStack* es = nullptr, const int32_t* first = nullptr,
-              const int32_t* first_slot = nullptr, int32_t max_ns = 0) {
+              const Scratch& sc, hipStream_t st) {
   const Sizes& s = h->sz;
   const int M = tok.M;
   if (M == 0) return MBP_OK;
-  if (h->engine && es != nullptr && es->nops > 0 && !tiled && M <= kEngineMaxRows) {
-    const int S = (max_ns + kEngineChunk - 1) / kEngineChunk + 1;
-    if (S <= s.Esplit)
-      return run_engine(h, *es, (int)layers.size(), X, tok, first, first_slot, S, grp_tab, kv_rows, st);
-  }
   const float scale = h->cfg.attn_scale / std::sqrt((float)s.dh);
   for (size_t l = 0; l < layers.size(); ++l) {
     const BlockW& w = layers[l];
@@ -623,6 +617,34 @@ int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, fl
     dn.epi.kind = EPI_RESID; dn.epi.Y = X; dn.epi.ldy = s.d;
     RCK(run_linear(h, dn, sc, st));
   }
+  return MBP_OK;
+}
+
+// One pass of a stack over the token rows of tok, with input rows and output
+// destinations as in io (engine.h).  Short passes go to the engine when the stack has
+// an operation list (es), which reads and writes those rows directly; otherwise the
+// input rows are gathered into X, the stack runs one kernel per operation, and X is
+// scattered to the destinations.
+int run_pass(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, const EngStack* es, const EIo& io,
+             float* X, const Tok& tok, const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles,
+             int max_kv, double kv_rows, const Scratch& sc, hipStream_t st, const int32_t* first,
+             const int32_t* first_slot, int32_t max_ns) {
+  const Sizes& s = h->sz;
+  const int M = tok.M;
+  if (M == 0) return MBP_OK;
+  if (h->engine && es != nullptr && es->nops > 0 && !tiled && M <= kEngineMaxRows) {
+    const int S = (max_ns + kEngineChunk - 1) / kEngineChunk + 1;
+    if (S <= s.Esplit)
+      return run_engine(h, *es, (int)layers.size(), io, tok, first, first_slot, S, grp_tab, kv_rows, st);
+  }
+  if (io.emb != nullptr) {
+    OTHER(h, launch_embed, io.emb, h->wdt, io.ie, X, s.d, M, st);
+  } else if (io.xa != X || io.ia != nullptr || io.xb != nullptr) {
+    OTHER(h, launch_copy_rows, io.xa, io.ia, io.xb, io.ib, X, nullptr, s.d, M, st);
+  }
+  RCK(run_stack(h, layers, kv, X, tok, grp_tab, tiled, tiles, ntiles, max_kv, kv_rows, sc, st));
+  if (io.xo != X || io.oi != nullptr) OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, io.xo, io.oi, s.d, M, st);
+  if (io.oi2 != nullptr) OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, io.xo2, io.oi2, s.d, M, st);
   return MBP_OK;
 }
 
@@ -714,12 +736,17 @@ int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
   RCK(upload(h, p, st));
   const Tok tok = dev_tok(p, om, tm.size());
   const Scratch& sc = h->sc_mb;
-  OTHER(h, launch_copy_rows, h->R<float>(rg.lat_out), p.at(o_z), h->R<float>(rg.lat_in), p.at(o_z), sc.X, nullptr,
-        s.d, tm.size(), st);
-  RCK(run_stack(h, h->mb, h->kv_mb, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st, &h->es_mb,
-                p.at(om.first), p.at(om.first_slot), om.max_ns));
-  OTHER(h, launch_copy_rows, sc.X, nullptr, nullptr, nullptr, h->rows_base(), p.at(o_w), s.d, tm.size(), st);
-  return MBP_OK;
+  // window rows z_g = latent output + latent input of the row's group; outputs to the
+  // MB rows of the window
+  EIo io{};
+  io.xa = h->R<float>(rg.lat_out);
+  io.ia = p.at(o_z);
+  io.xb = h->R<float>(rg.lat_in);
+  io.ib = p.at(o_z);
+  io.xo = h->rows_base();
+  io.oi = p.at(o_w);
+  return run_pass(h, h->mb, h->kv_mb, &h->es_mb, io, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st,
+                  p.at(om.first), p.at(om.first_slot), om.max_ns);
 }
 
 // Make the caller's stream wait for a forked MB update.
@@ -768,7 +795,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     if (!first_chunk) HIPCK(h, hipStreamSynchronize(h->st));  // plan buffer reuse
     first_chunk = false;
     Toks te, tl;
-    std::vector<int32_t> bytes, he_row, nt_src, lo_row, cnt, lat_row, last_src, last_dst;
+    std::vector<int32_t> bytes, he_row, nt_src, lo_row, cnt, lat_row, h1_dst;
     int max_kv_e = 0, max_kv_l = 0;
     double kvr_e = 0, kvr_l = 0;
     std::vector<int> rows_in_chunk;
@@ -811,10 +838,8 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
       nt_src.push_back(b * s.Kcap + L);
       max_kv_e = std::max(max_kv_e, pos + 1);
       kvr_e += pos + 1;
-      if (it + 1 == last || items[it + 1].b != b) {
-        last_src.push_back(te.size() - 1);
-        last_dst.push_back(h->rg.row_h1 + b);
-      }
+      // the NT output of the last new byte of a row is its h1 row
+      h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
     }
     const int Me = te.size(), Ml = tl.size();
     const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
@@ -824,29 +849,46 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     p.clear();
     const TokOffs oe = add_toks(p, te), ol = add_toks(p, tl);
     const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_nts = p.add(nt_src), o_lo = p.add(lo_row),
-                 o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_ls = p.add(last_src), o_ld = p.add(last_dst),
-                 o_te = p.add(tiles_e), o_tl = p.add(tiles_l);
+                 o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_h1 = p.add(h1_dst), o_te = p.add(tiles_e),
+                 o_tl = p.add(tiles_l);
     RCK(upload(h, p, h->st));
     const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
 
-    OTHER(h, launch_embed, h->emb, h->wdt, p.at(o_bytes), X, s.d, Me, h->st);
-    RCK(run_stack(h, h->enc, h->kv_enc, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                  kvr_e, sc, h->st, &h->es_enc, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
-    OTHER(h, launch_copy_rows, X, nullptr, nullptr, nullptr, he, p.at(o_he), s.d, Me, h->st);
+    // encoder: embeddings of the new bytes -> h_e rows
+    EIo ioe{};
+    ioe.emb = h->emb;
+    ioe.emb_bf16 = h->wdt;
+    ioe.ie = p.at(o_bytes);
+    ioe.xo = he;
+    ioe.oi = p.at(o_he);
+    RCK(run_pass(h, h->enc, h->kv_enc, &h->es_enc, ioe, X, tok_e, nullptr, tiled_e, p.at(o_te),
+                 (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
     if (Ml > 0) {
+      // LM module on the closed segments: pooled latent inputs -> latent outputs
       OTHER(h, launch_pool, he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st);
-      OTHER(h, launch_copy_rows, lat_in, p.at(o_lat), nullptr, nullptr, Xl, nullptr, s.d, Ml, h->st);
-      RCK(run_stack(h, h->lm, h->kv_lm, Xl, tok_l, nullptr, tiled_l, p.at(o_tl), (int)tiles_l.size() / 2, max_kv_l,
-                    kvr_l, sc, h->st, &h->es_lm, p.at(ol.first), p.at(ol.first_slot), ol.max_ns));
-      OTHER(h, launch_copy_rows, Xl, nullptr, nullptr, nullptr, lat_out, p.at(o_lat), s.d, Ml, h->st);
+      EIo iol{};
+      iol.xa = lat_in;
+      iol.ia = p.at(o_lat);
+      iol.xo = lat_out;
+      iol.oi = p.at(o_lat);
+      RCK(run_pass(h, h->lm, h->kv_lm, &h->es_lm, iol, Xl, tok_l, nullptr, tiled_l, p.at(o_tl),
+                   (int)tiles_l.size() / 2, max_kv_l, kvr_l, sc, h->st, p.at(ol.first), p.at(ol.first_slot),
+                   ol.max_ns));
     }
     const bool fork_here = fork && last == items.size();
     if (fork_here) HIPCK(h, hipEventRecord(h->ev_fork, h->st));  // the latents are final here
-    OTHER(h, launch_copy_rows, lat_out, p.at(o_nts), he, p.at(o_he), X, nullptr, s.d, Me, h->st);
-    RCK(run_stack(h, h->nt, h->kv_nt, X, tok_e, nullptr, tiled_e, p.at(o_te), (int)tiles_e.size() / 2, max_kv_e,
-                  kvr_e, sc, h->st, &h->es_nt, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
-    OTHER(h, launch_copy_rows, X, p.at(o_ls), nullptr, nullptr, h->rows_base(), p.at(o_ld), s.d,
-          (int)last_src.size(), h->st);
+    // NT decoder: latent of the byte's group + h_e -> X (token order), and each row's
+    // last output -> h1
+    EIo ion{};
+    ion.xa = lat_out;
+    ion.ia = p.at(o_nts);
+    ion.xb = he;
+    ion.ib = p.at(o_he);
+    ion.xo = X;
+    ion.xo2 = h->rows_base();
+    ion.oi2 = p.at(o_h1);
+    RCK(run_pass(h, h->nt, h->kv_nt, &h->es_nt, ion, X, tok_e, nullptr, tiled_e, p.at(o_te),
+                 (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
     if (fork_here) {
       // the next step's window update, enqueued after the NT decoder (the critical
       // path) but ordered only after the LM module; its plan reuses a host buffer
