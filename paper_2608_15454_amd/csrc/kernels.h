@@ -123,9 +123,11 @@ hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const floa
 // Per batch row b < B: greedy byte and probability of each of the n logit rows,
 // then accept_len (threshold mode; write_len = 0 leaves accept_len untouched).
 // accept_len is -1 for every row when *fault != 0 (a failed engine wait).
+// host_cand / host_len (device-mapped pinned host memory, or null) receive copies
+// of the candidates and accept_len.
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active,
                          uint8_t* cand, float* prob, int32_t* accept_len, int write_len, const int32_t* fault,
-                         hipStream_t st, const Ev& ev = Ev());
+                         uint8_t* host_cand, int32_t* host_len, hipStream_t st, const Ev& ev = Ev());
 // Greedy verification: NT logits of the n tentative rows vs the drafts.
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
                          int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev = Ev());

@@ -703,7 +703,8 @@ __device__ __forceinline__ float row_top1(const float* row, int lane, int* idx_o
 }
 
 __global__ void accept_kernel(const float* logits, int n, float tau, const int32_t* active, uint8_t* cand,
-                              float* prob, int32_t* accept_len, int write_len, const int32_t* fault) {
+                              float* prob, int32_t* accept_len, int write_len, const int32_t* fault,
+                              uint8_t* host_cand, int32_t* host_len) {
   __shared__ float ps[8];
   const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   if (wave < n) {
@@ -711,6 +712,7 @@ __global__ void accept_kernel(const float* logits, int n, float tau, const int32
     const float p = row_top1(logits + ((size_t)b * n + wave) * 256, lane, &bi);
     if (lane == 0) {
       cand[b * n + wave] = (uint8_t)bi;
+      if (host_cand) host_cand[b * n + wave] = (uint8_t)bi;
       if (prob) prob[b * n + wave] = p;
       ps[wave] = p;
     }
@@ -719,7 +721,9 @@ __global__ void accept_kernel(const float* logits, int n, float tau, const int32
   if (tid == 0 && write_len) {
     int k = 1;
     while (k < n && ps[k] >= tau) ++k;
-    accept_len[b] = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
+    const int32_t len = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
+    accept_len[b] = len;
+    if (host_len) host_len[b] = len;
   }
 }
 
@@ -935,11 +939,11 @@ hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const floa
 }
 
 hipError_t launch_accept(const float* logits, int B, int n, float tau, const int32_t* active, uint8_t* cand,
-                         float* prob, int32_t* accept_len, int write_len, const int32_t* fault, hipStream_t st,
-                         const Ev& ev) {
+                         float* prob, int32_t* accept_len, int write_len, const int32_t* fault, uint8_t* host_cand,
+                         int32_t* host_len, hipStream_t st, const Ev& ev) {
   if (B <= 0) return hipSuccess;
   return klaunch(accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau, active, cand, prob,
-                 accept_len, write_len, fault);
+                 accept_len, write_len, fault, host_cand, host_len);
 }
 
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,

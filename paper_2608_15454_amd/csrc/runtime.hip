@@ -82,7 +82,7 @@ struct Scratch {
   int64_t part_floats;
 };
 
-constexpr int kPlans = 4;  // 0 commit, 1 head, 2 forked MB update, 3 MB update in the step
+constexpr int kPlans = 3;  // 0 commit, 1 window update and head of a step, 2 forked MB update
 
 struct Regions {
   size_t gains, rope, enc_k, enc_v, lm_k, lm_v, nt_k, nt_v, mb_k, mb_v, he, lat_in, lat_out, rows, logits, vlogits,
@@ -351,6 +351,8 @@ struct mbp_handle {
   int last_n = 0, last_mode = 0;
   uint8_t* h_cand = nullptr;  // pinned [B, n] candidates of the last step
   int32_t* h_len = nullptr;   // pinned [B] accepted counts of the last step
+  uint8_t* h_cand_dev = nullptr;  // device addresses of the two (written by the accept kernel)
+  int32_t* h_len_dev = nullptr;
   std::vector<int32_t> pre_len;
   Plan plan[kPlans];
 
@@ -687,17 +689,26 @@ int32_t window_start(const Row& r) {
 }
 
 // LCA window of the current state for n candidates: window rows s..t+n-2 (previous
-// group, current group, n-2 virtual rows).  Computes, on stream st, the rows not yet
-// cached (rows are prefix-stable while the latent list is unchanged) and writes
-// their outputs to the MB rows of `rows`.  With clamp, n is reduced to fit the
-// window capacity instead of failing.
-int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
+// group, current group, n-2 virtual rows).  Computes the rows not yet cached (rows
+// are prefix-stable while the latent list is unchanged) and writes their outputs to
+// the MB rows of `rows`.  With clamp, n is reduced to fit the window capacity
+// instead of failing.  The update has a host part (mb_prepare: appends the pass's
+// arrays to p and advances the window state) and the launches (mb_launch, after p is
+// uploaded), so that one plan upload can serve several passes.
+struct MbPass {
+  Toks tm;
+  TokOffs om;
+  size_t o_z = 0, o_w = 0, o_g = 0;
+  int max_w = 0;
+  double kvr = 0;
+};
+
+int mb_prepare(mbp_handle* h, int n, Plan& p, bool clamp, MbPass* out) {
   const Sizes& s = h->sz;
   const Regions& rg = h->rg;
   const int B = h->batch;
   if (n < 2) return MBP_OK;
-  p.clear();
-  Toks tm;
+  Toks& tm = out->tm;
   std::vector<int32_t> zrow, wrow, grp_tab((size_t)B * s.Wcap, 0);
   int max_w = 0;
   double kvr_m = 0;
@@ -731,22 +742,40 @@ int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
     r.win_valid = std::max(r.win_valid, W);
   }
   if (tm.size() == 0) return MBP_OK;
-  const TokOffs om = add_toks(p, tm);
-  const size_t o_z = p.add(zrow), o_w = p.add(wrow), o_g = p.add(grp_tab);
-  RCK(upload(h, p, st));
-  const Tok tok = dev_tok(p, om, tm.size());
+  out->om = add_toks(p, tm);
+  out->o_z = p.add(zrow);
+  out->o_w = p.add(wrow);
+  out->o_g = p.add(grp_tab);
+  out->max_w = max_w;
+  out->kvr = kvr_m;
+  return MBP_OK;
+}
+
+int mb_launch(mbp_handle* h, const Plan& p, const MbPass& mp, hipStream_t st) {
+  const Regions& rg = h->rg;
+  if (mp.tm.size() == 0) return MBP_OK;
+  const Tok tok = dev_tok(p, mp.om, mp.tm.size());
   const Scratch& sc = h->sc_mb;
   // window rows z_g = latent output + latent input of the row's group; outputs to the
   // MB rows of the window
   EIo io{};
   io.xa = h->R<float>(rg.lat_out);
-  io.ia = p.at(o_z);
+  io.ia = p.at(mp.o_z);
   io.xb = h->R<float>(rg.lat_in);
-  io.ib = p.at(o_z);
+  io.ib = p.at(mp.o_z);
   io.xo = h->rows_base();
-  io.oi = p.at(o_w);
-  return run_pass(h, h->mb, h->kv_mb, &h->es_mb, io, sc.X, tok, p.at(o_g), false, nullptr, 0, max_w, kvr_m, sc, st,
-                  p.at(om.first), p.at(om.first_slot), om.max_ns);
+  io.oi = p.at(mp.o_w);
+  return run_pass(h, h->mb, h->kv_mb, &h->es_mb, io, sc.X, tok, p.at(mp.o_g), false, nullptr, 0, mp.max_w, mp.kvr, sc,
+                  st, p.at(mp.om.first), p.at(mp.om.first_slot), mp.om.max_ns);
+}
+
+int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
+  p.clear();
+  MbPass mp;
+  RCK(mb_prepare(h, n, p, clamp, &mp));
+  if (mp.tm.size() == 0) return MBP_OK;
+  RCK(upload(h, p, st));
+  return mb_launch(h, p, mp, st);
 }
 
 // Make the caller's stream wait for a forked MB update.
@@ -923,18 +952,22 @@ int check_ready(mbp_handle* h) {
 
 // Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
 // per-row greedy bytes / probabilities (and accept_len in threshold mode).
-int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len) {
+int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len,
+          bool host_out) {
   const Sizes& s = h->sz;
   const mbp_config& c = h->cfg;
   const Regions& rg = h->rg;
   const int B = h->batch;
   const bool lca = c.head == MBP_HEAD_LCA;
-  if (lca) {
-    RCK(mb_join(h));
-    RCK(mb_update(h, n, h->plan[3], h->st, false));  // rows the forked update did not cover
-  }
+  // one plan upload for the window update (rows a forked update did not cover) and
+  // the head
   Plan& p = h->plan[1];
   p.clear();
+  MbPass mp;
+  if (lca) {
+    RCK(mb_join(h));
+    RCK(mb_prepare(h, n, p, false, &mp));
+  }
   float* h1 = h->row_ptr(rg.row_h1);
   float* mlp_out = h->row_ptr(rg.row_mlp);
   float* logits = h->R<float>(rg.logits);
@@ -958,6 +991,7 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
       for (int b = 0; b < B; ++b) mlp_dst.push_back(rg.row_mlp + b * s.nmax + m);
   const size_t o_hr = p.add(head_rows), o_md = p.add(mlp_dst);
   RCK(upload(h, p, h->st));
+  if (lca) RCK(mb_launch(h, p, mp, h->st));
 
   if (!lca) {
     for (int m = 1; m < n; ++m) {
@@ -986,7 +1020,7 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
   un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
   RCK(run_linear(h, un, sc, h->st));
   OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
-        h->engine ? h->d_err : nullptr, h->st);
+        h->engine ? h->d_err : nullptr, host_out ? h->h_cand_dev : nullptr, host_out ? h->h_len_dev : nullptr, h->st);
   h->n_hint = n;
   return MBP_OK;
 }
@@ -1157,6 +1191,8 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   }
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_cand, (size_t)s.B * s.nmax, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_len, (size_t)s.B * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&h->h_cand_dev, h->h_cand, 0);
+  if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&h->h_len_dev, h->h_len, 0);
   if (e != hipSuccess) return bail();
 
   // norm gains and BOS converted to float32 once
@@ -1304,16 +1340,15 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   std::memset(h->h_cand, 0, (size_t)B * n);
   std::memset(h->h_len, 0, (size_t)B * 4);
   if (mode == MBP_ACCEPT_THRESHOLD) {
-    RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len));
-    HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
-    HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+    // the accept kernel also writes the candidates and lengths to pinned host memory
+    RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len, true));
     h->pending = true;
     h->last_n = n;
     h->last_mode = mode;
     return MBP_OK;
   }
   // self-verify: drafts, tentative commit of all n drafts, greedy check, rollback
-  RCK(draft(h, n, tau, false, d_cand, d_prob, d_accept_len));
+  RCK(draft(h, n, tau, false, d_cand, d_prob, d_accept_len, false));
   HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
   std::vector<std::vector<uint8_t>> add(B);
