@@ -723,7 +723,11 @@ __global__ void accept_kernel(const float* logits, int n, float tau, const int32
     while (k < n && ps[k] >= tau) ++k;
     const int32_t len = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
     accept_len[b] = len;
-    if (host_len) host_len[b] = len;
+    if (host_len) {
+      // the host waits for host_len: the block's candidates must be visible first
+      __threadfence_system();
+      __hip_atomic_store(host_len + b, len, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
   }
 }
 

@@ -16,6 +16,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -82,6 +83,8 @@ struct Scratch {
   int64_t part_floats;
 };
 
+// h_len value while a step's result has not arrived (the accept kernel writes >= -1)
+constexpr int32_t kLenPending = INT32_MIN;
 constexpr int kPlans = 3;  // 0 commit, 1 window update and head of a step, 2 forked MB update
 
 struct Regions {
@@ -944,6 +947,24 @@ int check_fault(mbp_handle* h) {
   return MBP_OK;
 }
 
+// Waits for the accept kernel of a threshold step, which writes every row's length
+// (kLenPending until then) to pinned host memory after its candidates.  Spinning on
+// that memory returns as soon as the values land; the stream keeps running.  If
+// they do not arrive within a second, waits for the stream instead (which reports
+// a failed launch).
+int wait_step_result(mbp_handle* h) {
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t it = 0;; ++it) {
+    bool done = true;
+    for (int b = 0; b < h->batch && done; ++b)
+      done = __atomic_load_n(h->h_len + b, __ATOMIC_ACQUIRE) != kLenPending;
+    if (done) return MBP_OK;
+    if ((it & 1023) == 1023 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(1)) break;
+  }
+  HIPCK(h, hipStreamSynchronize(h->st));
+  return MBP_OK;
+}
+
 int check_ready(mbp_handle* h) {
   if (!h) return MBP_EINVAL;
   if (h->poisoned) return fail(h, MBP_ESTATE, "handle poisoned by an earlier HIP error; call mbp_reset");
@@ -1338,7 +1359,7 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
       if ((int64_t)h->rows[b].x.size() + n > s.Tcap) return fail(h, MBP_ECAPACITY, "verify drafts exceed max_ctx");
   }
   std::memset(h->h_cand, 0, (size_t)B * n);
-  std::memset(h->h_len, 0, (size_t)B * 4);
+  for (int b = 0; b < B; ++b) h->h_len[b] = kLenPending;
   if (mode == MBP_ACCEPT_THRESHOLD) {
     // the accept kernel also writes the candidates and lengths to pinned host memory
     RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len, true));
@@ -1419,7 +1440,11 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
   const Sizes& s = h->sz;
   if (!h_override && !h->pending) return fail(h, MBP_ESTATE, "no pending step to accept");
   if ((h_override == nullptr) != (h_override_len == nullptr)) return fail(h, MBP_EINVAL, "override needs both arrays");
-  HIPCK(h, hipStreamSynchronize(h->st));
+  if (h->pending && h->last_mode == MBP_ACCEPT_THRESHOLD && !h->timing) {
+    RCK(wait_step_result(h));
+  } else {
+    HIPCK(h, hipStreamSynchronize(h->st));
+  }
   if (h->timing) {
     RCK(sync_all(h));
     RCK(t_drain(h));
