@@ -62,25 +62,29 @@ def cpu_threads():
 # readings scale the HBM counters of the kernels that follow.
 COPY_CAL_BYTES = 256 << 20
 # HBM traffic per launch of the dominant kernel class, from counter runs of this
-# command, valid only while the kernel source is the one that was measured.
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_lca_d1024_b1_hbm_counters.md")
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_15454_amd", "csrc", "kernels.hip")
+# command (profiles/<class>_<workload>_hbm_counters.md), valid only while the source
+# the class is built from is the one that was measured.
+CSRC = os.path.join(ROOT, "paper_2608_15454_amd", "csrc")
+CLASS_SOURCE = {"engine": "engine.hip", "gemv": "kernels.hip", "gemm": "kernels.hip", "attention": "kernels.hip",
+                "other": "kernels.hip"}
 
 
 def measured_traffic(kernel_class, workload):
     """Bytes per launch recorded for kernel_class on workload, or None when there is no
-    record or kernels.hip has changed since the counters were taken."""
+    record or the class's source has changed since the counters were taken."""
     import hashlib
 
-    if not os.path.exists(TRAFFIC_FILE):
+    path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_hbm_counters.md")
+    source = CLASS_SOURCE.get(kernel_class)
+    if source is None or not os.path.exists(path):
         return None
     fields = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         if line.startswith("- ") and ": " in line:
             k, v = line[2:].split(": ", 1)
             fields[k.strip()] = v.strip().strip("`")
-    src = hashlib.sha256(open(KERNEL_SOURCE, "rb").read()).hexdigest()
-    if fields.get("kernels.hip sha256") != src or fields.get("class") != kernel_class \
+    digest = hashlib.sha256(open(os.path.join(CSRC, source), "rb").read()).hexdigest()
+    if fields.get(f"{source} sha256") != digest or fields.get("class") != kernel_class \
             or fields.get("workload") != workload:
         return None
     return int(fields["hbm bytes per launch"])

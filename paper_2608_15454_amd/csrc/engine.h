@@ -14,8 +14,8 @@ namespace mbp {
 
 // Rows of one pass the engine accepts; larger passes use the per-kernel path.
 constexpr int kEngineMaxRows = 16;
-// Keys per attention split over cached slots (one block of eight waves).
-constexpr int kEngineChunk = 512;
+// Attention splits per (row, head) the engine's buffers hold.
+constexpr int kEngineMaxSplits = 64;
 
 // An operand of [M, ld] elements: tagged entries (ll != nullptr; valid once the tag
 // equals launch base + tag), plain float32 rows written before the launch (f), or,
@@ -79,10 +79,11 @@ struct ECall {
   const int32_t* first_slot;  // [M] cache slot of that row (the first slot this pass writes)
   const int32_t* grp_tab;  // [B, cap] group ids of cache slots (LCA mask) or nullptr
   int32_t S;               // attention splits per (row, head), the last one for pass rows
+  int32_t chunk;           // cached keys per split (a multiple of 64)
 };
 
 // Split-KV attention of the pass rows.  Split s < S-1 covers cached slots
-// [s*kEngineChunk, (s+1)*kEngineChunk) below the row's first pass slot; split S-1
+// [s*chunk, (s+1)*chunk) below the row's first pass slot; split S-1
 // covers the slots written by this pass, read from kvn.  Output per (row, head,
 // split): the unnormalized numerator [dh], the running max and the denominator.
 struct EAttn {

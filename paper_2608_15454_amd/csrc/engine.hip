@@ -625,13 +625,33 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
 }
 
 // --------------------------------------------------------------- attention ----
-// Block item (row i, head h, split s).  Wave w takes steps of KW keys starting at
-// lo + KW*w; G lanes share a key row (VEC elements each), so one load round covers
-// 64/G keys and a step is eight rounds.  The eight waves' (max, sum, numerator) are
-// combined in LDS and the block writes one partial.
+// Token values of an attention item's row that do not change between layers: batch
+// row, visible length, the first cache slot this pass writes, and the LCA group.
+struct AttnRow {
+  int b, kvlen, ns, gq;
+};
+
+__device__ __forceinline__ AttnRow attn_row(const ECall& c, int i) {
+  AttnRow r;
+  r.b = gld(c.tok.b + i);
+  r.kvlen = gld(c.tok.kvlen + i);
+  r.ns = gld(c.tok.slot + gld(c.first + i));
+  r.gq = c.grp_tab != nullptr ? gld(c.tok.grp + i) : 0;
+  return r;
+}
+
+// Block item (row i, head h, split s).  On a split over cached slots, wave 0 polls
+// the query and hands it to the block through LDS, while waves 1..EW-1 request their
+// first step's keys and values at once (a wave's memory counter drains in order, so
+// a wave holding cache requests would see the query only after them).  Wave w >= 1
+// takes steps of KW keys from lo + KW*(w-1); G lanes share a key row (VEC elements
+// each), so one load round covers 64/G keys and a step is eight rounds.  The split
+// over this pass's keys (read from kvn) uses all waves.  The waves' (max, sum,
+// numerator) are combined in LDS and the block writes one partial.  r0: the rows of
+// the block's first item (it = blockIdx.x), loaded once per launch.
 template <typename KV, int DH, class Late = NoHook>
 __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t base, uint32_t tag, int* err,
-                                        float* lds, Late&& late = Late()) {
+                                        float* lds, const AttnRow& r0, Late&& late = Late()) {
   constexpr int VEC = WT<KV>::VEC;
   constexpr int G = DH / VEC;                        // lanes per key row
   constexpr int KPR = 64 / G;                        // keys per load round
@@ -639,8 +659,10 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
   constexpr int NR = KW / KPR;
   float* wm = lds;
   float* wl = lds + EW;
-  float* wo = lds + 2 * EW;  // [EW][DH]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  float* wo = lds + 2 * EW;        // [EW][DH]
+  float* qs = wo + EW * DH;        // [DH] the item's scaled query
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int cq = lane % G, g = lane / G;
   const int S = c.S, H = a.H;
   const int items = c.M * H * S;
@@ -648,33 +670,33 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
   bool hooked = false;
   for (int it = blockIdx.x; it < items; it += gridDim.x) {
     const int s = it % S, h = (it / S) % H, i = it / (S * H);
-    const int b = gld(c.tok.b + i), kvlen = gld(c.tok.kvlen + i);
-    const int f = gld(c.first + i), ns = gld(c.tok.slot + f);
-    const int gq = c.grp_tab != nullptr ? gld(c.tok.grp + i) : 0;
+    const AttnRow rw = it == (int)blockIdx.x ? r0 : attn_row(c, i);
+    const int b = rw.b, kvlen = rw.kvlen, ns = rw.ns, gq = rw.gq;
+    const int f = gld(c.first + i);
     const int32_t* gt = c.grp_tab != nullptr ? c.grp_tab + (size_t)b * a.cap : nullptr;
     const bool fresh = s == S - 1;
-    const int lo = fresh ? ns : s * kEngineChunk;
-    const int hi = fresh ? kvlen : min(min(lo + kEngineChunk, ns), kvlen);
+    const int lo = fresh ? ns : s * c.chunk;
+    const int hi = fresh ? kvlen : min(min(lo + c.chunk, ns), kvlen);
     const size_t boff = (size_t)b * a.b_stride + (size_t)h * a.cap * DH + cq * VEC;
     const KV* kb = reinterpret_cast<const KV*>(a.kc) + boff;
     const KV* vb = reinterpret_cast<const KV*>(a.vc) + boff;
-    // the query entries are requested first, then the cached keys of the wave's first
-    // step (independent of the query), so both are in flight while the query's
-    // producer finishes; values and later steps load in the loop
-    const uint64_t* qp = a.q.ll + (size_t)i * a.q.ld + h * DH + cq * VEC;
-    uint64_t qraw[VEC];
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) qraw[v] = ll_load(qp + v);
     uint4 kr[NR], vr[NR];
-    int j0 = lo + wave * KW;
-    if (!fresh) {
+    int j0 = fresh || wave == 0 ? hi : lo + (wave - 1) * KW;  // wave 0: no cached keys
+    if (wave == 0) {
+      const uint64_t* qp = a.q.ll + (size_t)i * a.q.ld + h * DH + min(lane, DH - 1);
+      uint64_t qraw[1] = {ll_load(qp)};
+      ll_settle<1>(qraw, [&](int) { return qp; }, lane < DH ? 1u : 0u, base + a.q.tag, err);
+      if (lane < DH) qs[lane] = __uint_as_float((uint32_t)qraw[0]) * a.scale;
+    } else if (j0 < hi) {
 #pragma unroll
-      for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, max(hi - 1, 0)) * DH);
+      for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
+#pragma unroll
+      for (int r = 0; r < NR; ++r) vr[r] = ld16(vb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
     }
-    ll_settle<VEC>(qraw, [&](int v) { return qp + v; }, (1u << VEC) - 1u, base + a.q.tag, err);
+    lds_barrier();
     float q[VEC];
 #pragma unroll
-    for (int v = 0; v < VEC; ++v) q[v] = __uint_as_float((uint32_t)qraw[v]) * a.scale;
+    for (int v = 0; v < VEC; ++v) q[v] = qs[cq * VEC + v];
     if (!hooked) {  // the query has arrived: the next operation's requests go out now
       late();
       hooked = true;
@@ -686,13 +708,13 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
     for (int v = 0; v < VEC; ++v) o[v] = 0.f;
 
     if (!fresh) {
-      for (; j0 < hi; j0 += EW * KW) {
-        if (j0 != lo + wave * KW) {
+      for (; j0 < hi; j0 += (EW - 1) * KW) {
+        if (j0 != lo + (wave - 1) * KW) {
 #pragma unroll
           for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
-        }
 #pragma unroll
-        for (int r = 0; r < NR; ++r) vr[r] = ld16(vb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
+          for (int r = 0; r < NR; ++r) vr[r] = ld16(vb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
+        }
         float sc[NR];
         float mx = -INFINITY;
 #pragma unroll
@@ -932,10 +954,10 @@ __device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ
 // Every layer of a stack: QKV (RMSNorm, RoPE, KV append) -> split attention ->
 // merge -> output projection + residual -> gate/up (RMSNorm, SwiGLU) -> down
 // projection + residual.  ops holds six operations per layer.  Each linear layer's
-// first weight slice is requested ahead: the output projection's once the query has
-// arrived in the attention, gate/up's and down's right after the previous linear
-// layer's dot products, and QKV's as the layer starts (a request from the previous
-// layer would keep those registers live across the whole loop).
+// first weight slice is requested ahead: the output projection's after the
+// attention, gate/up's and down's after the previous linear layer's output stores,
+// and QKV's as the layer starts (a request from the previous layer would keep those
+// registers live across the whole loop).
 template <class SH, bool MULTI>
 __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops, int nlayers, ECall c, uint32_t base,
                                                     int* err) {
@@ -952,6 +974,8 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
   auto att = [&](int i) -> const EAttn& { return *(const EAttn*)&cops[i].at; };
   auto mrg = [&](int i) -> const EMerge& { return *(const EMerge*)&cops[i].mg; };
   const QkvItem qi = qkv_item<SH>(lin(0), c, pq);
+  const AttnRow ar = blockIdx.x < (unsigned)(c.M * att(1).H * c.S) ? attn_row(c, blockIdx.x / (att(1).H * c.S))
+                                                                  : AttnRow{0, 0, 0, 0};
 #pragma unroll 1
   for (int l = 0; l < nlayers; ++l) {
     const int o = 6 * l;
@@ -959,7 +983,8 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
     op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>(), true>(
         lin(o), c, base, base + cops[o].tag, err, lds, pq, &qi);
     lds_barrier();
-    op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, [&] { weights_ahead(lin(o + 3), po); });
+    op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, ar);
+    weights_ahead(lin(o + 3), po);
     lds_barrier();
     op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err);
     op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>(), false>(

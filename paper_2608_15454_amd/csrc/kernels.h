@@ -69,7 +69,7 @@ struct Linear {
 };
 
 // Split-K scratch of the matrix-core linear path, in floats.
-constexpr int64_t kGemmPartFloats = (int64_t)1 << 20;
+constexpr int64_t kGemmPartFloats = (int64_t)1 << 23;
 
 // Attention of M query rows (Q [M, ldq], head h at columns h*dh) over a KV cache.
 struct Attn {

@@ -259,8 +259,11 @@ constexpr int kMfmaBK = 64, kMfmaLD = kMfmaBK + 8;  // LDS row pitch in bf16 ele
 
 // With ksplit > 1, block z covers K steps [z*nk/ksplit, (z+1)*nk/ksplit) and writes its
 // raw sums to L.part[z][m][n]; gemm_finish_kernel adds the splits and applies the
-// epilogue.
-__global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, const float* inv_rms, int ksplit) {
+// epilogue.  RMSNorm (L.gain set): the staged activations are scaled by the gain
+// only; each block sums the squares of the rows it stages and the row's 1/RMS
+// multiplies the dot products at the end (the partial sums of squares of a split go
+// to L.part after the [ksplit][M][N] partials, written by the blocks of column 0).
+__global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   constexpr int BM = 64, BN = 64, BK = kMfmaBK, LD = kMfmaLD;
   __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LD];  // hi halves of X
   __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LD];  // lo halves of X
@@ -273,18 +276,19 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, const float* i
   const bool aok = am < L.M;
   const float* arow = L.X + (size_t)(aok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx;
   const bool norm = L.gain != nullptr;
-  const float ascale = (norm && aok) ? inv_rms[am] : 1.0f;
   const float* ag = norm ? row_gain(L, aok ? am : 0) : nullptr;
   const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K);
   float a[16];
+  float ss = 0.f;  // sum of squares of this thread's staged elements (norm)
   uint4 b0, b1;
   auto fetch = [&](int k0) {
 #pragma unroll
     for (int v = 0; v < 16; v += 4) {
       float4 t = aok ? *reinterpret_cast<const float4*>(arow + k0 + lk + v) : make_float4(0.f, 0.f, 0.f, 0.f);
       if (norm && aok) {
+        ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
         const float4 g = *reinterpret_cast<const float4*>(ag + k0 + lk + v);
-        t.x *= ascale * g.x; t.y *= ascale * g.y; t.z *= ascale * g.z; t.w *= ascale * g.w;
+        t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
       }
       a[v] = t.x; a[v + 1] = t.y; a[v + 2] = t.z; a[v + 3] = t.w;
     }
@@ -340,6 +344,9 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, const float* i
   const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
   const int j = lane & 31;
   const int n = n0 + wn * 32 + j;
+  // the four threads of a staged row hold its sum of squares over this block's K range
+  ss += __shfl_xor(ss, 1);
+  ss += __shfl_xor(ss, 2);
   if (ksplit > 1) {
     float* pp = L.part + (size_t)blockIdx.z * L.M * L.N;
 #pragma unroll
@@ -347,12 +354,17 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, const float* i
       const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       if (m < L.M) pp[(size_t)m * L.N + n] = acc[r];
     }
+    if (norm && blockIdx.x == 0 && (tid & 3) == 0 && aok)
+      L.part[(size_t)ksplit * L.M * L.N + (size_t)blockIdx.z * L.M + am] = ss;
     return;
   }
+  __shared__ float rs[BM];  // 1 / RMS of the tile's rows
+  if (norm && (tid & 3) == 0) rs[lr] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
+  __syncthreads();
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-    const float val = acc[r];
+    const float val = norm ? acc[r] * rs[m - m0] : acc[r];
     const float partner = __shfl_down(val, 1);  // column n + 1, same row
     if (m >= L.M) continue;
     if (!pair) epi_single(L.epi, m, n, val);
@@ -374,6 +386,13 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) 
     const float* pp = L.part + ((size_t)z * L.M + m) * L.N + n;
     a0 += pp[0];
     if (pair) a1 += pp[1];
+  }
+  if (L.gain != nullptr) {  // RMSNorm: 1/RMS of the row from the splits' sums of squares
+    float ss = 0.f;
+    for (int z = 0; z < ksplit; ++z) ss += L.part[(size_t)ksplit * L.M * L.N + (size_t)z * L.M + m];
+    const float sc = 1.0f / sqrtf(ss / (float)L.K + L.eps);
+    a0 *= sc;
+    a1 *= sc;
   }
   if (pair) epi_pair(L.epi, m, n, a0, a1);
   else epi_single(L.epi, m, n, a0);
@@ -805,6 +824,8 @@ hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
 
 // Linears of more rows than this use the matrix cores (bfloat16 weights).
 constexpr int kMfmaMinRows = 16;
+// split K until about this many blocks stream the weights (two 55 KiB blocks fit a CU)
+constexpr int kMfmaTargetBlocks = 512;
 
 template <typename W>
 bool mfma_fits(const Linear& L) {
@@ -814,21 +835,16 @@ bool mfma_fits(const Linear& L) {
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
   if (mfma_fits<W>(L)) {
-    // split K until about 256 blocks stream the weights (the partials must fit)
+    // split K until about kMfmaTargetBlocks blocks stream the weights (the partials
+    // and the splits' sums of squares must fit)
     const int tiles = (L.N / 64) * ((L.M + 63) / 64);
     const int nk = L.K / kMfmaBK;
     int ks = 1;
-    while (L.part != nullptr && tiles * ks * 2 <= 256 && ks * 2 <= nk &&
-           (int64_t)ks * 2 * L.M * L.N <= kGemmPartFloats)
+    while (L.part != nullptr && tiles * ks * 2 <= kMfmaTargetBlocks && ks * 2 <= nk &&
+           (int64_t)ks * 2 * L.M * (L.N + 1) <= kGemmPartFloats)
       ks *= 2;
     const dim3 grid(L.N / 64, (L.M + 63) / 64, ks);
-    const bool first_is_rms = L.gain != nullptr;
-    if (first_is_rms) {
-      hipError_t e = klaunch(rms_kernel, dim3((L.M + 3) / 4), dim3(256), 0, st, ev.start, nullptr, L, inv_rms);
-      if (e != hipSuccess) return e;
-    }
-    hipError_t e = klaunch(gemm_mfma_kernel, grid, dim3(256), 0, st, first_is_rms ? nullptr : ev.start,
-                           ks > 1 ? nullptr : ev.stop, L, (const float*)inv_rms, ks);
+    hipError_t e = klaunch(gemm_mfma_kernel, grid, dim3(256), 0, st, ev.start, ks > 1 ? nullptr : ev.stop, L, ks);
     if (e != hipSuccess || ks == 1) return e;
     const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
     const int64_t items = (int64_t)L.M * (pair ? L.N / 2 : L.N);

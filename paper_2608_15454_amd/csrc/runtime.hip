@@ -150,7 +150,7 @@ Sizes sizes_of(const mbp_config& c) {
   s.part_floats_mb = sw > 1 ? (int64_t)s.Mm * s.H * sw * (s.dh + 2) : 0;
   s.es = c.kv_dtype == MBP_F32 ? 4 : 2;
   const int ex = kEngineMaxRows;
-  s.Esplit = std::min(64, (s.Tcap + kEngineChunk - 1) / kEngineChunk + 1);
+  s.Esplit = kEngineMaxSplits;
   s.ll_entries = (int64_t)ex * s.d * 7 + (int64_t)ex * s.dff + (int64_t)ex * s.H * s.Esplit * (s.dh + 2);
   s.eng_ops = 6 * (c.n_enc + c.n_lm + c.n_nb + (c.head == MBP_HEAD_LCA ? c.n_mb : 0));
   return s;
@@ -373,6 +373,7 @@ struct mbp_handle {
   // persistent engine
   bool engine = false;
   int eng_shape = -1;
+  int eng_grid = 0;  // blocks of an engine launch
   EngStack es_enc, es_lm, es_nt, es_mb;
   uint32_t tag_base = 1;
   EOp* d_ops = nullptr;
@@ -549,7 +550,7 @@ double stack_bytes(const mbp_handle* h, int nlayers, int M, double kv_rows) {
 
 // One pass through a stack in the persistent engine (see engine.hip).
 int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, const Tok& tok, const int32_t* first,
-               const int32_t* first_slot, int S, const int32_t* grp_tab, double kv_rows, hipStream_t st) {
+               const int32_t* first_slot, int S, int chunk, const int32_t* grp_tab, double kv_rows, hipStream_t st) {
   ECall c;
   c.io = io;
   c.M = tok.M;
@@ -558,6 +559,7 @@ int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, co
   c.first_slot = first_slot;
   c.grp_tab = grp_tab;
   c.S = S;
+  c.chunk = chunk;
   if (h->tag_base > 0xF0000000u) {  // restart the tags before they wrap: clear the tagged buffers
     HIPCK(h, hipMemsetAsync(h->R<uint64_t>(h->rg.ll), 0, (size_t)h->sz.ll_entries * 8, st));
     h->tag_base = 1;
@@ -638,9 +640,14 @@ int run_pass(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, con
   const int M = tok.M;
   if (M == 0) return MBP_OK;
   if (h->engine && es != nullptr && es->nops > 0 && !tiled && M <= kEngineMaxRows) {
-    const int S = (max_ns + kEngineChunk - 1) / kEngineChunk + 1;
+    // cached keys per attention split: as few as keep the (row, head, split) items
+    // within one per block, so the cache reads are spread over every compute unit
+    const int items_per_split = M * s.H;
+    const int cached_splits = std::max(1, h->eng_grid / items_per_split - 1);
+    const int chunk = std::max(64, (max_ns + cached_splits - 1) / cached_splits + 63) / 64 * 64;
+    const int S = (max_ns + chunk - 1) / chunk + 1;
     if (S <= s.Esplit)
-      return run_engine(h, *es, (int)layers.size(), io, tok, first, first_slot, S, grp_tab, kv_rows, st);
+      return run_engine(h, *es, (int)layers.size(), io, tok, first, first_slot, S, chunk, grp_tab, kv_rows, st);
   }
   if (io.emb != nullptr) {
     OTHER(h, launch_embed, io.emb, h->wdt, io.ie, X, s.d, M, st);
@@ -1056,6 +1063,7 @@ int build_engine(mbp_handle* h) {
   const int shape = engine_shape(h->wdt, c.kv_dtype, s.dh, s.d, s.dff);
   if (shape < 0 || engine_grid(shape) <= 0) return MBP_OK;
   h->eng_shape = shape;
+  h->eng_grid = engine_grid(shape);
   const int ex = kEngineMaxRows;
   uint64_t* x0 = h->R<uint64_t>(h->rg.ll);
   uint64_t* x1 = x0 + (size_t)ex * s.d;
