@@ -173,27 +173,42 @@ __device__ __forceinline__ float ein_get(const EIn& x, const ECall& c, int m, in
 // launch still finishes.
 template <int N, class Addr>
 __device__ __forceinline__ void ll_settle(uint64_t (&v)[N], Addr&& addr, uint32_t live, uint32_t tag, int* err) {
-  auto any_stale = [&] {
+  auto stale = [&](const uint64_t(&x)[N]) {
     bool st = false;
 #pragma unroll
-    for (int j = 0; j < N; ++j) st |= ((live >> j) & 1u) && (uint32_t)(v[j] >> 32) != tag;
-    return st;
+    for (int j = 0; j < N; ++j) st |= ((live >> j) & 1u) && (uint32_t)(x[j] >> 32) != tag;
+    return __builtin_amdgcn_ballot_w64(st) != 0;
   };
-  if (__builtin_amdgcn_ballot_w64(any_stale()) == 0) return;
+  if (!stale(v)) return;
+  // Small batches take two samples per round trip (w, then v a short gap later, both
+  // in flight before w is checked), so a value that lands during a round trip is
+  // seen about half a round trip sooner.  v is requested after w, so when w is
+  // complete v is too.  Larger batches take one sample at a time (registers).
+  constexpr bool kTwo = N <= 4;
   const uint64_t t0 = __builtin_amdgcn_s_memrealtime();
+  uint64_t w[kTwo ? N : 1];
   for (int it = 1;; ++it) {
-    if ((it & 15) == 0) {
+    if ((it & 7) == 0) {
       if (err_get(err) != 0) return;
       if (__builtin_amdgcn_s_memrealtime() - t0 > kWaitTicks) {
         __hip_atomic_store((GLOBAL int*)err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return;
       }
     }
-    __builtin_amdgcn_s_sleep(1);
+    if constexpr (kTwo) {
+#pragma unroll
+      for (int j = 0; j < N; ++j) w[j] = ((live >> j) & 1u) ? ll_load(addr(j)) : 0ull;
+      __builtin_amdgcn_s_sleep(6);
+    } else {
+      __builtin_amdgcn_s_sleep(1);
+    }
 #pragma unroll
     for (int j = 0; j < N; ++j)
       if ((live >> j) & 1u) v[j] = ll_load(addr(j));
-    if (__builtin_amdgcn_ballot_w64(any_stale()) == 0) return;
+    if constexpr (kTwo) {
+      if (!stale(w)) return (void)stale(v);  // waits for v, complete as well
+    }
+    if (!stale(v)) return;
   }
 }
 
@@ -233,32 +248,42 @@ __device__ __forceinline__ void stage_rows(const EIn& x, const ECall& c, int m0,
     }
   } else {
     const uint32_t tag = base + x.tag;
-    constexpr int U = 8;
-    for (int eb = wave * 64; eb < n; eb += EB * U) {
-      // entry j of the batch: the wave's 64 entries from ej = eb + j*EB (uniform)
-      auto addr = [&](int j) {
-        const int ej = min(eb + j * EB, n - 64);
-        const int m = ej / K;
-        return x.ll + (size_t)(m0 + m) * x.ld + (ej - m * K) + lane;
-      };
-      uint64_t v[U];
-      uint32_t live = 0;
+    // batches of U entries per thread: two when the rows fit in one batch of two (a
+    // single row of up to 1024 entries, polled with two samples per round trip),
+    // else eight
+    auto batches = [&](auto u) {
+      constexpr int U = decltype(u)::value;
+      for (int eb = wave * 64; eb < n; eb += EB * U) {
+        // entry j of the batch: the wave's 64 entries from ej = eb + j*EB (uniform)
+        auto addr = [&](int j) {
+          const int ej = min(eb + j * EB, n - 64);
+          const int m = ej / K;
+          return x.ll + (size_t)(m0 + m) * x.ld + (ej - m * K) + lane;
+        };
+        uint64_t v[U];
+        uint32_t live = 0;
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
-        const bool in = eb + j * EB < n;
-        v[j] = in ? ll_load(addr(j)) : 0ull;
-        live |= in ? 1u << j : 0u;
-      }
-      ll_settle<U>(v, addr, live, tag, err);
+        for (int j = 0; j < U; ++j) {
+          const bool in = eb + j * EB < n;
+          v[j] = in ? ll_load(addr(j)) : 0ull;
+          live |= in ? 1u << j : 0u;
+        }
+        ll_settle<U>(v, addr, live, tag, err);
 #pragma unroll
-      for (int j = 0; j < U; ++j) {
-        const int ej = eb + j * EB;
-        if (ej < n) {
-          const float val = __uint_as_float((uint32_t)v[j]);
-          lds[ej + lane] = val;
-          if (ssw != nullptr) add(ej / K, val * val);
+        for (int j = 0; j < U; ++j) {
+          const int ej = eb + j * EB;
+          if (ej < n) {
+            const float val = __uint_as_float((uint32_t)v[j]);
+            lds[ej + lane] = val;
+            if (ssw != nullptr) add(ej / K, val * val);
+          }
         }
       }
+    };
+    if (n <= 2 * EB) {
+      batches(std::integral_constant<int, 2>());
+    } else {
+      batches(std::integral_constant<int, 8>());
     }
   }
   if (ssw != nullptr) flush();
