@@ -27,7 +27,7 @@ using namespace dev;
 
 constexpr int EB = 512;            // threads per block
 constexpr int EW = EB / 64;        // waves per block
-constexpr int kLdsFloats = 16384;  // 64 KiB of LDS per block
+constexpr int kLdsFloats = 40960;  // 160 KiB of LDS per block (gfx950)
 constexpr int kSsFloats = kEngineMaxRows * EW;  // per-wave sums of squares of staged rows
 constexpr int kStage = kLdsFloats - kSsFloats;   // staged input rows; the rest holds the sums
 constexpr uint64_t kWaitTicks = 20000000ull;  // 200 ms of the 100 MHz real-time counter
