@@ -82,7 +82,7 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *                             more mantissa bits; values beyond +-65504 saturate.
  *   no_engine                 0: passes of at most 16 token rows through a
  *                             transformer stack run in the persistent engine (one
- *                             cooperative launch per stack, layers chained through
+ *                             launch per stack, layers chained through
  *                             tagged device-coherent stores) when the dimensions
  *                             allow it; 1: one kernel launch per layer operation.
  *                             Both give the same results up to float32 rounding

@@ -1,5 +1,6 @@
-// Persistent decode engine: one cooperative launch runs a list of operations (the
-// layers of a transformer stack for a handful of token rows) with no grid barrier.
+// Persistent decode engine: one launch of one block per compute unit runs a list of
+// operations (the layers of a transformer stack for a handful of token rows) with no
+// grid barrier.
 // Every intermediate value is written as a 64-bit entry {tag, float32 bits} with a
 // device-coherent store, and its consumers poll the entries until the tag of the
 // producing operation appears.  Internal interface between runtime.hip and

@@ -1,14 +1,17 @@
 // gfx950 persistent decode engine.
 //
-// One cooperative launch (one block of eight waves per compute unit) runs the
-// operations of a transformer stack for the few token rows of a decode pass.  There
+// One launch of one block of eight waves per compute unit (all resident at once on an
+// otherwise idle device) runs the operations of a transformer stack for the few token
+// rows of a decode pass, reading its input rows and writing its output rows itself.
+// There
 // is no grid barrier: every value an operation produces is stored as a 64-bit entry
 // {tag, float32 bits} with a device-coherent store, and the blocks that consume it
 // poll the entries until the producer's tag is there.  A dependent step therefore
 // costs one store-to-load trip through the device coherence point instead of a
 // kernel boundary (end-of-kernel cache write-back plus the next dispatch).  Each
-// linear layer still reads every weight byte once: a wave loads its weight rows into
-// registers before it polls the inputs, so the weight fetch overlaps the wait.
+// linear layer still reads every weight byte once: a wave holds its weight rows in
+// registers, requested before it polls the inputs (or during the previous
+// operation), so the weight fetch overlaps the wait.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 

@@ -7,12 +7,12 @@
 // cache, last NT row) lives in the caller's device workspace.
 //
 // Passes of a few token rows through a transformer stack (decode steps) run in the
-// persistent engine of engine.hip, one cooperative launch per stack; long passes
-// (prefill) use the per-kernel path.  Without the engine, a second stream of the
-// library's own runs the LCA window update of the next step concurrently with the NT
-// decoder (both depend only on the encoder and LM outputs of the commit), joined by an
-// event before the head; with it, every launch stays on the caller's stream, since a
-// cooperative launch needs the compute units to itself.
+// persistent engine of engine.hip, one launch per stack; long passes (prefill) use
+// the per-kernel path.  Without the engine, a second stream of the library's own runs
+// the LCA window update of the next step concurrently with the NT decoder (both
+// depend only on the encoder and LM outputs of the commit), joined by an event before
+// the head; with it, every launch stays on the caller's stream, since an engine launch
+// needs the compute units to itself.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
