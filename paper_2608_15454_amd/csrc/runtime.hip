@@ -216,7 +216,7 @@ Regions layout(const mbp_config& c) {
   r.mb.inv = take((size_t)s.Mm * 4);
   r.mb.part = take((size_t)std::max<int64_t>(s.part_floats_mb, 1) * 4);
   r.mb.gpart = take((size_t)kGemmPartFloats * 4);
-  r.plan_ints = (size_t)20 * s.Ml + (size_t)s.B * s.Wcap + 64;
+  r.plan_ints = (size_t)40 * s.Ml + (size_t)2 * s.B * s.Wcap + 256;
   for (int i = 0; i < kPlans; ++i) r.plan[i] = take(r.plan_ints * 4);
   r.active = take((size_t)s.B * 4);
   r.ll = take((size_t)s.ll_entries * 8);
@@ -333,6 +333,11 @@ struct mbp_handle {
   bool mb_pending = false;   // the caller's stream has not yet waited for ev_mb
   bool mb_recorded = false;  // ev_mb was recorded at least once
   int n_hint = 3;
+  // window update and head rows of the next step, prepared by the last commit (plan
+  // 0) for n = pre_n candidates (engine path, LCA head)
+  bool pre_draft = false;
+  int pre_n = 0;
+  size_t pre_o_hr = 0, pre_o_md = 0;
   char* ws;
   bool poisoned = false;
   std::string err;
@@ -788,6 +793,8 @@ int mb_update(mbp_handle* h, int n, Plan& p, hipStream_t st, bool clamp) {
   return mb_launch(h, p, mp, st);
 }
 
+void head_rows_of(mbp_handle* h, int n, std::vector<int32_t>& head_rows, std::vector<int32_t>& mlp_dst);
+
 // Make the caller's stream wait for a forked MB update.
 int mb_join(mbp_handle* h) {
   if (h->mb_pending) {
@@ -827,6 +834,10 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
   const bool fork = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty() && !h->engine;
+  // with the engine, the next step's window update runs right after the NT decoder
+  // on the same stream, prepared in the commit's plan (and the head rows with it)
+  const bool pre = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty() && h->engine;
+  h->pre_draft = false;
   size_t first = 0;
   bool first_chunk = true;
   while (first < items.size()) {
@@ -890,6 +901,16 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_nts = p.add(nt_src), o_lo = p.add(lo_row),
                  o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_h1 = p.add(h1_dst), o_te = p.add(tiles_e),
                  o_tl = p.add(tiles_l);
+    const bool pre_here = pre && last == items.size();
+    MbPass mp_next;
+    size_t o_hr = 0, o_md = 0;
+    if (pre_here) {
+      RCK(mb_prepare(h, h->n_hint, p, true, &mp_next));
+      std::vector<int32_t> head_rows, mlp_dst;
+      head_rows_of(h, h->n_hint, head_rows, mlp_dst);
+      o_hr = p.add(head_rows);
+      o_md = p.add(mlp_dst);
+    }
     RCK(upload(h, p, h->st));
     const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
 
@@ -928,6 +949,13 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     ion.oi2 = p.at(o_h1);
     RCK(run_pass(h, h->nt, h->kv_nt, &h->es_nt, ion, X, tok_e, nullptr, tiled_e, p.at(o_te),
                  (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
+    if (pre_here) {
+      RCK(mb_launch(h, p, mp_next, h->st));
+      h->pre_draft = true;
+      h->pre_n = h->n_hint;
+      h->pre_o_hr = o_hr;
+      h->pre_o_md = o_md;
+    }
     if (fork_here) {
       // the next step's window update, enqueued after the NT decoder (the critical
       // path) but ordered only after the LM module; its plan reuses a host buffer
@@ -978,31 +1006,15 @@ int check_ready(mbp_handle* h) {
   return MBP_OK;
 }
 
-// Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
-// per-row greedy bytes / probabilities (and accept_len in threshold mode).
-int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len,
-          bool host_out) {
+// head_rows[b*n + m]: the row of `rows` holding the hidden state of candidate m of
+// batch row b; mlp_dst: the MLP-head output rows (MLP head only).
+void head_rows_of(mbp_handle* h, int n, std::vector<int32_t>& head_rows, std::vector<int32_t>& mlp_dst) {
   const Sizes& s = h->sz;
-  const mbp_config& c = h->cfg;
   const Regions& rg = h->rg;
   const int B = h->batch;
-  const bool lca = c.head == MBP_HEAD_LCA;
-  // one plan upload for the window update (rows a forked update did not cover) and
-  // the head
-  Plan& p = h->plan[1];
-  p.clear();
-  MbPass mp;
-  if (lca) {
-    RCK(mb_join(h));
-    RCK(mb_prepare(h, n, p, false, &mp));
-  }
-  float* h1 = h->row_ptr(rg.row_h1);
-  float* mlp_out = h->row_ptr(rg.row_mlp);
-  float* logits = h->R<float>(rg.logits);
-  const Scratch& sc = h->sc_main;
-
-  // head_rows[b*n + m]: row of `rows` holding the hidden state of candidate m of row b
-  std::vector<int32_t> head_rows((size_t)B * n), mlp_dst;
+  const bool lca = h->cfg.head == MBP_HEAD_LCA;
+  head_rows.assign((size_t)B * n, 0);
+  mlp_dst.clear();
   for (int b = 0; b < B; ++b) {
     head_rows[(size_t)b * n] = rg.row_h1 + b;
     if (n < 2) continue;
@@ -1017,9 +1029,42 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
   if (!lca)
     for (int m = 1; m < n; ++m)
       for (int b = 0; b < B; ++b) mlp_dst.push_back(rg.row_mlp + b * s.nmax + m);
-  const size_t o_hr = p.add(head_rows), o_md = p.add(mlp_dst);
-  RCK(upload(h, p, h->st));
-  if (lca) RCK(mb_launch(h, p, mp, h->st));
+}
+
+// Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
+// per-row greedy bytes / probabilities (and accept_len in threshold mode).
+int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len,
+          bool host_out) {
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  const Regions& rg = h->rg;
+  const int B = h->batch;
+  const bool lca = c.head == MBP_HEAD_LCA;
+  float* h1 = h->row_ptr(rg.row_h1);
+  float* mlp_out = h->row_ptr(rg.row_mlp);
+  float* logits = h->R<float>(rg.logits);
+  const Scratch& sc = h->sc_main;
+  // the window update and head rows: already run by the last commit for this n, or
+  // one plan upload for the window update (rows a forked update did not cover) and
+  // the head
+  const bool pre = lca && h->pre_draft && h->pre_n == n;
+  h->pre_draft = false;
+  Plan& p = pre ? h->plan[0] : h->plan[1];
+  size_t o_hr = h->pre_o_hr, o_md = h->pre_o_md;
+  if (!pre) {
+    p.clear();
+    MbPass mp;
+    if (lca) {
+      RCK(mb_join(h));
+      RCK(mb_prepare(h, n, p, false, &mp));
+    }
+    std::vector<int32_t> head_rows, mlp_dst;
+    head_rows_of(h, n, head_rows, mlp_dst);
+    o_hr = p.add(head_rows);
+    o_md = p.add(mlp_dst);
+    RCK(upload(h, p, h->st));
+    if (lca) RCK(mb_launch(h, p, mp, h->st));
+  }
 
   if (!lca) {
     for (int m = 1; m < n; ++m) {
@@ -1534,6 +1579,7 @@ extern "C" int mbp_reset(mbp_handle* h) {
     (void)hipStreamSynchronize(h->st);
   }
   h->mb_pending = false;
+  h->pre_draft = false;
   h->rows.assign(h->sz.B, Row());
   h->batch = 0;
   h->pending = false;
