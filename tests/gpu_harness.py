@@ -79,12 +79,15 @@ def new_decoder(model, W, batch, max_ctx, max_n=8, **kw):
 
 
 def forced_run(dec, W, model, prompts, steps, n, tau, mode=THRESHOLD, tol=None, label=""):
-    """Teacher-forced comparison over ``steps`` steps; returns Stats."""
+    """Teacher-forced comparison over ``steps`` steps; returns Stats.  ``n`` is the
+    candidate count of every step, or a list cycled over the steps."""
     tol = base_tol(model) if tol is None else tol
     dec.prefill(prompts)
     xs = [[int(b) for b in p] for p in prompts]
     st = Stats()
+    ns = list(n) if isinstance(n, (list, tuple)) else [n]
     for s in range(steps):
+        n = ns[s % len(ns)]
         refs = [oracle.step(W, model, x, n, tau) if mode == THRESHOLD else oracle.verify_step(W, model, x, n)
                 for x in xs]
         cand, prob, alen = dec.decode_step(n, tau, mode)

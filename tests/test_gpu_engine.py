@@ -46,6 +46,20 @@ def test_engine_small_f32_forced(small, n, tau):
 
 
 @pytest.mark.timeout(300)
+def test_engine_small_f32_varying_n(small):
+    """The candidate count changes between steps: a commit prepares the next step's
+    window update for the previous n, so steps with another n take the general path
+    (and rows computed for a smaller n are extended)."""
+    raw, W = small
+    dec = new_decoder(SMALL, raw, 1, 700)
+    dec.set_timing(True)
+    st = forced_run(dec, W, SMALL, [synth.make_prompt(5, 260)], 12, [3, 5, 2, 5, 4, 1, 6], 0.5, tol=TOL,
+                    label="engine f32 varying n")
+    print(st)
+    assert engine_launches(dec) > 0
+
+
+@pytest.mark.timeout(300)
 def test_engine_small_f32_batched(small):
     """Three rows of different lengths: passes hold 1..3 rows per batch row."""
     raw, W = small
