@@ -937,7 +937,7 @@ __device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32
 // A model shape the engine is compiled for: weight and cache types, head size, the
 // two inner sizes, and output rows per wave of the four linear layers of a block.
 template <typename W_, typename KV_, int DH_, int D_, int F_, int QNS, int QR, int ONS, int OR_, int GNS, int GR,
-          int DNS, int DR>
+          int DNS, int DR, int AH_>
 struct Shape {
   using W = W_;
   using KV = KV_;
@@ -946,6 +946,10 @@ struct Shape {
   static constexpr int KCD = D / (64 * VEC), KCF = F / (64 * VEC);
   // (K-slices, rows per wave) of the QKV, output, gate/up and down projections
   static constexpr int NSQ = QNS, RQ = QR, NSO = ONS, RO = OR_, NSG = GNS, RG = GR, NSD = DNS, RD = DR;
+  // when the weights of gate/up and down are requested with the output projection's
+  // (right after the attention) instead of one linear layer ahead: 0 never, 1 for
+  // single-row passes, 2 always (where the registers allow it without spills)
+  static constexpr int AH = AH_;
 };
 
 // Input rows per pass: one for single-row passes, else as many as keep R * MR <= 16
@@ -985,7 +989,11 @@ __device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ
 // first weight slice is requested ahead: the output projection's after the
 // attention, gate/up's and down's after the previous linear layer's output stores,
 // and QKV's as the layer starts (a request from the previous layer would keep those
-// registers live across the whole loop).
+// registers live across the whole loop).  With SH::AH, gate/up's and down's go out
+// with the output projection's: the merge and output-projection hops then hide
+// their arrival.  A block's requests are served in order, so a burst requested
+// right before a poll delays that poll until the burst has arrived; the early
+// requests move the two largest bursts away from the gate/up and down polls.
 template <class SH, bool MULTI>
 __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops, int nlayers, ECall c, uint32_t base,
                                                     int* err) {
@@ -1001,6 +1009,7 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
   auto lin = [&](int i) -> const ELinear& { return *(const ELinear*)&cops[i].lin; };
   auto att = [&](int i) -> const EAttn& { return *(const EAttn*)&cops[i].at; };
   auto mrg = [&](int i) -> const EMerge& { return *(const EMerge*)&cops[i].mg; };
+  constexpr bool kAhead = SH::AH == 2 || (SH::AH == 1 && !MULTI);
   const QkvItem qi = qkv_item<SH>(lin(0), c, pq);
   const AttnRow ar = blockIdx.x < (unsigned)(c.M * att(1).H * c.S) ? attn_row(c, blockIdx.x / (att(1).H * c.S))
                                                                   : AttnRow{0, 0, 0, 0};
@@ -1013,13 +1022,21 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
     lds_barrier();
     op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, ar);
     weights_ahead(lin(o + 3), po);
+    if constexpr (kAhead) {
+      weights_ahead(lin(o + 4), pg);
+      weights_ahead(lin(o + 5), pd);
+    }
     lds_barrier();
     op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err);
     op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>(), false>(
-        lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr, [&] { weights_ahead(lin(o + 4), pg); });
+        lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr, [&] {
+          if constexpr (!kAhead) weights_ahead(lin(o + 4), pg);
+        });
     lds_barrier();
     op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>(), true>(
-        lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr, [&] { weights_ahead(lin(o + 5), pd); });
+        lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr, [&] {
+          if constexpr (!kAhead) weights_ahead(lin(o + 5), pd);
+        });
     lds_barrier();
     op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>(), false>(
         lin(o + 5), c, base, base + cops[o + 5].tag, err, lds, pd, nullptr);
@@ -1029,9 +1046,9 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
 
 // The shapes compiled in (index = EngineShape id).
 // Tiles: 256 tiles (one per block of a 256-CU grid) wherever the row count allows.
-using Shape0 = Shape<uint16_t, _Float16, 64, 1024, 4096, 2, 3, 2, 1, 2, 8, 8, 4>;    // bf16, d 1024
-using Shape1 = Shape<uint16_t, _Float16, 64, 2048, 8192, 4, 6, 4, 4, 4, 8, 8, 4>;    // bf16, d 2048
-using Shape2 = Shape<float, float, 64, 256, 1024, 1, 1, 1, 1, 1, 1, 4, 1>;           // float32, d 256
+using Shape0 = Shape<uint16_t, _Float16, 64, 1024, 4096, 2, 3, 2, 1, 2, 8, 8, 4, 1>;    // bf16, d 1024
+using Shape1 = Shape<uint16_t, _Float16, 64, 2048, 8192, 4, 6, 4, 4, 4, 8, 8, 4, 0>;    // bf16, d 2048
+using Shape2 = Shape<float, float, 64, 256, 1024, 1, 1, 1, 1, 1, 1, 4, 1, 2>;           // float32, d 256
 
 template <class SH, bool MULTI>
 int grid_of() {
