@@ -752,8 +752,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
           float dot = 0.f;
 #pragma unroll
           for (int v = 0; v < VEC; ++v) dot += q[v] * fk[v];
-#pragma unroll
-          for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
+          dot = group_sum<G>(dot);
           const int j = j0 + r * KPR + g;
           bool vis = j < hi;
           if (vis && gt != nullptr) {
@@ -763,8 +762,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
           sc[r] = vis ? dot : -INFINITY;
           mx = fmaxf(mx, sc[r]);
         }
-#pragma unroll
-        for (int off = G; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        mx = across_max<G>(mx);
         if (mx == -INFINITY) continue;  // wave-uniform
         const float m_new = fmaxf(m_run, mx);
         const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
@@ -816,8 +814,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
 #pragma unroll
             for (int v = 0; v < VEC; ++v) vrow[r][v] = 0.f;
           }
-#pragma unroll
-          for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
+          dot = group_sum<G>(dot);
           bool vis = in;
           if (vis && gt != nullptr) {
             const int gj = gld(gt + j);
@@ -826,8 +823,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
           sc[r] = vis ? dot : -INFINITY;
           mx = fmaxf(mx, sc[r]);
         }
-#pragma unroll
-        for (int off = G; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+        mx = across_max<G>(mx);
         if (mx == -INFINITY) continue;
         const float m_new = fmaxf(m_run, mx);
         const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
@@ -846,12 +842,9 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
       }
     }
     // sum over the lanes that share a dimension chunk (different keys, same m_run)
+    l_run = across_sum<G>(l_run);
 #pragma unroll
-    for (int off = G; off < 64; off <<= 1) {
-      l_run += __shfl_xor(l_run, off);
-#pragma unroll
-      for (int v = 0; v < VEC; ++v) o[v] += __shfl_xor(o[v], off);
-    }
+    for (int v = 0; v < VEC; ++v) o[v] = across_sum<G>(o[v]);
     lds_barrier();  // the previous item's readers of wm / wl / wo are done
     if (lane < G) {
 #pragma unroll
@@ -926,7 +919,7 @@ __device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const int s = s0 + j;
-        const float ws = __shfl(w, min(s, 63));
+        const float ws = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, w), min(s, 63)));  // s is wave-uniform
         if (s < S && lane < DH && ws != 0.f) num += ws * __uint_as_float((uint32_t)v[j]);
       }
     }

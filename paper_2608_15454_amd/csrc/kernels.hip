@@ -345,8 +345,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   const int j = lane & 31;
   const int n = n0 + wn * 32 + j;
   // the four threads of a staged row hold its sum of squares over this block's K range
-  ss += __shfl_xor(ss, 1);
-  ss += __shfl_xor(ss, 2);
+  ss = group_sum<4>(ss);
   if (ksplit > 1) {
     float* pp = L.part + (size_t)blockIdx.z * L.M * L.N;
 #pragma unroll
@@ -365,7 +364,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   for (int r = 0; r < 16; ++r) {
     const int m = m0 + wm * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
     const float val = norm ? acc[r] * rs[m - m0] : acc[r];
-    const float partner = __shfl_down(val, 1);  // column n + 1, same row
+    const float partner = xor_lane<1>(val);  // column n + 1, same row (used by even columns)
     if (m >= L.M) continue;
     if (!pair) epi_single(L.epi, m, n, val);
     else if ((j & 1) == 0) epi_pair(L.epi, m, n, val, partner);
@@ -461,8 +460,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Attn a, int chunk, int
       float dot = 0.f;
 #pragma unroll
       for (int v = 0; v < VEC; ++v) dot += q[v] * f[v];
-#pragma unroll
-      for (int off = 1; off < G; off <<= 1) dot += __shfl_xor(dot, off);
+      dot = group_sum<G>(dot);
       const int j = j0 + r * KPR + g;
       bool vis = j < hi;
       if (vis && gt != nullptr) {
@@ -472,8 +470,7 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Attn a, int chunk, int
       sc[r] = vis ? dot : -INFINITY;
       mx = fmaxf(mx, sc[r]);
     }
-#pragma unroll
-    for (int off = G; off < 64; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    mx = across_max<G>(mx);
     if (mx == -INFINITY) continue;  // wave-uniform: nothing visible in this step
     const float m_new = fmaxf(m_run, mx);
     const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
@@ -493,12 +490,9 @@ __global__ __launch_bounds__(256) void attn_decode_kernel(Attn a, int chunk, int
     m_run = m_new;
   }
   // sum over the lanes that share a dimension chunk (different keys, same m_run)
+  l_run = across_sum<G>(l_run);
 #pragma unroll
-  for (int off = G; off < 64; off <<= 1) {
-    l_run += __shfl_xor(l_run, off);
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) o[v] += __shfl_xor(o[v], off);
-  }
+  for (int v = 0; v < VEC; ++v) o[v] = across_sum<G>(o[v]);
   if (lane < G) {
 #pragma unroll
     for (int v = 0; v < VEC; ++v) wo[wave][c * VEC + v] = o[v];
@@ -606,8 +600,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
       sc[cc] = sv;
       mx = fmaxf(mx, sv);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 1));
-    mx = fmaxf(mx, __shfl_xor(mx, 2));
+    mx = group_max<4>(mx);
     const float m_new = fmaxf(m_run, mx);
     const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
     float ls = 0.f;
@@ -617,8 +610,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
       Ps[r][cq * 16 + cc] = p;
       ls += p;
     }
-    ls += __shfl_xor(ls, 1);
-    ls += __shfl_xor(ls, 2);
+    ls = group_sum<4>(ls);
     if (m_new != -INFINITY) {
       l_run = l_run * alpha + ls;
       m_run = m_new;
@@ -707,12 +699,18 @@ __device__ __forceinline__ float row_top1(const float* row, int lane, int* idx_o
     const float v = row[lane + 64 * j];
     if (v > best) { best = v; bi = lane + 64 * j; }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const float ov = __shfl_xor(best, o);
-    const int oi = __shfl_xor(bi, o);
+  auto step = [&](auto oc) {
+    constexpr int o = decltype(oc)::value;
+    const float ov = xor_lane<o>(best);
+    const int oi = __builtin_bit_cast(int, xor_lane<o>(__builtin_bit_cast(float, bi)));
     if (ov > best || (ov == best && oi < bi)) { best = ov; bi = oi; }
-  }
+  };
+  step(std::integral_constant<int, 32>());
+  step(std::integral_constant<int, 16>());
+  step(std::integral_constant<int, 8>());
+  step(std::integral_constant<int, 4>());
+  step(std::integral_constant<int, 2>());
+  step(std::integral_constant<int, 1>());
   float s = 0.f;
 #pragma unroll
   for (int j = 0; j < 4; ++j) s += expf(row[lane + 64 * j] - best);

@@ -1584,6 +1584,7 @@ extern "C" int mbp_reset(mbp_handle* h) {
   h->batch = 0;
   h->pending = false;
   h->last_n = 0;
+  h->n_hint = std::min(3, h->cfg.max_n);  // as at creation, so a reset handle acts like a new one
   h->poisoned = false;
   h->err.clear();
   h->trecs.clear();
