@@ -673,8 +673,9 @@ __device__ __forceinline__ AttnRow attn_row(const ECall& c, int i) {
 // first step's keys and values at once (a wave's memory counter drains in order, so
 // a wave holding cache requests would see the query only after them).  Wave w >= 1
 // takes steps of KW keys from lo + KW*(w-1); G lanes share a key row (VEC elements
-// each), so one load round covers 64/G keys and a step is eight rounds.  The split
-// over this pass's keys (read from kvn) uses all waves.  The waves' (max, sum,
+// each), so one load round covers 64/G keys and a step is eight rounds.  On the
+// split over this pass's keys (read from kvn), waves 1..EW-1 take one load round
+// each.  The waves' (max, sum,
 // numerator) are combined in LDS and the block writes one partial.  r0: the rows of
 // the block's first item (it = blockIdx.x), loaded once per launch.
 template <typename KV, int DH, class Late = NoHook>
@@ -708,34 +709,41 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
     const size_t boff = (size_t)b * a.b_stride + (size_t)h * a.cap * DH + cq * VEC;
     const KV* kb = reinterpret_cast<const KV*>(a.kc) + boff;
     const KV* vb = reinterpret_cast<const KV*>(a.vc) + boff;
-    uint4 kr[NR], vr[NR];
-    int j0 = fresh || wave == 0 ? hi : lo + (wave - 1) * KW;  // wave 0: no cached keys
-    if (wave == 0) {
-      const uint64_t* qp = a.q.ll + (size_t)i * a.q.ld + h * DH + min(lane, DH - 1);
-      uint64_t qraw[1] = {ll_load(qp)};
-      ll_settle<1>(qraw, [&](int) { return qp; }, lane < DH ? 1u : 0u, base + a.q.tag, err);
-      if (lane < DH) qs[lane] = __uint_as_float((uint32_t)qraw[0]) * a.scale;
-    } else if (j0 < hi) {
-#pragma unroll
-      for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
-#pragma unroll
-      for (int r = 0; r < NR; ++r) vr[r] = ld16(vb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
-    }
-    lds_barrier();
     float q[VEC];
-#pragma unroll
-    for (int v = 0; v < VEC; ++v) q[v] = qs[cq * VEC + v];
-    if (!hooked) {  // the query has arrived: the next operation's requests go out now
-      late();
-      hooked = true;
-    }
-
     float m_run = -INFINITY, l_run = 0.f;
     float o[VEC];
 #pragma unroll
     for (int v = 0; v < VEC; ++v) o[v] = 0.f;
-
+    // wave 0 polls the query into LDS; after the barrier every wave takes it
+    auto poll_q = [&] {
+      const uint64_t* qp = a.q.ll + (size_t)i * a.q.ld + h * DH + min(lane, DH - 1);
+      uint64_t qraw[1] = {ll_load(qp)};
+      ll_settle<1>(qraw, [&](int) { return qp; }, lane < DH ? 1u : 0u, base + a.q.tag, err);
+      if (lane < DH) qs[lane] = __uint_as_float((uint32_t)qraw[0]) * a.scale;
+    };
+    auto take_q = [&] {
+#pragma unroll
+      for (int v = 0; v < VEC; ++v) q[v] = qs[cq * VEC + v];
+      if (!hooked) {  // the query has arrived: the next operation's requests go out now
+        late();
+        hooked = true;
+      }
+    };
+    // The two kinds of split run in separate branches (fresh is the same for the whole
+    // block), each with its own barrier, so their prefetched registers do not overlap.
     if (!fresh) {
+      uint4 kr[NR], vr[NR];
+      int j0 = wave == 0 ? hi : lo + (wave - 1) * KW;  // wave 0: no cached keys
+      if (wave == 0) {
+        poll_q();
+      } else if (j0 < hi) {
+#pragma unroll
+        for (int r = 0; r < NR; ++r) kr[r] = ld16(kb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
+#pragma unroll
+        for (int r = 0; r < NR; ++r) vr[r] = ld16(vb + (size_t)min(j0 + r * KPR + g, hi - 1) * DH);
+      }
+      lds_barrier();
+      take_q();
       for (; j0 < hi; j0 += (EW - 1) * KW) {
         if (j0 != lo + (wave - 1) * KW) {
 #pragma unroll
@@ -782,63 +790,50 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
         m_run = m_new;
       }
     } else {
-      // keys of this pass: slot j is row f + (j - ns) of kvn (float32, tagged); each
-      // round requests its key and value entries together before waiting.  A pass
-      // has at most kEngineMaxRows keys, so NRF rounds cover them.
-      constexpr int NRF = (kEngineMaxRows + KPR - 1) / KPR;
-      for (int j0 = lo + wave * NRF * KPR; j0 < hi; j0 += EW * NRF * KPR) {
-        float sc[NRF];
-        float mx = -INFINITY;
-        float vrow[NRF][VEC];
+      // keys of this pass: slot j is row f + (j - ns) of kvn (float32, tagged).  Wave
+      // w >= 1 takes key jf of one load round (KPR keys per wave), so the keys of a
+      // multi-row pass are polled by several waves at once.  (Requesting them before
+      // the query barrier holds their entries in registers across it, which spills.)
+      static_assert((EW - 1) * KPR >= kEngineMaxRows, "one round per wave covers a pass's keys");
+      const int jf = lo + (wave - 1) * KPR + g;
+      const bool fin = wave >= 1 && jf < hi && f + jf - ns < c.M;
+      if (wave == 0) poll_q();
+      lds_barrier();
+      take_q();
+      if (wave >= 1 && lo + (wave - 1) * KPR < hi) {  // wave-uniform: the wave has keys
+        float dot = 0.f;
+        float vrow[VEC];
+        if (fin) {
+          const uint64_t* kp = a.kvn + (size_t)(f + jf - ns) * a.kvn_ld + h * DH + cq * VEC;
+          auto ep = [&](int v) { return kp + (v < VEC ? v : a.d + v - VEC); };
+          uint64_t fe[2 * VEC];
 #pragma unroll
-        for (int r = 0; r < NRF; ++r) {
-          const int j = j0 + r * KPR + g;
-          const bool in = j < hi && f + j - ns < c.M;  // pass rows only
-          float dot = 0.f;
-          if (in) {
-            const uint64_t* kp = a.kvn + (size_t)(f + j - ns) * a.kvn_ld + h * DH + cq * VEC;
-            float kf[2 * VEC];
-            uint64_t e[2 * VEC];
-            auto ep = [&](int v) { return kp + (v < VEC ? v : a.d + v - VEC); };
+          for (int v = 0; v < 2 * VEC; ++v) fe[v] = ll_load(ep(v));
+          ll_settle<2 * VEC>(fe, ep, (1u << (2 * VEC)) - 1u, ktag, err);
 #pragma unroll
-            for (int v = 0; v < 2 * VEC; ++v) e[v] = ll_load(ep(v));
-            ll_settle<2 * VEC>(e, ep, (1u << (2 * VEC)) - 1u, ktag, err);
-#pragma unroll
-            for (int v = 0; v < 2 * VEC; ++v) kf[v] = __uint_as_float((uint32_t)e[v]);
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) {
-              dot += q[v] * kf[v];
-              vrow[r][v] = kf[VEC + v];
-            }
-          } else {
-#pragma unroll
-            for (int v = 0; v < VEC; ++v) vrow[r][v] = 0.f;
+          for (int v = 0; v < VEC; ++v) {
+            dot += q[v] * __uint_as_float((uint32_t)fe[v]);
+            vrow[v] = __uint_as_float((uint32_t)fe[VEC + v]);
           }
-          dot = group_sum<G>(dot);
-          bool vis = in;
-          if (vis && gt != nullptr) {
-            const int gj = gld(gt + j);
-            vis = (gj == gq) || (gj == gq - 1);
-          }
-          sc[r] = vis ? dot : -INFINITY;
-          mx = fmaxf(mx, sc[r]);
+        } else {
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) vrow[v] = 0.f;
         }
-        mx = across_max<G>(mx);
-        if (mx == -INFINITY) continue;
-        const float m_new = fmaxf(m_run, mx);
-        const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
-#pragma unroll
-        for (int v = 0; v < VEC; ++v) o[v] *= alpha;
-        float ps = 0.f;
-#pragma unroll
-        for (int r = 0; r < NRF; ++r) {
-          const float p = (sc[r] == -INFINITY) ? 0.f : expf(sc[r] - m_new);
-          ps += p;
-#pragma unroll
-          for (int v = 0; v < VEC; ++v) o[v] += p * vrow[r][v];
+        dot = group_sum<G>(dot);
+        bool vis = fin;
+        if (vis && gt != nullptr) {
+          const int gj = gld(gt + jf);
+          vis = (gj == gq) || (gj == gq - 1);
         }
-        l_run = l_run * alpha + ps;
-        m_run = m_new;
+        const float sc = vis ? dot : -INFINITY;
+        const float mx = across_max<G>(sc);
+        if (mx != -INFINITY) {  // wave-uniform
+          const float p = vis ? expf(sc - mx) : 0.f;
+#pragma unroll
+          for (int v = 0; v < VEC; ++v) o[v] = p * vrow[v];
+          l_run = p;
+          m_run = mx;
+        }
       }
     }
     // sum over the lanes that share a dimension chunk (different keys, same m_run)
