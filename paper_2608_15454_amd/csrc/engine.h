@@ -81,6 +81,7 @@ struct ECall {
   const int32_t* grp_tab;  // [B, cap] group ids of cache slots (LCA mask) or nullptr
   int32_t S;               // attention splits per (row, head), the last one for pass rows
   int32_t chunk;           // cached keys per split (a multiple of 64)
+  uint32_t zero;           // 0; the kernel cannot fold it away (see touch_lines in engine.hip)
 };
 
 // Split-KV attention of the pass rows.  Split s < S-1 covers cached slots

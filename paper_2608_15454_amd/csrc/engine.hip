@@ -299,6 +299,18 @@ __device__ __forceinline__ float row_scale(const float* ssw, int m, int K, float
   for (int w = 0; w < EW; ++w) ss += ssw[m * EW + w];
   return 1.0f / sqrtf(ss / (float)K + eps);
 }
+// One dword of every 64-byte line of an operation's descriptor fields, XOR-ed: bytes
+// [8, 200) of the EOp for a linear operation, [200, 296) for attention.  Reading them
+// early brings the lines into the scalar cache, so the fields read later (the
+// epilogue's, or the next operation's) do not each wait for a miss where they are
+// used.  The caller folds the result into a poll tag masked with ECall::zero (0 at
+// run time, opaque to the compiler): the loads are then needed only when the first
+// polled value is compared, so their misses overlap the poll's round trip.
+__device__ __forceinline__ uint32_t touch_lines(const CONST_AS EOp* op, bool attn = false) {
+  const CONST_AS uint32_t* w = (const CONST_AS uint32_t*)op;
+  return attn ? (w[50] ^ w[73]) : (w[2] ^ w[18] ^ w[34] ^ w[49]);
+}
+
 // ------------------------------------------------------------------ linear ----
 // A block computes tiles of RB = (EW / NS) * R consecutive output rows.  The waves of
 // a block form EW / NS row groups of NS waves; wave (group g, slice s) holds rows
@@ -520,10 +532,12 @@ struct QkvItem {
 // QKV epilogue operands (EPI_QKV).  next: runs once, after this operation's output
 // stores are issued (it requests a later operation's weights, which are then in
 // flight during the next input poll).
+// tz: touch_lines of descriptors to fetch during the input poll, masked with
+// ECall::zero (0 at run time).
 template <typename W, int KC, int NS, int R, int MR, bool NORM, class Next = NoHook>
 __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint32_t base, uint32_t tag, int* err,
                                           float* lds, const WPre<W, KC, NS, R, NORM>& pre, const QkvItem* qi,
-                                          Next&& next = Next()) {
+                                          uint32_t tz, Next&& next = Next()) {
   constexpr int KCW = KC / NS, GD = NORM ? KCW : 1;
   constexpr int RB = (EW / NS) * R;
   static_assert(KC % NS == 0 && EW % NS == 0 && NS * RB * 16 <= kPartFloats, "linear tiling");
@@ -579,7 +593,7 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
         if (NORM)
           for (int i = threadIdx.x; i < kSsFloats; i += EB) ssw[i] = 0.f;
         lds_barrier();
-        stage_rows(L.x, c, m0, mc, L.K, x, base, err, NORM ? ssw : nullptr);
+        stage_rows(L.x, c, m0, mc, L.K, x, base + tz, err, NORM ? ssw : nullptr);
         lds_barrier();
       }
       // first use of the weights here, after the input poll: without this anchor the
@@ -1006,7 +1020,8 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
     const int o = 6 * l;
     if (l > 0) weights_ahead(lin(o), pq);
     op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>(), true>(
-        lin(o), c, base, base + cops[o].tag, err, lds, pq, &qi);
+        lin(o), c, base, base + cops[o].tag, err, lds, pq, &qi,
+        (touch_lines(cops + o) ^ touch_lines(cops + o + 1, true)) & c.zero);
     lds_barrier();
     op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, ar);
     weights_ahead(lin(o + 3), po);
@@ -1017,17 +1032,20 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
     lds_barrier();
     op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err);
     op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>(), false>(
-        lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr, [&] {
+        lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr,
+        (touch_lines(cops + o + 3) ^ touch_lines(cops + o + 4)) & c.zero, [&] {
           if constexpr (!kAhead) weights_ahead(lin(o + 4), pg);
         });
     lds_barrier();
     op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>(), true>(
-        lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr, [&] {
+        lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr,
+        (touch_lines(cops + o + 4) ^ touch_lines(cops + o + 5)) & c.zero, [&] {
           if constexpr (!kAhead) weights_ahead(lin(o + 5), pd);
         });
     lds_barrier();
     op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>(), false>(
-        lin(o + 5), c, base, base + cops[o + 5].tag, err, lds, pd, nullptr);
+        lin(o + 5), c, base, base + cops[o + 5].tag, err, lds, pd, nullptr,
+        (touch_lines(cops + o + 5) ^ touch_lines(cops + (l + 1 < nlayers ? o + 6 : o + 5))) & c.zero);
     lds_barrier();
   }
 }

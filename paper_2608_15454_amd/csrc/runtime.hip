@@ -565,6 +565,7 @@ int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, co
   c.grp_tab = grp_tab;
   c.S = S;
   c.chunk = chunk;
+  c.zero = 0;
   if (h->tag_base > 0xF0000000u) {  // restart the tags before they wrap: clear the tagged buffers
     HIPCK(h, hipMemsetAsync(h->R<uint64_t>(h->rg.ll), 0, (size_t)h->sz.ll_entries * 8, st));
     h->tag_base = 1;
