@@ -30,6 +30,8 @@ from .model import (  # noqa: F401
     step,
     verify_drafts,
     verify_step,
+    verify_external,
+    generate_external,
     generate,
     greedy_generate,
 )

@@ -324,6 +324,43 @@ def verify_step(W, cfg, x, n):
     return {"logits": s["logits"], "cand": s["cand"], "prob": s["prob"], "k": j, "gamma": gammas}
 
 
+def verify_external(W, cfg, x, drafts):
+    """External verification (Section 6, "Improving Baseline Throughput with MBP
+    Models"): a separate next-byte model (the FxT baseline: encoder, LM module and
+    next-byte decoder, no MB head) checks another model's drafts c_1..c_n with greedy
+    speculative decoding.  g_m is the verifier's greedy byte after x ++ c_1..c_m
+    (m = 0..n); the drafts are kept while c_{m+1} == g_m, and the verifier's greedy
+    byte after the kept prefix is appended.  Returns k = j + 1 accepted bytes
+    (j = 0..n kept drafts), the bytes, and the greedy bytes seen."""
+    x = [int(b) for b in x]
+    drafts = [int(c) for c in drafts]
+    greedy = []
+    j = 0
+    while True:
+        g = _greedy_byte(W, cfg, x + drafts[:j])
+        greedy.append(g)
+        if j == len(drafts) or g != drafts[j]:
+            break
+        j += 1
+    return {"k": j + 1, "bytes": np.array(drafts[:j] + [greedy[j]], dtype=np.uint8), "greedy": greedy}
+
+
+def generate_external(Wd, cfg_d, Wv, cfg_v, prompt, n_new, n):
+    """Bytes emitted when the MBP model (Wd, cfg_d) drafts n candidates per step
+    (next-byte head + MB head) and the verifier (Wv, cfg_v) checks them
+    (verify_external); the last step is truncated."""
+    x = [int(b) for b in prompt]
+    out, steps = [], []
+    while len(out) < n_new:
+        drafts = step(Wd, cfg_d, x, n, tau=2.0)["cand"]
+        r = verify_external(Wv, cfg_v, x, drafts)
+        acc = [int(b) for b in r["bytes"][: n_new - len(out)]]
+        steps.append({"k": r["k"], "drafts": np.asarray(drafts).copy(), "bytes": r["bytes"].copy()})
+        out += acc
+        x += acc
+    return np.array(out, dtype=np.uint8), steps
+
+
 def generate(W, cfg, prompt, n_new, n, tau, mode="threshold"):
     """Run steps until ``n_new`` bytes are emitted; the last step is truncated."""
     x = [int(b) for b in prompt]

@@ -29,6 +29,8 @@ __all__ = [
     "Workload",
     "WORKLOADS",
     "SMALL_F32",
+    "TINY_FXT",
+    "D1024_FXT",
     "manifest",
     "head_manifest_start",
     "make_weights",
@@ -79,7 +81,8 @@ class Workload:
     gen_len: int
     n: int
     tau: float
-    mode: str = "threshold"  # "threshold" | "verify"
+    mode: str = "threshold"  # "threshold" | "verify" | "external"
+    verifier: "ModelConfig" = None  # mode "external": the next-byte model checking the drafts
     sweep_n: tuple = ()
     sweep_tau: tuple = ()
     note: str = ""
@@ -92,6 +95,11 @@ _D2048 = ModelConfig(d_model=2048, n_heads=32, n_enc=2, n_lm=16, n_nb=2, n_mb=2,
 # float32 model at the smallest width the persistent engine's register tiles take
 # (d_model 256, head size 64): parity of that path at the float32 tolerance
 SMALL_F32 = ModelConfig(d_model=256, n_heads=4, n_enc=2, n_lm=2, n_nb=2, n_mb=2, head="lca", dtype="f32")
+# next-byte models without an MB head (the FxT baseline the paper verifies MBP drafts
+# with: encoder, LM module, next-byte decoder) -- a tiny float32 one and the
+# parameter-matched d=1024 one with the 2/16/4 layer split
+TINY_FXT = ModelConfig(d_model=128, n_heads=4, n_enc=1, n_lm=2, n_nb=2, n_mb=0, head="lca", dtype="f32")
+D1024_FXT = ModelConfig(d_model=1024, n_heads=16, n_enc=2, n_lm=16, n_nb=4, n_mb=0, head="lca", dtype="bf16")
 
 WORKLOADS = {
     "tiny_f32": Workload("tiny_f32", _TINY, batch=1, prompt_len=256, gen_len=128, n=3, tau=0.75),
@@ -102,6 +110,9 @@ WORKLOADS = {
                               tau=0.75, sweep_tau=(0.5, 0.75, 0.9)),
     "verify_d2048_b16": Workload("verify_d2048_b16", _D2048, batch=16, prompt_len=8192, gen_len=512, n=7,
                                  tau=0.75, mode="verify"),
+    # the MBP d=1024 model drafts n = 7 candidates, the FxT d=1024 model verifies them
+    "extverify_d1024_b1": Workload("extverify_d1024_b1", _D1024_LCA, batch=1, prompt_len=4096, gen_len=1024, n=7,
+                                   tau=0.75, mode="external", verifier=D1024_FXT),
 }
 
 _BLOCK_PARTS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")

@@ -441,3 +441,49 @@ def test_verify_generation_equals_greedy(gain, n):
     out, steps = oracle.generate(W, TINY, p, 14, n, 0.0, mode="verify")
     np.testing.assert_array_equal(out, g)
     assert all(1 <= s["k"] <= n for s in steps)
+
+
+# ---------------------------------------------------- external verification --
+# A separate next-byte model (no MB head) checks another model's drafts; kept drafts
+# plus the verifier's greedy byte after them (Section 6, external verification).
+
+TINY_FXT = synth.TINY_FXT
+
+
+def test_external_verify_perfect_and_wrong_drafts():
+    Wv = synth.make_weights(TINY_FXT, seed=27, gain_jitter=0.2)
+    x = synth.make_prompt(2, 40)
+    g = oracle.greedy_generate(Wv, TINY_FXT, x, 7)
+    r = oracle.verify_external(Wv, TINY_FXT, x, g[:6])
+    assert r["k"] == 7
+    np.testing.assert_array_equal(r["bytes"], g)  # 6 kept drafts + the 7th greedy byte
+    for m in range(6):
+        bad = g[:6].copy()
+        bad[m] = (int(bad[m]) + 1) % 256
+        r = oracle.verify_external(Wv, TINY_FXT, x, bad)
+        assert r["k"] == m + 1
+        np.testing.assert_array_equal(r["bytes"], g[: m + 1])  # the bonus byte replaces the bad draft
+
+
+def test_external_verify_by_the_drafting_model_is_self_verify_plus_one_byte():
+    W = synth.make_weights(TINY, seed=28, logit_gain=30.0)
+    x = list(synth.make_prompt(4, 40))
+    for n in (2, 4, 6):
+        s = oracle.verify_step(W, TINY, x, n)
+        r = oracle.verify_external(W, TINY, x, s["cand"])
+        acc = [int(c) for c in s["cand"][: s["k"]]]
+        assert r["k"] == s["k"] + 1
+        assert [int(b) for b in r["bytes"][:-1]] == acc
+        assert int(r["bytes"][-1]) == int(oracle.greedy_generate(W, TINY, x + acc, 1)[0])
+
+
+@pytest.mark.parametrize("same,gain,n", [(False, 1.0, 3), (False, 30.0, 5), (True, 30.0, 4)])
+def test_external_generation_equals_verifier_greedy(same, gain, n):
+    Wd = synth.make_weights(TINY, seed=29, logit_gain=gain)
+    cfg_v, Wv = (TINY, Wd) if same else (TINY_FXT, synth.make_weights(TINY_FXT, seed=30, logit_gain=gain))
+    p = synth.make_prompt(5, 40)
+    out, steps = oracle.generate_external(Wd, TINY, Wv, cfg_v, p, 14, n)
+    np.testing.assert_array_equal(out, oracle.greedy_generate(Wv, cfg_v, p, 14))
+    assert all(1 <= s["k"] <= n + 1 for s in steps)
+    if same:  # the verifier's own drafts: its first draft is always its greedy byte
+        assert all(s["k"] >= 2 for s in steps[:-1])
