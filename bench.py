@@ -96,6 +96,17 @@ def run_steps(dec, steps, n, tau, mode):
         dec.accept()
 
 
+def run_external(dec, ver, steps, n, threshold):
+    """External verification: dec drafts n candidates, ver keeps the verified prefix and
+    adds its greedy byte; both commit the accepted bytes."""
+    for _ in range(steps):
+        cand, _, _ = dec.decode_step(n, 1.0, threshold)
+        ver.verify_draft(cand)
+        acc, lens = ver.last_accepted()
+        dec.accept([acc[b, : lens[b]] for b in range(len(lens))])
+        ver.accept()
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -115,38 +126,54 @@ def main():
     n = args.n or wl.n
     tau = wl.tau if args.tau is None else args.tau
     mode = SELF_VERIFY if wl.mode == "verify" else THRESHOLD
+    ext = wl.mode == "external"
     B, K, W = wl.batch, args.steps, args.warmup
     log(f"[bench] workload {wl.name} B={B} prompt={wl.prompt_len} n={n} tau={tau} steps={K} warmup={W}")
 
     t0 = time.time()
     weights = synth.make_weights(model, seed=0, logit_gain=args.logit_gain)
     prompts = [synth.make_prompt(r, wl.prompt_len) for r in range(B)]
-    max_ctx = wl.prompt_len + (max(K, W) + 2) * n + 16
-    dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max(n, 8), engine=not args.no_engine), weights)
+    max_ctx = wl.prompt_len + (max(K, W) + 2) * (n + 1) + 16
+    max_n = max(n + 1 if ext else n, 8)
+    dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max_n, engine=not args.no_engine), weights)
+    ver, vweights = None, None
+    if ext:
+        vweights = synth.make_weights(wl.verifier, seed=1, logit_gain=args.logit_gain)
+        ver = Decoder(make_config(wl.verifier, max_batch=B, max_ctx=max_ctx, max_n=max_n, engine=not args.no_engine),
+                      vweights)
+    decs = [dec] + ([ver] if ext else [])
     log(f"[bench] weights + init {time.time() - t0:.1f}s")
 
+    def run(steps):
+        if ext:
+            run_external(dec, ver, steps, n, THRESHOLD)
+        else:
+            run_steps(dec, steps, n, tau, mode)
+
     t0 = time.time()
-    dec.prefill(prompts)
+    for d in decs:
+        d.prefill(prompts)
     torch.cuda.synchronize()
     log(f"[bench] prefill {time.time() - t0:.2f}s")
-    run_steps(dec, W, n, tau, mode)
+    run(W)
     torch.cuda.synchronize()
     log("[bench] warm-up done")
 
     # ---- timed pass
-    dec.reset()
-    dec.prefill(prompts)
+    for d in decs:
+        d.reset()
+        d.prefill(prompts)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     ev0.record(stream)
     w0 = time.perf_counter()
-    run_steps(dec, K, n, tau, mode)
+    run(K)
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - w0
     gpu_ms = ev0.elapsed_time(ev1)
-    lens = [dec.row_length(b) for b in range(B)]
+    lens = [(ver if ext else dec).row_length(b) for b in range(B)]
     accepted = sum(L - wl.prompt_len for L in lens)
     elapsed = max(wall, gpu_ms / 1000.0)
     value = accepted / elapsed
@@ -155,21 +182,26 @@ def main():
     # ---- kernel timing pass (identical steps, launches bracketed by HIP events)
     roofline, classes, timing_step_ms = None, {}, None
     if not args.no_timing_pass:
-        dec.reset()
-        dec.prefill(prompts)
-        dec.set_timing(True)
+        for d in decs:
+            d.reset()
+            d.prefill(prompts)
+            d.set_timing(True)
         cal_src = torch.empty(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
         cal_dst = torch.empty_like(cal_src)
         torch.cuda.synchronize()
         cal_dst.copy_(cal_src)
         torch.cuda.synchronize()
         w1 = time.perf_counter()
-        run_steps(dec, K, n, tau, mode)
+        run(K)
         torch.cuda.synchronize()
         timing_step_ms = (time.perf_counter() - w1) * 1000.0 / K
         del cal_src, cal_dst
-        classes = dec.read_timing()
-        dec.set_timing(False)
+        classes = {}
+        for d in decs:  # both handles' launches (external verification)
+            for k, v in d.read_timing().items():
+                c = classes.get(k, (0, 0.0, 0.0))
+                classes[k] = (c[0] + v[0], c[1] + v[1], c[2] + v[2])
+            d.set_timing(False)
         dom = max(classes, key=lambda c: classes[c][1])
         launches, ms, nbytes = classes[dom]
         achieved = nbytes / (ms / 1000.0) / 1e9 if ms > 0 else 0.0
@@ -192,15 +224,20 @@ def main():
         x = [int(b) for b in prompts[0]]
         got = 0
         c0 = time.perf_counter()
-        for _ in range(args.cpu_steps):
-            r = oracle.step(W64, model, x, n, tau) if mode == THRESHOLD else oracle.verify_step(W64, model, x, n)
-            acc = [int(c) for c in r["cand"][: r["k"]]]
+        V64 = oracle.to_float64(vweights) if ext else None
+        for _ in range(args.cpu_steps if not ext else min(args.cpu_steps, 1)):
+            if ext:
+                r = oracle.verify_external(V64, wl.verifier, x, oracle.step(W64, model, x, n, tau)["cand"])
+                acc = [int(c) for c in r["bytes"]]
+            else:
+                r = oracle.step(W64, model, x, n, tau) if mode == THRESHOLD else oracle.verify_step(W64, model, x, n)
+                acc = [int(c) for c in r["cand"][: r["k"]]]
             x += acc
             got += len(acc)
         cs = time.perf_counter() - c0
         cpu = {"value": round(got / cs, 4), "unit": "accepted bytes/s", "cores": cpu_threads(), "kind": "oracle",
-               "sample": f"{args.cpu_steps} steps of batch row 0 of the same workload (float64 full recompute, "
-                         f"{cs:.1f}s)"}
+               "sample": f"{1 if ext else args.cpu_steps} steps of batch row 0 of the same workload (float64 full "
+                         f"recompute, {cs:.1f}s)"}
         log(f"[bench] cpu oracle {got} bytes in {cs:.1f}s")
 
     step_bytes = sum(v[2] for v in classes.values()) / K if classes else None
@@ -220,7 +257,9 @@ def main():
         "config": {
             "workload": f"{wl.name}: d={model.d_model} heads={model.n_heads} layers enc/lm/nt/mb="
                         f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb} head={model.head}, "
-                        f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
+                        + (f"verified by a next-byte model with layers enc/lm/nt={wl.verifier.n_enc}/"
+                           f"{wl.verifier.n_lm}/{wl.verifier.n_nb}, " if ext else "")
+                        + f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
             "batch": B, "prompt_len": wl.prompt_len, "n": n, "tau": tau, "mode": wl.mode,
             "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32",
             "logit_gain": args.logit_gain, "max_patch": model.max_patch,

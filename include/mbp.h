@@ -156,6 +156,27 @@ int mbp_prefill(mbp_handle *h, const uint8_t *h_bytes, const int32_t *h_lens, in
 int mbp_decode_step(mbp_handle *h, int32_t n, float tau, int32_t mode, uint8_t *d_cand,
                     float *d_prob, int32_t *d_accept_len);
 
+/* External verification (Section 6, "Improving Baseline Throughput with MBP Models"):
+ * this handle's model -- typically one without an MB head (n_mb = 0: encoder, LM
+ * module and next-byte decoder, the FxT baseline) -- checks n drafts made by another
+ * model, with greedy speculative decoding as in self-verification.  The drafts are
+ * committed tentatively (after a pending bonus byte of the previous call); g_m is this
+ * model's greedy byte after the first m drafts (m = 0..n); drafts are kept while
+ * draft[m] == g_m, and g_j after the j kept drafts is appended.  The caches are rolled
+ * back to the kept drafts; g_j is the row's pending bonus byte, committed at the start
+ * of the next verification (or before a decode step).  Free-running, the accepted
+ * bytes are exactly this model's greedy decoding.  Synchronizes.
+ *   d_draft       device uint8 [batch, n], complete on this handle's stream.
+ *   n             1..max_n-1.
+ *   d_out         device uint8 [batch, n+1]: row r's accepted bytes are
+ *                 d_out[r, 0 : d_accept_len[r]].
+ *   d_accept_len  device int32 [batch]: j + 1, 1..n+1.
+ * mbp_accept(h, NULL, NULL) then closes the step (the kept drafts are committed, the
+ * bonus stays pending); an override rolls the step back first.  mbp_last_accepted and
+ * mbp_get_logits report the n+1 accepted-byte slots and the verifier's n+1 logit rows.
+ * MBP_ECAPACITY if the drafts would exceed max_ctx or max_latents. */
+int mbp_verify_draft(mbp_handle *h, const uint8_t *d_draft, int32_t n, uint8_t *d_out, int32_t *d_accept_len);
+
 /* Copy the last step's accepted bytes to the host (synchronizes the stream).
  *   h_bytes  host [batch, max_n]: row r's bytes at h_bytes[r*max_n ...].
  *   h_lens   host [batch]: accepted counts. */

@@ -75,6 +75,8 @@ def lib():
     L.mbp_prefill.restype = ctypes.c_int
     L.mbp_decode_step.argtypes = [P, ctypes.c_int32, ctypes.c_float, ctypes.c_int32, P, P, P]
     L.mbp_decode_step.restype = ctypes.c_int
+    L.mbp_verify_draft.argtypes = [P, P, ctypes.c_int32, P, P]
+    L.mbp_verify_draft.restype = ctypes.c_int
     L.mbp_last_accepted.argtypes = [P, P, P]
     L.mbp_last_accepted.restype = ctypes.c_int
     L.mbp_accept.argtypes = [P, P, P]
@@ -177,6 +179,7 @@ class Decoder:
         self.cand = torch.zeros((B, nmax), dtype=torch.uint8, device=self.device)
         self.prob = torch.zeros((B, nmax), dtype=torch.float32, device=self.device)
         self.accept_len = torch.zeros((B,), dtype=torch.int32, device=self.device)
+        self.vout = torch.zeros((B, nmax), dtype=torch.uint8, device=self.device)
         self.logits_buf = torch.zeros((B, nmax, 256), dtype=torch.float32, device=self.device)
         self.batch = 0
         self.n = 0
@@ -214,6 +217,19 @@ class Decoder:
                                            ctypes.c_void_p(self.accept_len.data_ptr())))
         self.n = n
         return cand.view(B, n), prob.view(B, n), self.accept_len[:B]
+
+    def verify_draft(self, draft):
+        """External verification of another model's drafts (device uint8 [B, n], on this
+        decoder's stream); returns device views (accepted bytes [B, n+1], accept_len [B])."""
+        B = self.batch
+        draft = draft.contiguous()
+        n = int(draft.shape[1])
+        out = self.vout.view(-1)[: B * (n + 1)]
+        self._check(self.L.mbp_verify_draft(self.h, ctypes.c_void_p(draft.data_ptr()), n,
+                                            ctypes.c_void_p(out.data_ptr()),
+                                            ctypes.c_void_p(self.accept_len.data_ptr())))
+        self.n = n + 1
+        return out.view(B, n + 1), self.accept_len[:B]
 
     def last_accepted(self):
         B, nmax = self.batch, self.cfg.max_n

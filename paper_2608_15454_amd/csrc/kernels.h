@@ -131,6 +131,14 @@ hipError_t launch_accept(const float* logits, int B, int n, float tau, const int
 // Greedy verification: NT logits of the n tentative rows vs the drafts.
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
                          int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev = Ev());
+// External verification of n drafts per batch row (n + 1 <= kMaxVerifyRows): logits
+// [B, n+1, 256] are the verifier's next-byte logits after 0..n drafts; out [B, n+1]
+// gets the kept drafts and the verifier's greedy byte after them, accept_len their
+// count (kept + 1).
+constexpr int kMaxVerifyRows = 16;
+hipError_t launch_verify_ext(const float* logits, const uint8_t* draft, int B, int n, const int32_t* active,
+                             uint8_t* out, int32_t* accept_len, const int32_t* fault, hipStream_t st,
+                             const Ev& ev = Ev());
 hipError_t launch_to_f32(const void* src, int wdt, float* dst, int64_t n, hipStream_t st);
 hipError_t launch_rope_table(float2* tab, int npos, int dh, double base, hipStream_t st);
 hipError_t launch_fill_i32(int32_t* p, int32_t v, int64_t n, hipStream_t st);

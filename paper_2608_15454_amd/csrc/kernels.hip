@@ -768,6 +768,30 @@ __global__ void verify_kernel(const float* nt_logits, const uint8_t* cand, int n
   }
 }
 
+// External verification, one block per batch row b: logits row b*(n+1) + m holds the
+// verifier's next-byte logits after the first m drafts (m = 0..n).  The drafts are
+// kept while draft[m] equals the greedy byte of row m; out[b] = the kept drafts, then
+// the greedy byte after them; accept_len = kept + 1 (0 for inactive rows, -1 for
+// every row after a failed engine wait).
+__global__ void verify_ext_kernel(const float* logits, const uint8_t* draft, int n, const int32_t* active,
+                                  uint8_t* out, int32_t* accept_len, const int32_t* fault) {
+  __shared__ int gam[kMaxVerifyRows];
+  const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (wave <= n) {
+    int bi;
+    row_top1(logits + ((size_t)b * (n + 1) + wave) * 256, lane, &bi);
+    if (lane == 0) gam[wave] = bi;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int j = 0;
+    while (j < n && gam[j] == (int)draft[(size_t)b * n + j]) ++j;
+    for (int m = 0; m <= n; ++m)
+      out[(size_t)b * (n + 1) + m] = m < j ? draft[(size_t)b * n + m] : (m == j ? (uint8_t)gam[j] : (uint8_t)0);
+    accept_len[b] = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? j + 1 : 0);
+  }
+}
+
 template <typename W>
 __global__ void to_f32_kernel(const W* src, float* dst, int64_t n) {
   const int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x;
@@ -962,6 +986,14 @@ hipError_t launch_accept(const float* logits, int B, int n, float tau, const int
   if (B <= 0) return hipSuccess;
   return klaunch(accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau, active, cand, prob,
                  accept_len, write_len, fault, host_cand, host_len);
+}
+
+hipError_t launch_verify_ext(const float* logits, const uint8_t* draft, int B, int n, const int32_t* active,
+                             uint8_t* out, int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev) {
+  if (B <= 0) return hipSuccess;
+  if (n < 0 || n + 1 > kMaxVerifyRows) return hipErrorInvalidValue;
+  return klaunch(verify_ext_kernel, dim3(B), dim3(64 * (n + 1)), 0, st, ev.start, ev.stop, logits, draft, n, active,
+                 out, accept_len, fault);
 }
 
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,

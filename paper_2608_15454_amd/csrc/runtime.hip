@@ -53,6 +53,9 @@ struct KV {  // one module's KV cache: layer l of row b at k + l*layer_stride + 
   int32_t cap = 0;
 };
 
+// last_mode of a pending step made by mbp_verify_draft
+constexpr int kModeExternal = 2;
+
 struct Row {
   bool active = false;
   std::vector<uint8_t> x;   // committed bytes
@@ -61,6 +64,9 @@ struct Row {
   int64_t epoch = 0;        // bumped whenever the latent list changes
   int64_t win_epoch = -1;   // epoch of the MB window cache
   int32_t win_s = 0, win_valid = 0;
+  // a byte accepted by external verification and not yet committed (-1: none); the
+  // next tentative commit of drafts starts with it
+  int32_t bonus = -1;
 };
 
 struct Sizes {
@@ -356,7 +362,7 @@ struct mbp_handle {
   std::vector<Row> rows;
   int batch = 0;
   bool pending = false;
-  int last_n = 0, last_mode = 0;
+  int last_n = 0, last_mode = 0;  // last_mode: mbp_mode, or kModeExternal
   uint8_t* h_cand = nullptr;  // pinned [B, n] candidates of the last step
   int32_t* h_len = nullptr;   // pinned [B] accepted counts of the last step
   uint8_t* h_cand_dev = nullptr;  // device addresses of the two (written by the accept kernel)
@@ -834,10 +840,10 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
   float* he = h->R<float>(h->rg.he);
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
-  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty() && !h->engine;
+  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && !h->engine;
   // with the engine, the next step's window update runs right after the NT decoder
   // on the same stream, prepared in the commit's plan (and the head rows with it)
-  const bool pre = fork_mb && c.head == MBP_HEAD_LCA && h->n_hint >= 2 && !items.empty() && h->engine;
+  const bool pre = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && h->engine;
   h->pre_draft = false;
   size_t first = 0;
   bool first_chunk = true;
@@ -1387,6 +1393,22 @@ extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t*
   return commit(h, add, true);
 }
 
+// Commits every row's pending bonus byte (external verification), so that the caches
+// hold all accepted bytes before a step that does not start with a tentative commit.
+int commit_bonus(mbp_handle* h) {
+  bool any = false;
+  std::vector<std::vector<uint8_t>> add(h->batch);
+  for (int b = 0; b < h->batch; ++b) {
+    Row& r = h->rows[b];
+    if (r.bonus >= 0) {
+      add[b].push_back((uint8_t)r.bonus);
+      r.bonus = -1;
+      any = true;
+    }
+  }
+  return any ? commit(h, add, true) : MBP_OK;
+}
+
 extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, uint8_t* d_cand, float* d_prob,
                                int32_t* d_accept_len) {
   int rc = check_ready(h);
@@ -1397,10 +1419,12 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   if (h->pending) return fail(h, MBP_ESTATE, "the previous step was not accepted");
   if (n < 1 || n > s.nmax) return fail(h, MBP_EINVAL, "n out of range");
   if (c.head == MBP_HEAD_MLP && n - 1 > c.n_mb) return fail(h, MBP_EINVAL, "n - 1 exceeds the MLP heads");
+  if (c.head == MBP_HEAD_LCA && c.n_mb == 0 && n > 1) return fail(h, MBP_EINVAL, "no MB head: n must be 1");
   if (!(tau >= 0.f && tau <= 1.f)) return fail(h, MBP_EINVAL, "tau must be in [0, 1]");
   if (mode != MBP_ACCEPT_THRESHOLD && mode != MBP_ACCEPT_SELF_VERIFY) return fail(h, MBP_EINVAL, "bad mode");
   if (!d_cand || !d_accept_len) return fail(h, MBP_EINVAL, "null output pointer");
   const int B = h->batch;
+  RCK(commit_bonus(h));
   if (c.head == MBP_HEAD_LCA && n >= 2) {
     for (int b = 0; b < B; ++b) {
       const Row& r = h->rows[b];
@@ -1472,6 +1496,98 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   return MBP_OK;
 }
 
+extern "C" int mbp_verify_draft(mbp_handle* h, const uint8_t* d_draft, int32_t n, uint8_t* d_out,
+                                int32_t* d_accept_len) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  if (h->batch == 0) return fail(h, MBP_ESTATE, "no prefill");
+  if (h->pending) return fail(h, MBP_ESTATE, "the previous step was not accepted");
+  if (n < 1 || n + 1 > s.nmax || n + 1 > kMaxVerifyRows) return fail(h, MBP_EINVAL, "n out of range (1..max_n-1)");
+  if (!d_draft || !d_out || !d_accept_len) return fail(h, MBP_EINVAL, "null pointer");
+  const int B = h->batch;
+  HIPCK(h, hipMemcpyAsync(h->h_cand, d_draft, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipStreamSynchronize(h->st));
+  // tentative commit: each row's pending bonus byte, then its n drafts
+  std::vector<std::vector<uint8_t>> add(B);
+  std::vector<int32_t> nb(B, 0), o(B + 1, 0);
+  h->pre_len.assign(B, 0);
+  for (int b = 0; b < B; ++b) {
+    const Row& r = h->rows[b];
+    if (r.bonus >= 0) {
+      add[b].push_back((uint8_t)r.bonus);
+      nb[b] = 1;
+    }
+    add[b].insert(add[b].end(), h->h_cand + (size_t)b * n, h->h_cand + (size_t)(b + 1) * n);
+    h->pre_len[b] = (int32_t)r.x.size() + nb[b];
+    o[b + 1] = o[b] + (int32_t)add[b].size();
+    if ((int64_t)r.x.size() + (int64_t)add[b].size() > s.Tcap) return fail(h, MBP_ECAPACITY, "verify drafts exceed max_ctx");
+    if (simulate_latents(c, r, add[b].data(), (int)add[b].size()) > c.max_latents)
+      return fail(h, MBP_ECAPACITY, "verify drafts exceed max_latents");
+  }
+  float* h1 = h->row_ptr(h->rg.row_h1);
+  float* h1s = h->row_ptr(h->rg.row_h1s);
+  HIPCK(h, hipMemcpyAsync(h1s, h1, (size_t)B * s.d * 4, hipMemcpyDeviceToDevice, h->st));
+  for (int b = 0; b < B; ++b) h->rows[b].bonus = -1;
+  RCK(commit(h, add, false));
+  // the next-byte decoder outputs of the tentative rows are in X in item order; the
+  // prediction after m drafts (m = 0..n) is the output at the byte before draft m+1:
+  // the bonus row or, with no bonus, the saved h1 for m = 0
+  float* X = h->sc_main.X;
+  float* G = h->sc_main.Hid;  // [B*(n+1), d] gathered prediction rows
+  Plan& p = h->plan[1];
+  p.clear();
+  std::vector<int32_t> s1, d1, s2, d2, s3, d3;
+  for (int b = 0; b < B; ++b) {
+    s1.push_back(b);
+    d1.push_back(b * (n + 1));
+    for (int m = 0; m <= n; ++m) {
+      const int src = m == 0 ? (nb[b] ? o[b] : -1) : o[b] + nb[b] + m - 1;
+      s2.push_back(std::max(src, 0));
+      d2.push_back(src >= 0 ? b * (n + 1) + m : -1);
+    }
+  }
+  const size_t os1 = p.add(s1), od1 = p.add(d1), os2 = p.add(s2), od2 = p.add(d2);
+  RCK(upload(h, p, h->st));
+  OTHER(h, launch_copy_rows, h1s, p.at(os1), nullptr, nullptr, G, p.at(od1), s.d, B, h->st);
+  OTHER(h, launch_copy_rows, X, p.at(os2), nullptr, nullptr, G, p.at(od2), s.d, B * (n + 1), h->st);
+  float* logits = h->R<float>(h->rg.logits);
+  Linear un{};
+  un.X = G; un.ldx = s.d; un.M = B * (n + 1); un.K = s.d; un.N = 256; un.gain = h->g_nt; un.eps = c.rms_eps;
+  un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
+  un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
+  RCK(run_linear(h, un, h->sc_main, h->st));
+  OTHER(h, launch_verify_ext, logits, d_draft, B, n, h->R<int32_t>(h->rg.active), d_out, d_accept_len,
+        h->engine ? h->d_err : nullptr, h->st);
+  HIPCK(h, hipMemcpyAsync(h->h_cand, d_out, (size_t)B * (n + 1), hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
+  HIPCK(h, hipStreamSynchronize(h->st));
+  RCK(check_fault(h));
+  // keep the accepted drafts; the verifier's byte after them is the pending bonus; h1
+  // = the prediction row after the kept drafts, h1s = the one before any draft
+  Plan& q = h->plan[1];  // its previous upload completed at the synchronization above
+  q.clear();
+  for (int b = 0; b < B; ++b) {
+    const int j = std::max(0, std::min(n, h->h_len[b] - 1));
+    truncate_row(h->rows[b], h->pre_len[b] + j);
+    h->rows[b].bonus = h->h_cand[(size_t)b * (n + 1) + j];
+    s3.push_back(b * (n + 1) + j);
+    d3.push_back(h->rg.row_h1 + b);
+  }
+  for (int b = 0; b < B; ++b) {
+    s3.push_back(b * (n + 1));
+    d3.push_back(h->rg.row_h1s + b);
+  }
+  const size_t os3 = q.add(s3), od3 = q.add(d3);
+  RCK(upload(h, q, h->st));
+  OTHER(h, launch_copy_rows, G, q.at(os3), nullptr, nullptr, h->rows_base(), q.at(od3), s.d, 2 * B, h->st);
+  h->pending = true;
+  h->last_n = n + 1;
+  h->last_mode = kModeExternal;
+  return MBP_OK;
+}
+
 extern "C" int mbp_last_accepted(mbp_handle* h, uint8_t* h_bytes, int32_t* h_lens) {
   int rc = check_ready(h);
   if (rc) return rc;
@@ -1508,7 +1624,7 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
   if (h_override) {
     for (int b = 0; b < B; ++b)
       if (h_override_len[b] < 0 || h_override_len[b] > s.nmax) return fail(h, MBP_EINVAL, "override length out of range");
-    const bool rollback = h->pending && h->last_mode == MBP_ACCEPT_SELF_VERIFY;
+    const bool rollback = h->pending && (h->last_mode == MBP_ACCEPT_SELF_VERIFY || h->last_mode == kModeExternal);
     for (int b = 0; b < B; ++b) {
       add[b].assign(h_override + (size_t)b * s.nmax, h_override + (size_t)b * s.nmax + h_override_len[b]);
       Row sim = h->rows[b];
@@ -1518,10 +1634,18 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
         return fail(h, MBP_ECAPACITY, "row would exceed max_latents");
     }
     if (rollback) {
-      for (int b = 0; b < B; ++b) truncate_row(h->rows[b], h->pre_len[b]);
+      for (int b = 0; b < B; ++b) {
+        truncate_row(h->rows[b], h->pre_len[b]);
+        h->rows[b].bonus = -1;  // part of the rolled-back step
+      }
       HIPCK(h, hipMemcpyAsync(h->row_ptr(h->rg.row_h1), h->row_ptr(h->rg.row_h1s), (size_t)B * s.d * 4,
                               hipMemcpyDeviceToDevice, h->st));
     }
+  } else if (h->last_mode == kModeExternal) {
+    // the kept drafts are committed; each row's bonus byte stays pending for the next
+    // tentative commit (or is committed before a decode step)
+    h->pending = false;
+    return MBP_OK;
   } else if (h->last_mode == MBP_ACCEPT_THRESHOLD) {
     RCK(check_fault(h));
     const int n = h->last_n;
@@ -1546,7 +1670,7 @@ extern "C" int mbp_get_logits(mbp_handle* h, float* d_logits) {
 
 extern "C" int32_t mbp_row_length(const mbp_handle* h, int32_t row) {
   if (!h || row < 0 || row >= h->batch) return MBP_EINVAL;
-  return (int32_t)h->rows[row].x.size();
+  return (int32_t)h->rows[row].x.size() + (h->rows[row].bonus >= 0 ? 1 : 0);
 }
 
 extern "C" int mbp_set_timing(mbp_handle* h, int32_t on) {

@@ -47,6 +47,15 @@ def _cfg(mbp, wl="lca_d1024_b1", **kw):
     return mbp.make_config(w.model, **args)
 
 
+def test_manifest_of_models_without_mb_head(mbp):
+    for model in (synth.TINY_FXT, synth.D1024_FXT):
+        cfg = mbp.make_config(model, max_batch=1, max_ctx=512, max_n=8)
+        lib_man = mbp.weight_manifest(cfg)
+        gen_man = synth.manifest(model)
+        assert [n for n, _ in lib_man] == [n for n, _ in gen_man]
+        assert mbp.lib().mbp_workspace_bytes(ctypes.byref(cfg)) > 0
+
+
 @pytest.mark.parametrize("wl", list(synth.WORKLOADS))
 def test_manifest_matches_generator(mbp, wl):
     cfg = _cfg(mbp, wl)
