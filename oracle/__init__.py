@@ -31,6 +31,11 @@ from .model import (  # noqa: F401
     verify_drafts,
     verify_step,
     verify_external,
+    decoding_dist,
+    sample_byte,
+    step_sampled,
+    speculative_accept,
+    verify_step_sampled,
     generate_external,
     generate,
     greedy_generate,

@@ -361,6 +361,81 @@ def generate_external(Wd, cfg_d, Wv, cfg_v, prompt, n_new, n):
     return np.array(out, dtype=np.uint8), steps
 
 
+# ------------------------------------------------------------ sampled decoding --
+# Sampled decoding (the paper samples at temperature 0.7 with top-p 0.9 for one of its
+# tasks and verifies drafts with speculative decoding, Section 6).  The uniforms are
+# inputs: u[m] samples candidate m, u[n + m] decides the acceptance of draft m and
+# u[2n + m] samples its replacement (verification), m = 0..n-1.
+
+def decoding_dist(logits, temperature, top_p):
+    """Distribution a byte is sampled from: softmax(logits / temperature) restricted to
+    the nucleus (bytes ranked by probability, ties by lower byte value; a byte is in
+    the nucleus while the probability ranked before it is below top_p) and
+    renormalized."""
+    z = np.asarray(logits, np.float64) / float(temperature)
+    p = np.exp(z - z.max())
+    p /= p.sum()
+    before = np.empty(256)
+    for i in range(256):
+        ahead = (p > p[i]) | ((p == p[i]) & (np.arange(256) < i))
+        before[i] = p[ahead].sum()
+    q = np.where(before < top_p, p, 0.0)
+    return q / q.sum()
+
+
+def sample_byte(q, u):
+    """Inverse CDF in byte order: the first byte whose cumulative mass exceeds u (the
+    last byte of positive mass if rounding leaves none)."""
+    c = np.cumsum(np.asarray(q, np.float64))
+    hit = np.nonzero(c > u)[0]
+    return int(hit[0]) if len(hit) else int(np.nonzero(np.asarray(q) > 0)[0][-1])
+
+
+def step_sampled(W, cfg, x, n, tau, temperature, top_p, u):
+    """Threshold acceptance on sampled candidates: candidate m is sampled from its
+    row's decoding distribution with u[m]; P_m is its probability there; the rule of
+    Section 3.1 then applies to P."""
+    logits = step_logits(W, cfg, x, n)
+    qs = [decoding_dist(logits[m], temperature, top_p) for m in range(n)]
+    cand = np.array([sample_byte(qs[m], u[m]) for m in range(n)], np.int64)
+    prob = np.array([qs[m][cand[m]] for m in range(n)])
+    return {"logits": logits, "q": qs, "cand": cand, "prob": prob, "k": threshold_accept(prob, tau)}
+
+
+def speculative_accept(p_rows, q_rows, cand, u, n):
+    """Speculative sampling (Leviathan et al.) of drafts cand[1..n-1] (cand[0] is kept):
+    draft m (m >= 2), drawn from q_rows[m-1], is kept when u[n+m-1] < p(c_m) / q(c_m)
+    with p = p_rows[m-2], the target distribution after the previous drafts; at the first
+    rejection a byte drawn from max(0, p - q) (normalized) with u[2n+m-1] replaces it and
+    ends the step.  Returns the accepted bytes."""
+    out = [int(cand[0])]
+    for m in range(2, n + 1):
+        pm, qm, c = np.asarray(p_rows[m - 2], np.float64), np.asarray(q_rows[m - 1], np.float64), int(cand[m - 1])
+        if u[n + m - 1] < pm[c] / qm[c]:
+            out.append(c)
+            continue
+        r = np.maximum(pm - qm, 0.0)
+        out.append(sample_byte(r / r.sum(), u[2 * n + m - 1]))
+        break
+    return out
+
+
+def verify_step_sampled(W, cfg, x, n, temperature, top_p, u):
+    """Verification of sampled drafts (Section 6): c_1 is sampled from the next-byte
+    head and kept; drafts c_2..c_n are sampled from the MB rows and checked by
+    speculative sampling against the next-byte decoding distribution after the
+    drafts before them.  Returns the accepted bytes (k of them)."""
+    s = step_sampled(W, cfg, x, n, 2.0, temperature, top_p, u)
+    p_rows = []
+    for m in range(2, n + 1):
+        seq = np.asarray(list(x) + [int(c) for c in s["cand"][: m - 1]], np.int64)
+        tr = trunk(W, cfg, seq)
+        p_rows.append(decoding_dist(head_logits(tr["h1"][-1], W["nt_norm"], W, cfg.rms_eps), temperature, top_p))
+    out = speculative_accept(p_rows, s["q"], s["cand"], u, n)
+    return {"logits": s["logits"], "cand": s["cand"], "prob": s["prob"], "p": p_rows, "q": s["q"], "k": len(out),
+            "bytes": np.array(out, dtype=np.uint8)}
+
+
 def generate(W, cfg, prompt, n_new, n, tau, mode="threshold"):
     """Run steps until ``n_new`` bytes are emitted; the last step is truncated."""
     x = [int(b) for b in prompt]

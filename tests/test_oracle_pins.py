@@ -487,3 +487,79 @@ def test_external_generation_equals_verifier_greedy(same, gain, n):
     assert all(1 <= s["k"] <= n + 1 for s in steps)
     if same:  # the verifier's own drafts: its first draft is always its greedy byte
         assert all(s["k"] >= 2 for s in steps[:-1])
+
+
+# --------------------------------------------------------------- sampling --
+# Temperature / top-p sampling with given uniforms and speculative sampling of drafts.
+
+def _row(vals):
+    r = np.full(256, -1e30)
+    r[: len(vals)] = vals
+    return r
+
+
+def test_decoding_dist_closed_forms():
+    rng = np.random.default_rng(0)
+    l = rng.normal(size=256) * 3
+    for T in (0.5, 1.0, 2.0):
+        e = np.exp(l / T - np.max(l / T))
+        np.testing.assert_allclose(oracle.decoding_dist(l, T, 1.0), e / e.sum(), rtol=1e-12, atol=1e-15)
+    q = oracle.decoding_dist(l, 0.7, 1e-12)  # the nucleus is the top byte alone
+    assert q[int(np.argmax(l))] == 1.0 and q.sum() == 1.0
+    # hand example: P = .4 .3 .2 .1; the mass before byte 1 is .4 < .65, before byte 2 .7
+    q = oracle.decoding_dist(_row(np.log([4.0, 3.0, 2.0, 1.0])), 1.0, 0.65)
+    np.testing.assert_allclose(q[:4], [4 / 7, 3 / 7, 0.0, 0.0], atol=1e-12)
+    # ties rank by lower byte value: of two equal top bytes (2/7 each) only byte 3 is kept
+    # at top_p .25 (the mass before byte 4 is 2/7 > .25)
+    q = oracle.decoding_dist(_row(np.log([1.0, 1.0, 1.0, 2.0, 2.0])), 1.0, 0.25)
+    np.testing.assert_allclose(q[:5], [0, 0, 0, 1, 0], atol=1e-12)
+
+
+def test_sample_byte_inverse_cdf_counts():
+    q = oracle.decoding_dist(np.random.default_rng(1).normal(size=256) * 2, 0.8, 0.9)
+    N = 20000
+    counts = np.bincount([oracle.sample_byte(q, (k + 0.5) / N) for k in range(N)], minlength=256)
+    assert np.all(np.abs(counts - q * N) <= 1.0 + 1e-9)
+    assert counts[q == 0].sum() == 0
+
+
+def test_sampled_step_with_a_one_byte_nucleus_is_greedy():
+    W = synth.make_weights(TINY, seed=31, logit_gain=5.0)
+    x = synth.make_prompt(6, 40)
+    u = np.random.default_rng(2).random(12)
+    s = oracle.step_sampled(W, TINY, x, 4, 0.5, 0.7, 1e-12, u)
+    g = oracle.step(W, TINY, x, 4, 0.5)
+    np.testing.assert_array_equal(s["cand"], g["cand"])
+    assert s["k"] == 4 and np.all(s["prob"] == 1.0)
+    # one-hot p and q: a rejected draft is replaced by the next-byte greedy byte, so the
+    # step gives greedy verification's bytes plus that byte when a draft is rejected
+    for n in (2, 4, 6):
+        v = oracle.verify_step_sampled(W, TINY, x, n, 0.7, 1e-12, np.random.default_rng(n).random(3 * n))
+        gv = oracle.verify_step(W, TINY, x, n)
+        acc = [int(c) for c in gv["cand"][: gv["k"]]]
+        assert [int(b) for b in v["bytes"][: gv["k"]]] == acc
+        if gv["k"] < n:
+            assert v["k"] == gv["k"] + 1
+            assert int(v["bytes"][-1]) == int(oracle.greedy_generate(W, TINY, list(x) + acc, 1)[0])
+        else:
+            assert v["k"] == n
+
+
+def test_speculative_accept_output_law_is_the_target():
+    """The byte after c_1 has the target distribution p whatever the draft
+    distribution q (the property speculative sampling guarantees): enumerate the draft
+    over q and the two uniforms on grids."""
+    rng = np.random.default_rng(3)
+    for _ in range(3):
+        p = rng.dirichlet(np.ones(8) * 0.7)
+        q = rng.dirichlet(np.ones(8) * 0.7)
+        N = 400
+        law = np.zeros(8)
+        for c in range(8):
+            for a in range(N):
+                for r in range(N):
+                    u = np.zeros(6)
+                    u[3], u[5] = (a + 0.5) / N, (r + 0.5) / N
+                    out = oracle.speculative_accept([p], [None, q], [0, c], u, 2)
+                    law[out[1]] += q[c] / (N * N)
+        np.testing.assert_allclose(law, p, atol=3.0 / N)
