@@ -90,9 +90,14 @@ def measured_traffic(kernel_class, workload):
     return int(fields["hbm bytes per launch"])
 
 
-def run_steps(dec, steps, n, tau, mode):
-    for _ in range(steps):
-        dec.decode_step(n, tau, mode)
+def run_steps(dec, steps, n, tau, mode, samp=None):
+    """samp: (temperature, top_p, uniforms [steps, B, 3n] on the device) for sampled
+    decoding."""
+    for i in range(steps):
+        if samp:
+            dec.decode_step_sampled(n, tau, mode, samp[0], samp[1], samp[2][i])
+        else:
+            dec.decode_step(n, tau, mode)
         dec.accept()
 
 
@@ -144,11 +149,19 @@ def main():
     decs = [dec] + ([ver] if ext else [])
     log(f"[bench] weights + init {time.time() - t0:.1f}s")
 
+    # sampled decoding: every step's uniforms, generated before any timed region
+    samp = None
+    if wl.temperature > 0:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(0)
+        U = torch.rand((max(K, W), B, 3 * n), generator=gen, device="cuda", dtype=torch.float32)
+        samp = (wl.temperature, wl.top_p, U)
+
     def run(steps):
         if ext:
             run_external(dec, ver, steps, n, THRESHOLD)
         else:
-            run_steps(dec, steps, n, tau, mode)
+            run_steps(dec, steps, n, tau, mode, samp)
 
     t0 = time.time()
     for d in decs:
@@ -225,10 +238,18 @@ def main():
         got = 0
         c0 = time.perf_counter()
         V64 = oracle.to_float64(vweights) if ext else None
-        for _ in range(args.cpu_steps if not ext else min(args.cpu_steps, 1)):
+        for got_steps in range(args.cpu_steps if not ext else min(args.cpu_steps, 1)):
             if ext:
                 r = oracle.verify_external(V64, wl.verifier, x, oracle.step(W64, model, x, n, tau)["cand"])
                 acc = [int(c) for c in r["bytes"]]
+            elif samp:
+                u = samp[2][got_steps, 0].double().cpu().numpy()
+                if mode == THRESHOLD:
+                    r = oracle.step_sampled(W64, model, x, n, tau, wl.temperature, wl.top_p, u)
+                    acc = [int(c) for c in r["cand"][: r["k"]]]
+                else:
+                    acc = [int(c) for c in oracle.verify_step_sampled(W64, model, x, n, wl.temperature, wl.top_p,
+                                                                      u)["bytes"]]
             else:
                 r = oracle.step(W64, model, x, n, tau) if mode == THRESHOLD else oracle.verify_step(W64, model, x, n)
                 acc = [int(c) for c in r["cand"][: r["k"]]]
@@ -259,6 +280,7 @@ def main():
                         f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb} head={model.head}, "
                         + (f"verified by a next-byte model with layers enc/lm/nt={wl.verifier.n_enc}/"
                            f"{wl.verifier.n_lm}/{wl.verifier.n_nb}, " if ext else "")
+                        + (f"sampled at temperature {wl.temperature} top-p {wl.top_p}, " if samp else "")
                         + f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
             "batch": B, "prompt_len": wl.prompt_len, "n": n, "tau": tau, "mode": wl.mode,
             "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32",

@@ -156,6 +156,28 @@ int mbp_prefill(mbp_handle *h, const uint8_t *h_bytes, const int32_t *h_lens, in
 int mbp_decode_step(mbp_handle *h, int32_t n, float tau, int32_t mode, uint8_t *d_cand,
                     float *d_prob, int32_t *d_accept_len);
 
+/* mbp_decode_step with sampled candidates (the paper decodes one task at temperature
+ * 0.7 with top-p 0.9, and verifies drafts with speculative decoding following
+ * Leviathan et al., Section 6).  Each candidate row's decoding distribution is
+ * softmax(logits / temperature) restricted to the nucleus -- bytes ranked by
+ * probability, ties by lower byte value; a byte is in the nucleus while the
+ * probability ranked before it is below top_p -- and renormalized; candidate m is
+ * drawn from it by the inverse CDF in byte order with d_uniforms[b, m].
+ *   mode MBP_ACCEPT_THRESHOLD: d_prob = the candidates' probabilities in their decoding
+ *        distributions, accept_len by the threshold rule on them.
+ *   mode MBP_ACCEPT_SELF_VERIFY: speculative sampling.  Candidate 1 is kept; draft m >= 2
+ *        (drawn from the MB head's distribution q) is kept when d_uniforms[b, n+m-1] <
+ *        p(c_m) / q(c_m), p being the next-byte decoding distribution after the drafts
+ *        before it; at the first rejection a byte drawn from max(0, p - q), normalized,
+ *        with d_uniforms[b, 2n+m-1] replaces the draft in d_cand and ends the step
+ *        (accept_len counts it).  The caches hold the kept drafts; a replacement byte is
+ *        committed at the start of the next step.  Synchronizes.
+ *   temperature > 0, top_p in (0, 1], n <= 8.
+ *   d_uniforms  device float [batch, 3n], values in [0, 1).
+ * Other arguments and results as mbp_decode_step. */
+int mbp_decode_step_sampled(mbp_handle *h, int32_t n, float tau, int32_t mode, float temperature, float top_p,
+                            const float *d_uniforms, uint8_t *d_cand, float *d_prob, int32_t *d_accept_len);
+
 /* External verification (Section 6, "Improving Baseline Throughput with MBP Models"):
  * this handle's model -- typically one without an MB head (n_mb = 0: encoder, LM
  * module and next-byte decoder, the FxT baseline) -- checks n drafts made by another

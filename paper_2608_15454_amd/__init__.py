@@ -75,6 +75,9 @@ def lib():
     L.mbp_prefill.restype = ctypes.c_int
     L.mbp_decode_step.argtypes = [P, ctypes.c_int32, ctypes.c_float, ctypes.c_int32, P, P, P]
     L.mbp_decode_step.restype = ctypes.c_int
+    L.mbp_decode_step_sampled.argtypes = [P, ctypes.c_int32, ctypes.c_float, ctypes.c_int32, ctypes.c_float,
+                                          ctypes.c_float, P, P, P, P]
+    L.mbp_decode_step_sampled.restype = ctypes.c_int
     L.mbp_verify_draft.argtypes = [P, P, ctypes.c_int32, P, P]
     L.mbp_verify_draft.restype = ctypes.c_int
     L.mbp_last_accepted.argtypes = [P, P, P]
@@ -215,6 +218,23 @@ class Decoder:
         self._check(self.L.mbp_decode_step(self.h, n, float(tau), mode, ctypes.c_void_p(cand.data_ptr()),
                                            ctypes.c_void_p(prob.data_ptr()),
                                            ctypes.c_void_p(self.accept_len.data_ptr())))
+        self.n = n
+        return cand.view(B, n), prob.view(B, n), self.accept_len[:B]
+
+    def decode_step_sampled(self, n, tau, mode, temperature, top_p, uniforms):
+        """decode_step with candidates sampled at ``temperature`` / ``top_p`` with the
+        device float uniforms [B, 3n]; returns the same device views as decode_step."""
+        import torch
+
+        B = self.batch
+        uniforms = uniforms.contiguous()
+        assert uniforms.dtype == torch.float32 and uniforms.numel() == B * 3 * n
+        cand = self.cand.view(-1)[: B * n]
+        prob = self.prob.view(-1)[: B * n]
+        self._check(self.L.mbp_decode_step_sampled(self.h, n, float(tau), mode, float(temperature), float(top_p),
+                                                   ctypes.c_void_p(uniforms.data_ptr()),
+                                                   ctypes.c_void_p(cand.data_ptr()), ctypes.c_void_p(prob.data_ptr()),
+                                                   ctypes.c_void_p(self.accept_len.data_ptr())))
         self.n = n
         return cand.view(B, n), prob.view(B, n), self.accept_len[:B]
 

@@ -131,6 +131,22 @@ hipError_t launch_accept(const float* logits, int B, int n, float tau, const int
 // Greedy verification: NT logits of the n tentative rows vs the drafts.
 hipError_t launch_verify(const float* nt_logits, const uint8_t* cand, int B, int n, const int32_t* active,
                          int32_t* accept_len, const int32_t* fault, hipStream_t st, const Ev& ev = Ev());
+// Sampled decoding (n <= 8).  uniforms: device float [B, 3n] in [0, 1): u[m] samples
+// candidate m, u[n + m] decides draft m's acceptance, u[2n + m] samples its
+// replacement.  launch_sample_accept: candidates sampled from each row's decoding
+// distribution (softmax(l / temperature) on the top-p nucleus), prob = their
+// probability there, then accept_len as launch_accept.  launch_verify_sampled:
+// speculative sampling of drafts 2..n against target_logits [B, n, 256] (row m-2 is
+// the next-byte output after the drafts before m); cand gets a rejected draft's
+// replacement, accept_len the accepted count.
+hipError_t launch_sample_accept(const float* logits, int B, int n, float tau, float temperature, float top_p,
+                                const float* uniforms, const int32_t* active, uint8_t* cand, float* prob,
+                                int32_t* accept_len, int write_len, const int32_t* fault, uint8_t* host_cand,
+                                int32_t* host_len, hipStream_t st, const Ev& ev = Ev());
+hipError_t launch_verify_sampled(const float* draft_logits, const float* target_logits, int B, int n,
+                                 float temperature, float top_p, const float* uniforms, const int32_t* active,
+                                 uint8_t* cand, int32_t* accept_len, const int32_t* fault, hipStream_t st,
+                                 const Ev& ev = Ev());
 // External verification of n drafts per batch row (n + 1 <= kMaxVerifyRows): logits
 // [B, n+1, 256] are the verifier's next-byte logits after 0..n drafts; out [B, n+1]
 // gets the kept drafts and the verifier's greedy byte after them, accept_len their

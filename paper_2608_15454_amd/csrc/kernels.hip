@@ -719,6 +719,228 @@ __device__ __forceinline__ float row_top1(const float* row, int lane, int* idx_o
   return 1.0f / s;
 }
 
+// ---- sampled decoding ----
+// Partner of a compare-exchange at a stride of 4*O positions: the same slot of lane ^ O.
+template <int O>
+__device__ __forceinline__ void cx_fetch(const float (&key)[4], const int (&idx)[4], float (&ok)[4], int (&oi)[4]) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    ok[t] = xor_lane<O>(key[t]);
+    oi[t] = __builtin_bit_cast(int, xor_lane<O>(__builtin_bit_cast(float, idx[t])));
+  }
+}
+
+// Bitonic sort of the wave's 256 (key, idx) pairs, position 4*lane + t, into
+// descending key order, ties by ascending idx (idx values distinct).
+__device__ __forceinline__ void sort_desc_wave(float (&key)[4], int (&idx)[4], int lane) {
+#pragma unroll
+  for (int size = 2; size <= 256; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      float ok[4];
+      int oi[4];
+      if (stride == 128) cx_fetch<32>(key, idx, ok, oi);
+      else if (stride == 64) cx_fetch<16>(key, idx, ok, oi);
+      else if (stride == 32) cx_fetch<8>(key, idx, ok, oi);
+      else if (stride == 16) cx_fetch<4>(key, idx, ok, oi);
+      else if (stride == 8) cx_fetch<2>(key, idx, ok, oi);
+      else if (stride == 4) cx_fetch<1>(key, idx, ok, oi);
+      else {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          ok[t] = key[t ^ stride];
+          oi[t] = idx[t ^ stride];
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const int e = 4 * lane + t;
+        const bool lower = (e & stride) == 0;  // the lower position of its pair
+        const bool down = (e & size) == 0;     // this block sorts most-probable first
+        const bool og = ok[t] > key[t] || (ok[t] == key[t] && oi[t] < idx[t]);  // the partner ranks first
+        if (lower == down ? og : !og) {
+          key[t] = ok[t];
+          idx[t] = oi[t];
+        }
+      }
+    }
+  }
+}
+
+
+// Decoding distribution of a 256-logit row, by one wave: softmax(row / T) restricted to
+// the nucleus (bytes ranked by probability, ties by lower byte value; a byte is kept
+// while the probability ranked before it is below top_p), renormalized, into q[256].
+// p[256] is the wave's LDS scratch.  A wave's own LDS accesses are ordered, so no
+// barrier is needed.
+__device__ void decoding_dist_wave(const float* row, float inv_t, float top_p, float* p, float* q, int lane) {
+  float e[4], mx = -INFINITY;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    e[j] = row[lane + 64 * j] * inv_t;
+    mx = fmaxf(mx, e[j]);
+  }
+  mx = wave_max(mx);
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    e[j] = expf(e[j] - mx);
+    s += e[j];
+  }
+  s = wave_sum(s);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    e[j] /= s;
+    p[lane + 64 * j] = e[j];
+  }
+  // rank: sort (probability, byte) pairs, most probable first, ties by lower byte
+  // (bitonic network over positions 4*lane + t; strides >= 4 pair lanes lane ^ stride/4)
+  float key[4];
+  int idx[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    key[t] = p[4 * lane + t];
+    idx[t] = 4 * lane + t;
+  }
+  sort_desc_wave(key, idx, lane);
+  // mass ranked before each sorted entry: lane prefix plus a scan over the lanes
+  const float tot = key[0] + key[1] + key[2] + key[3];
+  float incl = tot;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  float before = incl - tot, kept = 0.f;
+  bool keep[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    keep[t] = before < top_p;
+    kept += keep[t] ? key[t] : 0.f;
+    before += key[t];
+  }
+  kept = wave_sum(kept);
+#pragma unroll
+  for (int t = 0; t < 4; ++t) q[idx[t]] = keep[t] ? key[t] / kept : 0.f;
+}
+
+// Inverse CDF in byte order, by one wave (every lane gets the result): the first byte
+// of positive mass whose cumulative mass exceeds u, else the last byte of positive
+// mass.  Lane l sums bytes 4l..4l+3, then a scan over the lanes gives the cumulative
+// mass before each lane's bytes.
+__device__ int sample_inv_cdf(const float* q, float u, int lane) {
+  const float4 v = reinterpret_cast<const float4*>(q)[lane];
+  const float qv[4] = {v.x, v.y, v.z, v.w};
+  const float tot = v.x + v.y + v.z + v.w;
+  float incl = tot;  // inclusive scan of the lane totals
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const float t = __shfl_up(incl, o);
+    if (lane >= o) incl += t;
+  }
+  float acc = incl - tot;
+  int hit = -1, last = -1;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    acc += qv[t];
+    if (qv[t] > 0.f) {
+      last = 4 * lane + t;
+      if (hit < 0 && acc > u) hit = 4 * lane + t;
+    }
+  }
+  const uint64_t hits = __builtin_amdgcn_ballot_w64(hit >= 0);
+  if (hits != 0) return __shfl(hit, __builtin_ctzll(hits));
+  const uint64_t pos = __builtin_amdgcn_ballot_w64(last >= 0);
+  return pos != 0 ? __shfl(last, 63 - __builtin_clzll(pos)) : 0;
+}
+
+// Threshold acceptance on sampled candidates: per batch row b, wave m samples
+// candidate m from the decoding distribution of logits row (b, m) with
+// uniforms[b*3n + m]; its probability there is prob; accept_len and the pinned host
+// copies as in accept_kernel.
+__global__ void sample_accept_kernel(const float* logits, int n, float tau, float inv_t, float top_p,
+                                     const float* uniforms, const int32_t* active, uint8_t* cand, float* prob,
+                                     int32_t* accept_len, int write_len, const int32_t* fault, uint8_t* host_cand,
+                                     int32_t* host_len) {
+  __shared__ __align__(16) float sp[8][256];
+  __shared__ __align__(16) float sq[8][256];
+  __shared__ float ps[8];
+  const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  if (wave < n) {
+    decoding_dist_wave(logits + ((size_t)b * n + wave) * 256, inv_t, top_p, sp[wave], sq[wave], lane);
+    const int c = sample_inv_cdf(sq[wave], uniforms[(size_t)b * 3 * n + wave], lane);
+    if (lane == 0) {
+      const float pr = sq[wave][c];
+      cand[b * n + wave] = (uint8_t)c;
+      if (host_cand) host_cand[b * n + wave] = (uint8_t)c;
+      if (prob) prob[b * n + wave] = pr;
+      ps[wave] = pr;
+    }
+  }
+  __syncthreads();
+  if (tid == 0 && write_len) {
+    int k = 1;
+    while (k < n && ps[k] >= tau) ++k;
+    const int32_t len = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
+    accept_len[b] = len;
+    if (host_len) {
+      __threadfence_system();
+      __hip_atomic_store(host_len + b, len, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+  }
+}
+
+// Speculative sampling of drafts cand[b, 1..n-1] (cand[b, 0] is kept): wave w handles
+// draft m = w + 2, sampled from the decoding distribution q of draft_logits row
+// (b, m-1); p is the decoding distribution of target row (b, m-2) (the next-byte
+// output after the drafts before m).  The draft is kept when u[n+m-1] < p(c) / q(c);
+// else a byte drawn from max(0, p - q) with u[2n+m-1] replaces it and ends the step.
+// cand gets the replacement; accept_len the accepted count (-1 after a failed wait).
+__global__ void verify_sampled_kernel(const float* draft_logits, const float* target_logits, int n, float inv_t,
+                                      float top_p, const float* uniforms, const int32_t* active, uint8_t* cand,
+                                      int32_t* accept_len, const int32_t* fault) {
+  __shared__ __align__(16) float sp[7][256];
+  __shared__ __align__(16) float sq[7][256];
+  __shared__ __align__(16) float sr[7][256];
+  __shared__ int keep[7], rep[7];
+  const int b = blockIdx.x, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const float* u = uniforms + (size_t)b * 3 * n;
+  if (wave < n - 1) {
+    const int m = wave + 2;
+    decoding_dist_wave(draft_logits + ((size_t)b * n + m - 1) * 256, inv_t, top_p, sr[wave], sq[wave], lane);
+    decoding_dist_wave(target_logits + ((size_t)b * n + m - 2) * 256, inv_t, top_p, sr[wave], sp[wave], lane);
+    const int c = cand[b * n + m - 1];
+    float rs = 0.f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int i = lane + 64 * j;
+      const float r = fmaxf(sp[wave][i] - sq[wave][i], 0.f);
+      sr[wave][i] = r;
+      rs += r;
+    }
+    rs = wave_sum(rs);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) sr[wave][lane + 64 * j] = rs > 0.f ? sr[wave][lane + 64 * j] / rs : 0.f;
+    const int r = sample_inv_cdf(sr[wave], u[2 * n + m - 1], lane);
+    if (lane == 0) {
+      const float qc = sq[wave][c];
+      keep[wave] = qc > 0.f && u[n + m - 1] < sp[wave][c] / qc;
+      rep[wave] = rs > 0.f ? r : c;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int k = n;
+    for (int m = 2; m <= n; ++m) {
+      if (keep[m - 2]) continue;
+      cand[b * n + m - 1] = (uint8_t)rep[m - 2];
+      k = m;
+      break;
+    }
+    accept_len[b] = (fault != nullptr && *fault != 0) ? -1 : (active[b] ? k : 0);
+  }
+}
+
 __global__ void accept_kernel(const float* logits, int n, float tau, const int32_t* active, uint8_t* cand,
                               float* prob, int32_t* accept_len, int write_len, const int32_t* fault,
                               uint8_t* host_cand, int32_t* host_len) {
@@ -986,6 +1208,27 @@ hipError_t launch_accept(const float* logits, int B, int n, float tau, const int
   if (B <= 0) return hipSuccess;
   return klaunch(accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau, active, cand, prob,
                  accept_len, write_len, fault, host_cand, host_len);
+}
+
+hipError_t launch_sample_accept(const float* logits, int B, int n, float tau, float temperature, float top_p,
+                                const float* uniforms, const int32_t* active, uint8_t* cand, float* prob,
+                                int32_t* accept_len, int write_len, const int32_t* fault, uint8_t* host_cand,
+                                int32_t* host_len, hipStream_t st, const Ev& ev) {
+  if (B <= 0) return hipSuccess;
+  if (n < 1 || n > 8) return hipErrorInvalidValue;
+  return klaunch(sample_accept_kernel, dim3(B), dim3(64 * n), 0, st, ev.start, ev.stop, logits, n, tau,
+                 1.0f / temperature, top_p, uniforms, active, cand, prob, accept_len, write_len, fault, host_cand,
+                 host_len);
+}
+
+hipError_t launch_verify_sampled(const float* draft_logits, const float* target_logits, int B, int n,
+                                 float temperature, float top_p, const float* uniforms, const int32_t* active,
+                                 uint8_t* cand, int32_t* accept_len, const int32_t* fault, hipStream_t st,
+                                 const Ev& ev) {
+  if (B <= 0) return hipSuccess;
+  if (n < 1 || n > 8) return hipErrorInvalidValue;
+  return klaunch(verify_sampled_kernel, dim3(B), dim3(64 * (n > 1 ? n - 1 : 1)), 0, st, ev.start, ev.stop,
+                 draft_logits, target_logits, n, 1.0f / temperature, top_p, uniforms, active, cand, accept_len, fault);
 }
 
 hipError_t launch_verify_ext(const float* logits, const uint8_t* draft, int B, int n, const int32_t* active,

@@ -56,6 +56,12 @@ struct KV {  // one module's KV cache: layer l of row b at k + l*layer_stride + 
 // last_mode of a pending step made by mbp_verify_draft
 constexpr int kModeExternal = 2;
 
+// Sampled decoding of a step (mbp_decode_step_sampled): uniforms device [B, 3n].
+struct Sampling {
+  float temperature, top_p;
+  const float* u;
+};
+
 struct Row {
   bool active = false;
   std::vector<uint8_t> x;   // committed bytes
@@ -1041,7 +1047,7 @@ void head_rows_of(mbp_handle* h, int n, std::vector<int32_t>& head_rows, std::ve
 // Candidates of the current step: h1 -> NT row; MB head -> rows 2..n; logits and
 // per-row greedy bytes / probabilities (and accept_len in threshold mode).
 int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, float* d_prob, int32_t* d_len,
-          bool host_out) {
+          bool host_out, const Sampling* smp = nullptr) {
   const Sizes& s = h->sz;
   const mbp_config& c = h->cfg;
   const Regions& rg = h->rg;
@@ -1099,8 +1105,15 @@ int draft(mbp_handle* h, int n, float tau, bool threshold, uint8_t* d_cand, floa
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = logits; un.epi.ldy = 256;
   RCK(run_linear(h, un, sc, h->st));
-  OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
-        h->engine ? h->d_err : nullptr, host_out ? h->h_cand_dev : nullptr, host_out ? h->h_len_dev : nullptr, h->st);
+  if (smp) {
+    OTHER(h, launch_sample_accept, logits, B, n, tau, smp->temperature, smp->top_p, smp->u, h->R<int32_t>(rg.active),
+          d_cand, d_prob, d_len, threshold ? 1 : 0, h->engine ? h->d_err : nullptr,
+          host_out ? h->h_cand_dev : nullptr, host_out ? h->h_len_dev : nullptr, h->st);
+  } else {
+    OTHER(h, launch_accept, logits, B, n, tau, h->R<int32_t>(rg.active), d_cand, d_prob, d_len, threshold ? 1 : 0,
+          h->engine ? h->d_err : nullptr, host_out ? h->h_cand_dev : nullptr, host_out ? h->h_len_dev : nullptr,
+          h->st);
+  }
   h->n_hint = n;
   return MBP_OK;
 }
@@ -1409,8 +1422,8 @@ int commit_bonus(mbp_handle* h) {
   return any ? commit(h, add, true) : MBP_OK;
 }
 
-extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, uint8_t* d_cand, float* d_prob,
-                               int32_t* d_accept_len) {
+static int decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, const Sampling* smp, uint8_t* d_cand,
+                       float* d_prob, int32_t* d_accept_len) {
   int rc = check_ready(h);
   if (rc) return rc;
   const Sizes& s = h->sz;
@@ -1440,14 +1453,14 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   for (int b = 0; b < B; ++b) h->h_len[b] = kLenPending;
   if (mode == MBP_ACCEPT_THRESHOLD) {
     // the accept kernel also writes the candidates and lengths to pinned host memory
-    RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len, true));
+    RCK(draft(h, n, tau, true, d_cand, d_prob, d_accept_len, true, smp));
     h->pending = true;
     h->last_n = n;
     h->last_mode = mode;
     return MBP_OK;
   }
   // self-verify: drafts, tentative commit of all n drafts, greedy check, rollback
-  RCK(draft(h, n, tau, false, d_cand, d_prob, d_accept_len, false));
+  RCK(draft(h, n, tau, false, d_cand, d_prob, d_accept_len, false, smp));
   HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
   std::vector<std::vector<uint8_t>> add(B);
@@ -1472,19 +1485,31 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
   un.epi.kind = EPI_STORE; un.epi.Y = vlog; un.epi.ldy = 256;
   RCK(run_linear(h, un, h->sc_main, h->st));
-  OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len,
-        h->engine ? h->d_err : nullptr, h->st);
+  std::vector<uint8_t> drafts(h->h_cand, h->h_cand + (size_t)B * n);
+  if (smp) {
+    OTHER(h, launch_verify_sampled, h->R<float>(h->rg.logits), vlog, B, n, smp->temperature, smp->top_p, smp->u,
+          h->R<int32_t>(h->rg.active), d_cand, d_accept_len, h->engine ? h->d_err : nullptr, h->st);
+    HIPCK(h, hipMemcpyAsync(h->h_cand, d_cand, (size_t)B * n, hipMemcpyDeviceToHost, h->st));
+  } else {
+    OTHER(h, launch_verify, vlog, d_cand, B, n, h->R<int32_t>(h->rg.active), d_accept_len,
+          h->engine ? h->d_err : nullptr, h->st);
+  }
   HIPCK(h, hipMemcpyAsync(h->h_len, d_accept_len, (size_t)B * 4, hipMemcpyDeviceToHost, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
   RCK(check_fault(h));
-  // roll back to the accepted prefix; h1 = NT row of the last accepted draft
+  // roll back to the accepted prefix; h1 = NT row of the last accepted draft.  A
+  // rejected draft's replacement (sampled verification; it differs from the draft)
+  // is not in the caches: it stays pending like an external verification's bonus byte
   Plan& p = h->plan[1];
   p.clear();
   std::vector<int32_t> src, dst;
   for (int b = 0; b < B; ++b) {
     const int j = std::max(1, std::min(n, h->h_len[b]));
-    truncate_row(h->rows[b], h->pre_len[b] + j);
-    src.push_back(b * n + j - 1);
+    const bool replaced = smp && h->h_cand[(size_t)b * n + j - 1] != drafts[(size_t)b * n + j - 1];
+    const int kept = replaced ? j - 1 : j;
+    truncate_row(h->rows[b], h->pre_len[b] + kept);
+    if (replaced) h->rows[b].bonus = h->h_cand[(size_t)b * n + j - 1];
+    src.push_back(b * n + kept - 1);
     dst.push_back(h->rg.row_h1 + b);
   }
   const size_t os = p.add(src), od = p.add(dst);
@@ -1494,6 +1519,23 @@ extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode
   h->last_n = n;
   h->last_mode = mode;
   return MBP_OK;
+}
+
+extern "C" int mbp_decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, uint8_t* d_cand, float* d_prob,
+                               int32_t* d_accept_len) {
+  return decode_step(h, n, tau, mode, nullptr, d_cand, d_prob, d_accept_len);
+}
+
+extern "C" int mbp_decode_step_sampled(mbp_handle* h, int32_t n, float tau, int32_t mode, float temperature,
+                                       float top_p, const float* d_uniforms, uint8_t* d_cand, float* d_prob,
+                                       int32_t* d_accept_len) {
+  if (!h) return MBP_EINVAL;
+  if (!(temperature > 0.f) || !std::isfinite(temperature)) return fail(h, MBP_EINVAL, "temperature must be > 0");
+  if (!(top_p > 0.f && top_p <= 1.f)) return fail(h, MBP_EINVAL, "top_p must be in (0, 1]");
+  if (!d_uniforms) return fail(h, MBP_EINVAL, "null uniforms");
+  if (n > 8) return fail(h, MBP_EINVAL, "sampled decoding takes n <= 8");
+  const Sampling smp{temperature, top_p, d_uniforms};
+  return decode_step(h, n, tau, mode, &smp, d_cand, d_prob, d_accept_len);
 }
 
 extern "C" int mbp_verify_draft(mbp_handle* h, const uint8_t* d_draft, int32_t n, uint8_t* d_out,

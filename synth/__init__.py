@@ -83,6 +83,8 @@ class Workload:
     tau: float
     mode: str = "threshold"  # "threshold" | "verify" | "external"
     verifier: "ModelConfig" = None  # mode "external": the next-byte model checking the drafts
+    temperature: float = 0.0  # > 0: sampled decoding at this temperature (0: greedy)
+    top_p: float = 1.0        # nucleus of sampled decoding
     sweep_n: tuple = ()
     sweep_tau: tuple = ()
     note: str = ""
@@ -110,6 +112,9 @@ WORKLOADS = {
                               tau=0.75, sweep_tau=(0.5, 0.75, 0.9)),
     "verify_d2048_b16": Workload("verify_d2048_b16", _D2048, batch=16, prompt_len=8192, gen_len=512, n=7,
                                  tau=0.75, mode="verify"),
+    # sampled decoding at the paper's settings for its instruction-following task
+    "sampled_d1024_b1": Workload("sampled_d1024_b1", _D1024_LCA, batch=1, prompt_len=4096, gen_len=1024, n=3,
+                                 tau=0.75, temperature=0.7, top_p=0.9),
     # the MBP d=1024 model drafts n = 7 candidates, the FxT d=1024 model verifies them
     "extverify_d1024_b1": Workload("extverify_d1024_b1", _D1024_LCA, batch=1, prompt_len=4096, gen_len=1024, n=7,
                                    tau=0.75, mode="external", verifier=D1024_FXT),
