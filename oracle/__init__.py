@@ -16,6 +16,8 @@ from .model import (  # noqa: F401
     ffn,
     block,
     boundaries,
+    boundary_logits,
+    learned_boundaries,
     group_ids,
     group_start,
     downsample,

@@ -153,6 +153,28 @@ def boundaries(x, max_patch):
     return q
 
 
+def boundary_logits(h_e, W, eps):
+    """Boundary predictor of the encoder-module paragraph, read as a linear probe on the
+    RMS-normalized encoder state: logit_i = w . h_e[i] / RMS(h_e[i]) + b, boundary
+    probability sigmoid(logit_i)."""
+    h = np.asarray(h_e, np.float64)
+    r = np.sqrt(np.mean(h * h, axis=-1) + eps)
+    return (h @ np.asarray(W["bp.w"], np.float64)) / r + float(np.asarray(W["bp.b"]).reshape(-1)[0])
+
+
+def learned_boundaries(h_e, W, max_patch, eps):
+    """Inference-time segmentation with the boundary predictor: byte i ends a segment
+    when its boundary probability is >= 0.5 (logit >= 0; the Gumbel-sigmoid draw is a
+    training device), or when the segment reaches ``max_patch`` bytes."""
+    z = boundary_logits(h_e, W, eps)
+    q, prev = [], -1
+    for i in range(len(z)):
+        if z[i] >= 0.0 or (max_patch > 0 and i - prev >= max_patch):
+            q.append(i)
+            prev = i
+    return q
+
+
 def group_ids(T, q):
     """L(i) = number of boundaries q_j <= i: the latent a byte is upsampled from
     (the boundary byte already uses the latent of the segment it closes)."""
@@ -191,7 +213,8 @@ def trunk(W, cfg, x):
     pos = np.arange(T)
     E = np.asarray(W["emb"], np.float64)[x]
     h_e = stack(E, W, "enc", cfg.n_enc, causal_mask(T), pos, cfg)
-    q = boundaries(x, cfg.max_patch)
+    q = (learned_boundaries(h_e, W, cfg.max_patch, cfg.rms_eps) if cfg.boundary == "learned"
+         else boundaries(x, cfg.max_patch))
     h_down = downsample(h_e, q)
     LMin = np.vstack([np.asarray(W["bos"], np.float64)[None, :], h_down])
     K1 = LMin.shape[0]

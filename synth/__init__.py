@@ -56,12 +56,14 @@ class ModelConfig:
     attn_scale: float = 1.0
     max_patch: int = 16  # length cap of a segment; 0 = pure space rule
     window_mode: int = 0  # 0: MB layers see only the previous+current group window
+    boundary: str = "space"  # "space": 0x20 rule; "learned": boundary predictor on h_e
 
     def __post_init__(self):
         if self.d_ff == 0:
             object.__setattr__(self, "d_ff", 4 * self.d_model)
         assert self.head in ("lca", "mlp")
         assert self.dtype in ("f32", "bf16")
+        assert self.boundary in ("space", "learned")
         assert self.d_model % self.n_heads == 0
 
     @property
@@ -155,6 +157,8 @@ def manifest(cfg: ModelConfig):
         for i in range(cfg.n_mb):
             out += [(f"mlp.{i}.norm", (d,)), (f"mlp.{i}.w_gate", (dff, d)),
                     (f"mlp.{i}.w_up", (dff, d)), (f"mlp.{i}.w_down", (d, dff))]
+    if cfg.boundary == "learned":
+        out += [("bp.w", (d,)), ("bp.b", (1,))]  # boundary predictor: logit = w . h_e + b
     return out
 
 
@@ -176,7 +180,7 @@ def _is_gain(name: str) -> bool:
 
 
 def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logit_gain: float = 1.0,
-                 std: float = 0.02) -> dict:
+                 std: float = 0.02, bp_bias: float = -0.43) -> dict:
     """Draw every parameter tensor, in manifest order.
 
     * matrices, the embedding, ``bos`` and ``unembed``: N(0, std^2), trunk tensors from
@@ -184,7 +188,11 @@ def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logi
       only in the head share identical trunk weights);
     * norm gains: 1, or 1 + U(-gain_jitter, gain_jitter) from ``PCG64(seed + 2)``;
     * ``logit_gain`` multiplies the two final head norms (``nt_norm``, ``mb_norm``),
-      which scales every logit and so raises the top-1 probabilities of a random model.
+      which scales every logit and so raises the top-1 probabilities of a random model;
+    * boundary predictor (learned boundaries): ``bp.w`` ~ N(0, 1/d) from the head
+      stream, so that w . h / RMS(h) is about N(0, 1), and ``bp.b`` = ``bp_bias``
+      (default -0.43: about one byte in three ends a segment, the paper's 3x
+      compression).
     bf16 models get every tensor rounded to bfloat16.
     """
     rng_trunk = np.random.Generator(np.random.PCG64(seed))
@@ -202,6 +210,10 @@ def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logi
             if name in ("nt_norm", "mb_norm"):
                 a = a * logit_gain
             a = a.astype(np.float32)
+        elif name == "bp.w":
+            a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d_model))
+        elif name == "bp.b":
+            a = np.full(shape, bp_bias, dtype=np.float32)
         else:
             a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(std)
         if cfg.dtype == "bf16":

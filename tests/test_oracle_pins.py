@@ -563,3 +563,37 @@ def test_speculative_accept_output_law_is_the_target():
                     out = oracle.speculative_accept([p], [None, q], [0, c], u, 2)
                     law[out[1]] += q[c] / (N * N)
         np.testing.assert_allclose(law, p, atol=3.0 / N)
+
+
+# ------------------------------------------------------- learned boundaries --
+# Boundary predictor at inference: logit = w . h_e / RMS(h_e) + b, a boundary where
+# the probability is >= 0.5 (logit >= 0) or the segment reaches max_patch bytes.
+
+LEARNED = TINY.replace(boundary="learned")
+
+
+def _nospace(seed, length):
+    x = synth.make_prompt(seed, length).copy()
+    x[x == oracle.SPACE] = 65
+    return x
+
+
+def test_learned_boundaries_limits():
+    x = _nospace(20, 70)
+    W = synth.make_weights(LEARNED, seed=32)
+    W["bp.w"] = np.zeros_like(W["bp.w"])
+    W["bp.b"] = np.array([-1.0], np.float32)  # never: only the length cap remains
+    assert oracle.trunk(W, LEARNED, x)["q"] == oracle.boundaries(x, LEARNED.max_patch)
+    W["bp.b"] = np.array([1.0], np.float32)  # always
+    assert oracle.trunk(W, LEARNED, x)["q"] == list(range(len(x)))
+
+
+def test_learned_boundaries_are_causal_and_scale_free():
+    W = synth.make_weights(LEARNED, seed=33)
+    x = synth.make_prompt(21, 60)
+    longer = np.concatenate([x, synth.make_prompt(22, 20)])
+    q1 = oracle.trunk(W, LEARNED, x)["q"]
+    q2 = [i for i in oracle.trunk(W, LEARNED, longer)["q"] if i < len(x)]
+    assert q1 == q2 and 0 < len(q1) < len(x)
+    h = oracle.trunk(W, LEARNED, x)["h_e"]
+    np.testing.assert_allclose(oracle.boundary_logits(3.7 * h, W, 0.0), oracle.boundary_logits(h, W, 0.0), atol=1e-12)
