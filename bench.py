@@ -281,10 +281,12 @@ def main():
                         + (f"verified by a next-byte model with layers enc/lm/nt={wl.verifier.n_enc}/"
                            f"{wl.verifier.n_lm}/{wl.verifier.n_nb}, " if ext else "")
                         + (f"sampled at temperature {wl.temperature} top-p {wl.top_p}, " if samp else "")
+                        + (f"learned boundaries (probe scale {model.bp_scale}, bias {model.bp_bias}), "
+                           if model.boundary == "learned" else "")
                         + f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
             "batch": B, "prompt_len": wl.prompt_len, "n": n, "tau": tau, "mode": wl.mode,
             "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32",
-            "logit_gain": args.logit_gain, "max_patch": model.max_patch,
+            "logit_gain": args.logit_gain, "max_patch": model.max_patch, "boundary": model.boundary,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,

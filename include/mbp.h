@@ -68,7 +68,7 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *   max_latents               closed segments per row (latents, BOS excluded).
  *   max_n                     candidates per step, 1..8.
  *   max_patch                 a segment also closes when it reaches this many bytes;
- *                             0 = only the space byte (0x20) closes a segment.
+ *                             0 = only the boundary rule (boundary_mode) closes one.
  *   max_window                MB window rows; 0 = 2*max_patch + max_n - 2 (needs
  *                             max_patch > 0).
  *   max_chunk                 tokens per internal pass of a long commit (0 = 4096).
@@ -89,6 +89,17 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *                             order.  The engine needs one resident block of 512
  *                             threads per compute unit and the handle's stream to
  *                             itself while a launch runs.
+ *   boundary_mode             how segments close (Section 2.2, encoder module).
+ *                             0: after a space byte (0x20).  1: after byte i when
+ *                             the boundary predictor's logit
+ *                             w . h_e[i] / RMS(h_e[i]) + b is >= 0 (probability
+ *                             >= 0.5 at inference, no Gumbel noise); the manifest
+ *                             then ends with bp.w [d_model] and bp.b [1].  Either
+ *                             way a segment also closes at max_patch bytes.  In
+ *                             mode 1 a commit runs the encoder, waits for the
+ *                             logits on the host, then runs the LM module and the
+ *                             NT decoder; capacity checks count every new byte as
+ *                             a possible segment end.
  */
 typedef struct {
   int32_t d_model, n_heads, d_ff;
@@ -99,6 +110,7 @@ typedef struct {
   int32_t window_mode;
   int32_t kv_dtype;
   int32_t no_engine;
+  int32_t boundary_mode;
 } mbp_config;
 
 /* Number of weight tensors of the manifest for cfg, or a negative status. */
@@ -241,6 +253,14 @@ int mbp_read_timing(mbp_handle *h, mbp_kernel_time *out);
 
 /* Current committed length of row r (host value), or a negative status. */
 int32_t mbp_row_length(const mbp_handle *h, int32_t row);
+
+/* Segment ends of row r (Section 2.2, encoder module): the 0-based positions of the
+ * bytes that closed a segment, ascending, among the bytes segmented so far (a byte
+ * the verifier appended stays unsegmented until the next step commits it).  Writes
+ * the first min(count, cap) of them to h_q (host memory, caller-owned; may be NULL
+ * when cap = 0) and returns the count, or MBP_EINVAL for a bad row or buffer.  Host
+ * state only: no device call, no wait. */
+int32_t mbp_row_boundaries(const mbp_handle *h, int32_t row, int32_t *h_q, int32_t cap);
 
 /* Forget all rows and clear an engine timeout (waits for the stream); the handle
  * becomes usable again after a HIP error. */

@@ -39,6 +39,7 @@ class MbpConfig(ctypes.Structure):
         ("max_chunk", ctypes.c_int32),
         ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float), ("attn_scale", ctypes.c_float),
         ("window_mode", ctypes.c_int32), ("kv_dtype", ctypes.c_int32), ("no_engine", ctypes.c_int32),
+        ("boundary_mode", ctypes.c_int32),
     ]
 
 
@@ -88,6 +89,8 @@ def lib():
     L.mbp_get_logits.restype = ctypes.c_int
     L.mbp_row_length.argtypes = [P, ctypes.c_int32]
     L.mbp_row_length.restype = ctypes.c_int32
+    L.mbp_row_boundaries.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32]
+    L.mbp_row_boundaries.restype = ctypes.c_int32
     L.mbp_reset.argtypes = [P]
     L.mbp_reset.restype = ctypes.c_int
     L.mbp_destroy.argtypes = [P]
@@ -128,6 +131,7 @@ def make_config(model, *, max_batch, max_ctx, max_latents=None, max_n=8, max_win
         kv_dtype = F16 if model.dtype == "bf16" else F32
     c.kv_dtype = kv_dtype
     c.no_engine = 0 if engine else 1
+    c.boundary_mode = 1 if getattr(model, "boundary", "space") == "learned" else 0
     return c
 
 
@@ -283,6 +287,17 @@ class Decoder:
         if r < 0:
             raise MbpError(r, "row_length")
         return r
+
+    def row_boundaries(self, row):
+        """Positions of the bytes of ``row`` that closed a segment (numpy int32)."""
+        n = self.L.mbp_row_boundaries(self.h, row, None, 0)
+        if n < 0:
+            raise MbpError(n, "row_boundaries")
+        q = np.zeros(max(n, 1), dtype=np.int32)
+        r = self.L.mbp_row_boundaries(self.h, row, q.ctypes.data_as(ctypes.c_void_p), n)
+        if r < 0:
+            raise MbpError(r, "row_boundaries")
+        return q[:n]
 
     def reset(self):
         self._check(self.L.mbp_reset(self.h))

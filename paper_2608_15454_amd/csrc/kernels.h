@@ -117,6 +117,9 @@ hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const floa
 // Mean of cnt[i] rows of src starting at row lo[i] -> dst[dst_idx[i]]; cnt 0 copies bos.
 hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, const float* bos,
                        float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());
+// Boundary logits of encoder rows: z[i] = w . x / RMS(x) + b[0] with x = src[src_idx[i]].
+hipError_t launch_boundary_logits(const float* src, const int32_t* src_idx, const float* w, const float* b,
+                                  float eps, float* z, int d, int M, hipStream_t st, const Ev& ev = Ev());
 // out[dst_idx[i]] = RMSNorm(src[src_idx[i]]) * gain; null index arrays mean i.
 hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps,
                             float* out, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());

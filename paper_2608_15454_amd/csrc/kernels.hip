@@ -674,6 +674,33 @@ __global__ void pool_kernel(const float* src, const int32_t* lo, const int32_t* 
   }
 }
 
+// One block per row: the dot product with the probe and the sum of squares in one pass.
+__global__ __launch_bounds__(256) void boundary_logits_kernel(const float* src, const int32_t* src_idx,
+                                                              const float* w, const float* b, float eps, float* z,
+                                                              int d) {
+  __shared__ float red[2][4];
+  const int i = blockIdx.x, tid = threadIdx.x;
+  const float* x = src + (size_t)src_idx[i] * d;
+  float ss = 0.f, dot = 0.f;
+  for (int k = tid; k < d; k += 256) {
+    const float v = x[k];
+    ss += v * v;
+    dot += v * w[k];
+  }
+  ss = wave_sum(ss);
+  dot = wave_sum(dot);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = ss;
+    red[1][tid >> 6] = dot;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float sst = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+    const float dt = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+    z[i] = dt / sqrtf(sst / (float)d + eps) + b[0];
+  }
+}
+
 __global__ __launch_bounds__(256) void norm_rows_kernel(const float* src, const int32_t* src_idx, const float* gain,
                                                         float eps, float* out, const int32_t* dst_idx, int d) {
   __shared__ float red[4];
@@ -1193,6 +1220,13 @@ hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, 
                        const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
   return klaunch(pool_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, lo, cnt, bos, dst, dst_idx, d);
+}
+
+hipError_t launch_boundary_logits(const float* src, const int32_t* src_idx, const float* w, const float* b,
+                                  float eps, float* z, int d, int M, hipStream_t st, const Ev& ev) {
+  if (M <= 0) return hipSuccess;
+  return klaunch(boundary_logits_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, src_idx, w, b, eps, z,
+                 d);
 }
 
 hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps, float* out,

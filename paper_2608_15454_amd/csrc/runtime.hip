@@ -137,6 +137,7 @@ bool valid_cfg(const mbp_config* c, std::string* why) {
   if (c->window_mode != 0) return bad("only window_mode 0 is implemented");
   if (c->kv_dtype != MBP_F32 && c->kv_dtype != MBP_BF16 && c->kv_dtype != MBP_F16) return bad("bad kv_dtype");
   if (c->no_engine != 0 && c->no_engine != 1) return bad("no_engine must be 0 or 1");
+  if (c->boundary_mode != 0 && c->boundary_mode != 1) return bad("boundary_mode must be 0 or 1");
   if (!(c->rope_base > 0.f) || !(c->rms_eps >= 0.f) || !std::isfinite(c->attn_scale)) return bad("bad rope_base/rms_eps/attn_scale");
   return true;
 }
@@ -172,6 +173,7 @@ int n_gain_vectors(const mbp_config& c) {
   int n = 2 * (c.n_enc + c.n_lm + c.n_nb) + 1 /*nt_norm*/ + 1 /*bos*/;
   if (c.head == MBP_HEAD_LCA) n += 2 * c.n_mb + 1;
   else n += c.n_mb;
+  if (c.boundary_mode == 1) n += 2;  // bp.w and the one-element bp.b
   return n;
 }
 
@@ -277,6 +279,10 @@ std::vector<WInfo> manifest(const mbp_config& c) {
       m.push_back({p + ".w_down", d, f});
     }
   }
+  if (c.boundary_mode == 1) {  // boundary predictor: logit = w . h_e / RMS(h_e) + b
+    m.push_back({"bp.w", d, 1});
+    m.push_back({"bp.b", 1, 1});
+  }
   return m;
 }
 
@@ -356,6 +362,9 @@ struct mbp_handle {
 
   const void* emb;
   const void* unembed;
+  const float* bp_w = nullptr;  // boundary predictor (boundary_mode 1), float32
+  const float* bp_b = nullptr;
+  float* h_bpz = nullptr;       // pinned [Mc] boundary logits of a commit's new bytes
   const float* bos32;
   const float* g_nt;
   const float* g_mb;
@@ -502,9 +511,11 @@ int run_linear(mbp_handle* h, Linear L, const Scratch& sc, hipStream_t st) {
   return MBP_OK;
 }
 
-int upload(mbp_handle* h, Plan& p, hipStream_t st) {
+// Copies entries from .. p.n of the plan to the device (the earlier ones are there).
+int upload(mbp_handle* h, Plan& p, hipStream_t st, size_t from = 0) {
   if (p.overflow) return fail(h, MBP_ECAPACITY, "internal plan exceeds its capacity");
-  if (p.n) HIPCK(h, hipMemcpyAsync(p.dev, p.host, p.n * 4, hipMemcpyHostToDevice, st));
+  if (p.n > from)
+    HIPCK(h, hipMemcpyAsync(p.dev + from, p.host + from, (p.n - from) * 4, hipMemcpyHostToDevice, st));
   return MBP_OK;
 }
 
@@ -684,6 +695,7 @@ int32_t group_of(const Row& r, int32_t p) {  // L(p): boundaries at or before p
 
 // Number of boundaries a row would have after appending bytes (capacity check).
 int32_t simulate_latents(const mbp_config& c, const Row& r, const uint8_t* add, int n) {
+  if (c.boundary_mode == 1) return (int32_t)r.q.size() + n;  // any new byte may end a segment
   int32_t prev = r.q.empty() ? -1 : r.q.back();
   int32_t K = (int32_t)r.q.size();
   int32_t pos = (int32_t)r.x.size();
@@ -850,6 +862,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
   // with the engine, the next step's window update runs right after the NT decoder
   // on the same stream, prepared in the commit's plan (and the head rows with it)
   const bool pre = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && h->engine;
+  const bool learned = c.boundary_mode == 1;
   h->pre_draft = false;
   size_t first = 0;
   bool first_chunk = true;
@@ -862,27 +875,72 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     int max_kv_e = 0, max_kv_l = 0;
     double kvr_e = 0, kvr_l = 0;
     std::vector<int> rows_in_chunk;
+    // the new bytes: encoder tokens and the rows their outputs go to
     for (size_t it = first; it < last; ++it) {
       const int b = items[it].b;
       Row& r = h->rows[b];
-      if (rows_in_chunk.empty() || rows_in_chunk.back() != b) {
-        rows_in_chunk.push_back(b);
-        if (r.lm_rows == 0) {  // BOS latent of a fresh row
-          tl.push(b, 0, 0, 1, 0);
-          lo_row.push_back(0);
-          cnt.push_back(0);
-          lat_row.push_back(b * s.Kcap);
-          r.lm_rows = 1;
-          r.epoch++;
-          max_kv_l = std::max(max_kv_l, 1);
-          kvr_l += 1;
-        }
-      }
+      if (rows_in_chunk.empty() || rows_in_chunk.back() != b) rows_in_chunk.push_back(b);
       const uint8_t byte = add[b][items[it].idx];
       const int32_t pos = (int32_t)r.x.size();
       r.x.push_back(byte);
+      te.push(b, pos, pos, pos + 1, 0);
+      bytes.push_back(byte);
+      he_row.push_back(b * s.Tcap + pos);
+      max_kv_e = std::max(max_kv_e, pos + 1);
+      kvr_e += pos + 1;
+      // the NT output of the last new byte of a row is its h1 row
+      h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
+    }
+    const int Me = te.size();
+    const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
+    std::vector<int32_t> tiles_e = make_tiles(te);
+    Plan& p = h->plan[0];
+    p.clear();
+    const TokOffs oe = add_toks(p, te);
+    const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_h1 = p.add(h1_dst), o_te = p.add(tiles_e);
+    auto encoder = [&]() -> int {  // embeddings of the new bytes -> h_e rows
+      const Tok tok_e = dev_tok(p, oe, Me);
+      EIo ioe{};
+      ioe.emb = h->emb;
+      ioe.emb_bf16 = h->wdt;
+      ioe.ie = p.at(o_bytes);
+      ioe.xo = he;
+      ioe.oi = p.at(o_he);
+      return run_pass(h, h->enc, h->kv_enc, &h->es_enc, ioe, X, tok_e, nullptr, tiled_e, p.at(o_te),
+                      (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot),
+                      oe.max_ns);
+    };
+    size_t tail = 0;
+    if (learned) {
+      // the boundaries depend on the encoder outputs: run the encoder first and bring
+      // the new bytes' boundary logits to the host (X is free between the encoder
+      // and the NT decoder)
+      RCK(upload(h, p, h->st));
+      tail = p.n;
+      RCK(encoder());
+      OTHER(h, launch_boundary_logits, he, p.at(o_he), h->bp_w, h->bp_b, c.rms_eps, X, s.d, Me, h->st);
+      HIPCK(h, hipMemcpyAsync(h->h_bpz, X, (size_t)Me * 4, hipMemcpyDeviceToHost, h->st));
+      HIPCK(h, hipStreamSynchronize(h->st));
+    }
+    // segmentation: a closed segment becomes an LM token (BOS first on a fresh row)
+    for (size_t it = first; it < last; ++it) {
+      const int k = (int)(it - first);
+      const int b = items[it].b;
+      Row& r = h->rows[b];
+      if ((it == first || items[it - 1].b != b) && r.lm_rows == 0) {  // BOS latent of a fresh row
+        tl.push(b, 0, 0, 1, 0);
+        lo_row.push_back(0);
+        cnt.push_back(0);
+        lat_row.push_back(b * s.Kcap);
+        r.lm_rows = 1;
+        r.epoch++;
+        max_kv_l = std::max(max_kv_l, 1);
+        kvr_l += 1;
+      }
+      const int32_t pos = te.pos[k];
       const int32_t prev = r.q.empty() ? -1 : r.q.back();
-      if (byte == 0x20 || (c.max_patch > 0 && pos - prev >= c.max_patch)) {
+      const bool ends = learned ? h->h_bpz[k] >= 0.f : bytes[k] == 0x20;
+      if (ends || (c.max_patch > 0 && pos - prev >= c.max_patch)) {
         r.q.push_back(pos);
         const int32_t j = (int32_t)r.q.size();
         tl.push(b, j, j, j + 1, 0);
@@ -894,25 +952,13 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
         max_kv_l = std::max(max_kv_l, j + 1);
         kvr_l += j + 1;
       }
-      const int32_t L = (int32_t)r.q.size();  // group of this byte
-      te.push(b, pos, pos, pos + 1, 0);
-      bytes.push_back(byte);
-      he_row.push_back(b * s.Tcap + pos);
-      nt_src.push_back(b * s.Kcap + L);
-      max_kv_e = std::max(max_kv_e, pos + 1);
-      kvr_e += pos + 1;
-      // the NT output of the last new byte of a row is its h1 row
-      h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
+      nt_src.push_back(b * s.Kcap + (int32_t)r.q.size());  // the latent of this byte's group
     }
-    const int Me = te.size(), Ml = tl.size();
-    const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
+    const int Ml = tl.size();
     const bool tiled_l = Ml >= 16 * (int)rows_in_chunk.size();
-    std::vector<int32_t> tiles_e = make_tiles(te), tiles_l = make_tiles(tl);
-    Plan& p = h->plan[0];
-    p.clear();
-    const TokOffs oe = add_toks(p, te), ol = add_toks(p, tl);
-    const size_t o_bytes = p.add(bytes), o_he = p.add(he_row), o_nts = p.add(nt_src), o_lo = p.add(lo_row),
-                 o_cnt = p.add(cnt), o_lat = p.add(lat_row), o_h1 = p.add(h1_dst), o_te = p.add(tiles_e),
+    std::vector<int32_t> tiles_l = make_tiles(tl);
+    const TokOffs ol = add_toks(p, tl);
+    const size_t o_nts = p.add(nt_src), o_lo = p.add(lo_row), o_cnt = p.add(cnt), o_lat = p.add(lat_row),
                  o_tl = p.add(tiles_l);
     const bool pre_here = pre && last == items.size();
     MbPass mp_next;
@@ -924,18 +970,9 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
       o_hr = p.add(head_rows);
       o_md = p.add(mlp_dst);
     }
-    RCK(upload(h, p, h->st));
+    RCK(upload(h, p, h->st, tail));
     const Tok tok_e = dev_tok(p, oe, Me), tok_l = dev_tok(p, ol, Ml);
-
-    // encoder: embeddings of the new bytes -> h_e rows
-    EIo ioe{};
-    ioe.emb = h->emb;
-    ioe.emb_bf16 = h->wdt;
-    ioe.ie = p.at(o_bytes);
-    ioe.xo = he;
-    ioe.oi = p.at(o_he);
-    RCK(run_pass(h, h->enc, h->kv_enc, &h->es_enc, ioe, X, tok_e, nullptr, tiled_e, p.at(o_te),
-                 (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
+    if (!learned) RCK(encoder());
     if (Ml > 0) {
       // LM module on the closed segments: pooled latent inputs -> latent outputs
       OTHER(h, launch_pool, he, p.at(o_lo), p.at(o_cnt), h->bos32, lat_in, p.at(o_lat), s.d, Ml, h->st);
@@ -1285,6 +1322,7 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   }
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_cand, (size_t)s.B * s.nmax, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_len, (size_t)s.B * 4, hipHostMallocDefault);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&h->h_bpz, (size_t)s.Mc * 4, hipHostMallocDefault);
   if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&h->h_cand_dev, h->h_cand, 0);
   if (e == hipSuccess) e = hipHostGetDevicePointer((void**)&h->h_len_dev, h->h_len, 0);
   if (e != hipSuccess) return bail();
@@ -1335,6 +1373,13 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
       w += 4;
       h->mlp.push_back(m);
     }
+  }
+  if (cfg->boundary_mode == 1) {
+    h->bp_w = gain(w++);
+    float* dst = gains + (size_t)gi * s.d;
+    ++gi;
+    if (launch_to_f32(d_weights[w++], h->wdt, dst, 1, h->st) != hipSuccess) h->poisoned = true;
+    h->bp_b = dst;
   }
   auto kvof = [&](size_t ko, size_t vo, int cap) {
     KV k;
@@ -1715,6 +1760,14 @@ extern "C" int32_t mbp_row_length(const mbp_handle* h, int32_t row) {
   return (int32_t)h->rows[row].x.size() + (h->rows[row].bonus >= 0 ? 1 : 0);
 }
 
+extern "C" int32_t mbp_row_boundaries(const mbp_handle* h, int32_t row, int32_t* h_q, int32_t cap) {
+  if (!h || row < 0 || row >= h->batch || cap < 0 || (cap > 0 && !h_q)) return MBP_EINVAL;
+  const std::vector<int32_t>& q = h->rows[row].q;
+  const int32_t n = (int32_t)q.size();
+  if (n > 0 && cap > 0) std::memcpy(h_q, q.data(), (size_t)std::min(n, cap) * 4);
+  return n;
+}
+
 extern "C" int mbp_set_timing(mbp_handle* h, int32_t on) {
   int rc = check_ready(h);
   if (rc) return rc;
@@ -1770,6 +1823,7 @@ extern "C" void mbp_destroy(mbp_handle* h) {
     if (p.host) (void)hipHostFree(p.host);
   if (h->h_cand) (void)hipHostFree(h->h_cand);
   if (h->h_len) (void)hipHostFree(h->h_len);
+  if (h->h_bpz) (void)hipHostFree(h->h_bpz);
   if (h->ev_fork) (void)hipEventDestroy(h->ev_fork);
   if (h->ev_mb) (void)hipEventDestroy(h->ev_mb);
   for (hipEvent_t e : h->events) (void)hipEventDestroy(e);

@@ -57,6 +57,11 @@ class ModelConfig:
     max_patch: int = 16  # length cap of a segment; 0 = pure space rule
     window_mode: int = 0  # 0: MB layers see only the previous+current group window
     boundary: str = "space"  # "space": 0x20 rule; "learned": boundary predictor on h_e
+    # bias of the synthetic boundary probe (learned boundaries); with bp.w ~ N(0, 1/d)
+    # the probe w . h / RMS(h) is N(0, 1) over random directions, so -0.43 ends about
+    # one segment in three bytes when the encoder states vary freely (the tiny models)
+    bp_bias: float = -0.43
+    bp_scale: float = 1.0  # bp.w ~ N(0, bp_scale^2 / d)
 
     def __post_init__(self):
         if self.d_ff == 0:
@@ -120,6 +125,14 @@ WORKLOADS = {
     # the MBP d=1024 model drafts n = 7 candidates, the FxT d=1024 model verifies them
     "extverify_d1024_b1": Workload("extverify_d1024_b1", _D1024_LCA, batch=1, prompt_len=4096, gen_len=1024, n=7,
                                    tau=0.75, mode="external", verifier=D1024_FXT),
+    # segments from the learned boundary predictor instead of the space rule; the probe
+    # is scaled to confident logits (std about 1 on this model's encoder states) and
+    # biased so that about one byte in three ends a segment where decoding runs (the
+    # last 1024 prompt bytes: the states drift with position, and about 45% of the
+    # whole prompt's bytes end one), the paper's 3x compression
+    "learned_d1024_b1": Workload("learned_d1024_b1",
+                                 _D1024_LCA.replace(boundary="learned", bp_scale=4.0, bp_bias=0.84), batch=1,
+                                 prompt_len=4096, gen_len=1024, n=3, tau=0.75),
 }
 
 _BLOCK_PARTS = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "w_gate", "w_up", "w_down")
@@ -158,7 +171,7 @@ def manifest(cfg: ModelConfig):
             out += [(f"mlp.{i}.norm", (d,)), (f"mlp.{i}.w_gate", (dff, d)),
                     (f"mlp.{i}.w_up", (dff, d)), (f"mlp.{i}.w_down", (d, dff))]
     if cfg.boundary == "learned":
-        out += [("bp.w", (d,)), ("bp.b", (1,))]  # boundary predictor: logit = w . h_e + b
+        out += [("bp.w", (d,)), ("bp.b", (1,))]  # boundary predictor: logit = w . h_e / RMS(h_e) + b
     return out
 
 
@@ -180,7 +193,7 @@ def _is_gain(name: str) -> bool:
 
 
 def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logit_gain: float = 1.0,
-                 std: float = 0.02, bp_bias: float = -0.43) -> dict:
+                 std: float = 0.02) -> dict:
     """Draw every parameter tensor, in manifest order.
 
     * matrices, the embedding, ``bos`` and ``unembed``: N(0, std^2), trunk tensors from
@@ -189,10 +202,8 @@ def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logi
     * norm gains: 1, or 1 + U(-gain_jitter, gain_jitter) from ``PCG64(seed + 2)``;
     * ``logit_gain`` multiplies the two final head norms (``nt_norm``, ``mb_norm``),
       which scales every logit and so raises the top-1 probabilities of a random model;
-    * boundary predictor (learned boundaries): ``bp.w`` ~ N(0, 1/d) from the head
-      stream, so that w . h / RMS(h) is about N(0, 1), and ``bp.b`` = ``bp_bias``
-      (default -0.43: about one byte in three ends a segment, the paper's 3x
-      compression).
+    * boundary predictor (learned boundaries): ``bp.w`` ~ N(0, cfg.bp_scale^2 / d) from
+      the head stream and ``bp.b`` = ``cfg.bp_bias``.
     bf16 models get every tensor rounded to bfloat16.
     """
     rng_trunk = np.random.Generator(np.random.PCG64(seed))
@@ -211,9 +222,9 @@ def make_weights(cfg: ModelConfig, seed: int = 0, gain_jitter: float = 0.0, logi
                 a = a * logit_gain
             a = a.astype(np.float32)
         elif name == "bp.w":
-            a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(1.0 / np.sqrt(cfg.d_model))
+            a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(cfg.bp_scale / np.sqrt(cfg.d_model))
         elif name == "bp.b":
-            a = np.full(shape, bp_bias, dtype=np.float32)
+            a = np.full(shape, cfg.bp_bias, dtype=np.float32)
         else:
             a = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(std)
         if cfg.dtype == "bf16":

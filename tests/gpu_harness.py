@@ -102,6 +102,7 @@ def forced_run(dec, W, model, prompts, steps, n, tau, mode=THRESHOLD, tol=None, 
             xs[b] += [int(c) for c in a]
             st.accepted += len(a)
         st.steps += 1
+    st.seqs = xs  # the committed byte sequences the run ended on
     return st
 
 

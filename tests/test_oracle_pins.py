@@ -597,3 +597,13 @@ def test_learned_boundaries_are_causal_and_scale_free():
     assert q1 == q2 and 0 < len(q1) < len(x)
     h = oracle.trunk(W, LEARNED, x)["h_e"]
     np.testing.assert_allclose(oracle.boundary_logits(3.7 * h, W, 0.0), oracle.boundary_logits(h, W, 0.0), atol=1e-12)
+
+
+def test_learned_boundaries_hand_computed():
+    """Constructed states, d = 4, w = (1/4, 0, 0, 0), b = -1/4: the logits by hand,
+    a logit of exactly 0 ends a segment, and max_patch = 2 closes a 2-byte segment."""
+    W = {"bp.w": np.array([0.25, 0.0, 0.0, 0.0]), "bp.b": np.array([-0.25])}
+    h = np.array([[1, 1, 1, 1], [-1, 1, 1, 1], [-1, 1, 1, 1], [4, 0, 0, 0], [-1, 1, 1, 1], [5, 5, 5, 5]], np.float64)
+    np.testing.assert_allclose(oracle.boundary_logits(h, W, 0.0), [0.0, -0.5, -0.5, 0.25, -0.5, 0.0], atol=1e-15)
+    assert oracle.learned_boundaries(h, W, 0, 0.0) == [0, 3, 5]
+    assert oracle.learned_boundaries(h, W, 2, 0.0) == [0, 2, 3, 5]
