@@ -41,4 +41,8 @@ from .model import (  # noqa: F401
     generate_external,
     generate,
     greedy_generate,
+    log_softmax,
+    forward_full,
+    boundary_loss,
+    forward_losses,
 )

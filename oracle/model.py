@@ -482,3 +482,61 @@ def greedy_generate(W, cfg, prompt, n_new):
         out.append(b)
         x.append(b)
     return np.array(out, dtype=np.uint8)
+
+
+# ------------------------------------------------------ full-sequence forward --
+
+def log_softmax(logits):
+    """log of the softmax over the last axis (the log-sum-exp taken about the max)."""
+    l = np.asarray(logits, np.float64)
+    m = l.max(axis=-1, keepdims=True)
+    return l - m - np.log(np.sum(np.exp(l - m), axis=-1, keepdims=True))
+
+
+def forward_full(W, cfg, x):
+    """Training-form forward over a whole byte sequence (Section 3, the MB head under
+    the LCA mask; Section 2.2 modules): the trunk, then the MB layers over every byte
+    at once with the full-sequence LCA mask (each byte sees its own group so far and
+    the whole previous group), inputs z_{L(i)} = h'[L(i)] + LMin[L(i)].
+
+    Returns the next-byte logits [T, 256] (row t predicts x_{t+1}) and the MB logits
+    [T, 256] (row t predicts x_{t+2}), plus the trunk.
+    """
+    tr = trunk(W, cfg, x)
+    T = len(x)
+    l_nt = head_logits(tr["h1"], W["nt_norm"], W, cfg.rms_eps)
+    out = {"trunk": tr, "nt": l_nt, "mb": None}
+    if cfg.head == "lca" and cfg.n_mb > 0:
+        z = tr["h_lm"] + tr["LMin"]
+        h2 = stack(z[tr["L"]], W, "mb", cfg.n_mb, lca_mask(tr["L"]), np.arange(T), cfg)
+        out["mb"] = head_logits(h2, W["mb_norm"], W, cfg.rms_eps)
+    return out
+
+
+def boundary_loss(k, T, alpha, beta):
+    """L_BP of the encoder-module paragraph: zero while the boundary rate k/T lies in
+    [beta, alpha], else its distance to the nearer bound."""
+    r = k / T
+    return max(r - alpha, 0.0) + max(beta - r, 0.0)
+
+
+def forward_losses(W, cfg, x, lam0=1.0, lam1=1.0, lam2=1.0, alpha=1.0, beta=0.0):
+    """The training objective of Section 3 (next-byte plus multi-byte terms) plus
+    lambda_2 L_BP on one sequence: per-position
+    negative log-likelihoods of the next-byte head (targets x_{t+1}, t < T-1) and of
+    the MB head (targets x_{t+2}, t < T-2), their sums, L_LM = lam0 * sum_nt +
+    lam1 * sum_mb, L_BP with k = the number of boundaries, and L_LM + lam2 * L_BP.
+    Sums, not means, as the equation is written."""
+    x = np.asarray(x, np.int64)
+    T = len(x)
+    f = forward_full(W, cfg, x)
+    nll_nt = -np.take_along_axis(log_softmax(f["nt"][: T - 1]), x[1:, None], axis=1)[:, 0]
+    if f["mb"] is not None and T > 2:
+        nll_mb = -np.take_along_axis(log_softmax(f["mb"][: T - 2]), x[2:, None], axis=1)[:, 0]
+    else:
+        nll_mb = np.zeros(0)
+    s_nt, s_mb = float(np.sum(nll_nt)), float(np.sum(nll_mb))
+    l_lm = lam0 * s_nt + lam1 * s_mb
+    l_bp = boundary_loss(len(f["trunk"]["q"]), T, alpha, beta)
+    return {"nll_nt": nll_nt, "nll_mb": nll_mb, "sum_nt": s_nt, "sum_mb": s_mb, "l_lm": l_lm, "l_bp": l_bp,
+            "total": l_lm + lam2 * l_bp, "k": len(f["trunk"]["q"]), "forward": f}

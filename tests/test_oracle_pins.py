@@ -607,3 +607,69 @@ def test_learned_boundaries_hand_computed():
     np.testing.assert_allclose(oracle.boundary_logits(h, W, 0.0), [0.0, -0.5, -0.5, 0.25, -0.5, 0.0], atol=1e-15)
     assert oracle.learned_boundaries(h, W, 0, 0.0) == [0, 3, 5]
     assert oracle.learned_boundaries(h, W, 2, 0.0) == [0, 2, 3, 5]
+
+
+# ------------------------------------------------------ full-sequence forward --
+
+MB2 = TINY.replace(n_mb=2)
+
+
+def test_log_softmax_is_scipys():
+    from scipy.special import log_softmax as ref
+    rng = np.random.default_rng(5)
+    l = rng.normal(size=(7, 256)) * 30
+    np.testing.assert_allclose(oracle.log_softmax(l), ref(l, axis=-1), atol=1e-12)
+
+
+def test_forward_losses_uniform_logits_closed_form():
+    """A zero unembedding gives all-zero logits: every NLL is log 256."""
+    W = synth.make_weights(TINY, seed=40)
+    W["unembed"] = np.zeros_like(W["unembed"])
+    x = synth.make_prompt(30, 40)
+    r = oracle.forward_losses(W, TINY, x, lam0=0.5, lam1=2.0, lam2=0.0)
+    assert len(r["nll_nt"]) == 39 and len(r["nll_mb"]) == 38
+    np.testing.assert_allclose(r["nll_nt"], np.log(256.0), atol=1e-12)
+    np.testing.assert_allclose(r["nll_mb"], np.log(256.0), atol=1e-12)
+    np.testing.assert_allclose(r["l_lm"], (0.5 * 39 + 2.0 * 38) * np.log(256.0), rtol=1e-12)
+
+
+def test_boundary_loss_closed_forms():
+    assert oracle.boundary_loss(30, 100, 0.4, 0.2) == 0.0
+    assert abs(oracle.boundary_loss(50, 100, 0.4, 0.2) - 0.1) < 1e-15
+    assert abs(oracle.boundary_loss(10, 100, 0.4, 0.2) - 0.1) < 1e-15
+    W = synth.make_weights(TINY, seed=41)
+    x = synth.make_prompt(31, 60)
+    r = oracle.forward_losses(W, TINY, x, lam2=3.0, alpha=0.05, beta=0.0)
+    assert r["k"] == len(oracle.boundaries(x, TINY.max_patch))
+    np.testing.assert_allclose(r["total"], r["l_lm"] + 3.0 * (r["k"] / 60 - 0.05), rtol=1e-12)
+
+
+def test_forward_nll_is_the_definition():
+    """One position by hand: -log of the softmax probability of the target byte."""
+    W = oracle.to_float64(synth.make_weights(TINY, seed=42, logit_gain=20.0))
+    x = synth.make_prompt(32, 30)
+    r = oracle.forward_losses(W, TINY, x)
+    l = r["forward"]["nt"][11]
+    p = np.exp(l - l.max()) / np.sum(np.exp(l - l.max()))
+    np.testing.assert_allclose(r["nll_nt"][11], -np.log(p[x[12]]), rtol=1e-12)
+    l = r["forward"]["mb"][11]
+    p = np.exp(l - l.max()) / np.sum(np.exp(l - l.max()))
+    np.testing.assert_allclose(r["nll_mb"][11], -np.log(p[x[13]]), rtol=1e-12)
+
+
+def test_forward_rows_equal_decode_rows():
+    """Every position of the full-sequence forward is the decode step on the prefix:
+    next-byte row t = the step's row 1 after x[:t+1]; MB row t = its row 2 with the
+    MB layers run over the whole sequence (window mode 1).  With two MB layers the
+    windowed step (mode 0) differs, so the check tells the two masks apart."""
+    W = oracle.to_float64(synth.make_weights(MB2, seed=43, gain_jitter=0.2))
+    x = synth.make_prompt(33, 48)
+    f = oracle.forward_full(W, MB2, x)
+    full = MB2.replace(window_mode=1)
+    differs = False
+    for t in (0, 5, 17, 30, 47):
+        st = oracle.step_logits(W, full, x[: t + 1], 2)
+        np.testing.assert_allclose(f["nt"][t], st[0], atol=1e-10)
+        np.testing.assert_allclose(f["mb"][t], st[1], atol=1e-10)
+        differs |= np.max(np.abs(oracle.step_logits(W, MB2, x[: t + 1], 2)[1] - st[1])) > 1e-6
+    assert differs
