@@ -254,6 +254,41 @@ int mbp_read_timing(mbp_handle *h, mbp_kernel_time *out);
 /* Current committed length of row r (host value), or a negative status. */
 int32_t mbp_row_length(const mbp_handle *h, int32_t row);
 
+/* Weights and bounds of the training objective: L_LM of Section 3 (lambda0 times the
+ * next-byte negative log-likelihoods plus lambda1 times the MB head's, both summed
+ * over positions) plus lambda2 times L_BP of Section 2.2 (encoder module), the
+ * distance of the boundary rate k/T to the interval [beta, alpha]. */
+typedef struct {
+  float lambda0, lambda1, lambda2;
+  float alpha, beta;
+} mbp_loss_params;
+
+/* Bytes of the device workspace mbp_forward needs for a sequence of T bytes (0 for
+ * an invalid config or T < 1). */
+size_t mbp_forward_workspace_bytes(const mbp_config *cfg, int32_t T);
+
+/* Training-form forward over one whole sequence (Section 3; LCA head, or no MB head):
+ * encoder, segmentation, LM module and next-byte decoder over the T bytes, then the
+ * MB layers over every position at once under the full-sequence LCA mask (a position
+ * sees its own group up to itself and the whole previous group; the training mask,
+ * which the decode step's window reproduces exactly when n_mb = 1), and both heads
+ * through the shared unembedding at every position.
+ *   h_bytes   host [T] bytes, T <= max_ctx (its segments count toward max_latents).
+ *   lp        loss weights and bounds.
+ *   d_work    caller-owned device workspace of mbp_forward_workspace_bytes(cfg, T)
+ *             bytes, 256-byte aligned; work_bytes its size.
+ *   d_nll     device float [2, T]: row 0 the next-byte NLL of x_{t+1} at t < T-1,
+ *             row 1 the MB head's NLL of x_{t+2} at t < T-2; other entries 0 (all of
+ *             row 1 without an MB head).
+ *   d_loss    device float [6]: sum of row 0, sum of row 1, L_LM, L_BP, L_LM +
+ *             lambda2 L_BP, and k (the number of segment ends).
+ * Uses batch row 0's caches and the handle's scratch: every row is forgotten (as
+ * after mbp_reset) when it returns, and the call waits for its work to finish.
+ * MBP_EINVAL for bad arguments or an MLP head, MBP_ECAPACITY for a sequence beyond
+ * the capacities or a short workspace. */
+int mbp_forward(mbp_handle *h, const uint8_t *h_bytes, int32_t T, const mbp_loss_params *lp, void *d_work,
+                size_t work_bytes, float *d_nll, float *d_loss);
+
 /* Segment ends of row r (Section 2.2, encoder module): the 0-based positions of the
  * bytes that closed a segment, ascending, among the bytes segmented so far (a byte
  * the verifier appended stays unsegmented until the next step commits it).  Writes

@@ -29,6 +29,12 @@ def lib_path() -> str:
     return os.path.join(_HERE, "libmbp.so")
 
 
+class LossParams(ctypes.Structure):
+    """Mirror of mbp_loss_params."""
+    _fields_ = [("lambda0", ctypes.c_float), ("lambda1", ctypes.c_float), ("lambda2", ctypes.c_float),
+                ("alpha", ctypes.c_float), ("beta", ctypes.c_float)]
+
+
 class MbpConfig(ctypes.Structure):
     _fields_ = [
         ("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("d_ff", ctypes.c_int32),
@@ -91,6 +97,10 @@ def lib():
     L.mbp_row_length.restype = ctypes.c_int32
     L.mbp_row_boundaries.argtypes = [P, ctypes.c_int32, P, ctypes.c_int32]
     L.mbp_row_boundaries.restype = ctypes.c_int32
+    L.mbp_forward_workspace_bytes.argtypes = [P, ctypes.c_int32]
+    L.mbp_forward_workspace_bytes.restype = ctypes.c_size_t
+    L.mbp_forward.argtypes = [P, P, ctypes.c_int32, P, P, ctypes.c_size_t, P, P]
+    L.mbp_forward.restype = ctypes.c_int
     L.mbp_reset.argtypes = [P]
     L.mbp_reset.restype = ctypes.c_int
     L.mbp_destroy.argtypes = [P]
@@ -213,6 +223,28 @@ class Decoder:
         lens = np.array([len(p) for p in prompts], dtype=np.int32)
         self._check(self.L.mbp_prefill(self.h, flat.ctypes.data, lens.ctypes.data, len(prompts)))
         self.batch = len(prompts)
+
+    def forward(self, seq, lam0=1.0, lam1=1.0, lam2=1.0, alpha=1.0, beta=0.0, work=None):
+        """Full-sequence forward of one byte sequence (mbp_forward).  Returns device
+        tensors nll [2, T] and loss [6]; every row is forgotten afterwards.  ``work``:
+        a device uint8 tensor to reuse as the workspace (allocated when too small)."""
+        torch = self.torch
+        seq = np.ascontiguousarray(seq, dtype=np.uint8)
+        T = len(seq)
+        need = self.L.mbp_forward_workspace_bytes(ctypes.byref(self.cfg), T)
+        if need == 0:
+            raise MbpError(EINVAL, "forward workspace size")
+        if work is None or work.numel() < need:
+            work = torch.empty(need, dtype=torch.uint8, device=self.device)
+        self.fwork = work
+        nll = torch.zeros((2, T), dtype=torch.float32, device=self.device)
+        loss = torch.zeros((6,), dtype=torch.float32, device=self.device)
+        lp = LossParams(lam0, lam1, lam2, alpha, beta)
+        self._check(self.L.mbp_forward(self.h, seq.ctypes.data, T, ctypes.byref(lp),
+                                       ctypes.c_void_p(work.data_ptr()), work.numel(),
+                                       ctypes.c_void_p(nll.data_ptr()), ctypes.c_void_p(loss.data_ptr())))
+        self.batch = 0
+        return nll, loss
 
     def decode_step(self, n, tau, mode=THRESHOLD):
         """Enqueue one step; returns device views (cand [B,n], prob [B,n], accept_len [B])."""

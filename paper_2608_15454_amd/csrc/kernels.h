@@ -120,6 +120,16 @@ hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, 
 // Boundary logits of encoder rows: z[i] = w . x / RMS(x) + b[0] with x = src[src_idx[i]].
 hipError_t launch_boundary_logits(const float* src, const int32_t* src_idx, const float* w, const float* b,
                                   float eps, float* z, int d, int M, hipStream_t st, const Ev& ev = Ev());
+// Negative log-likelihood of each row's target: nll[i] = logsumexp(logits[i, :256]) -
+// logits[i, target[i]] for i < M, nll[i] = 0 for M <= i < M_total; one wave per row.
+hipError_t launch_nll(const float* logits, const int32_t* target, float* nll, int M, int M_total, hipStream_t st,
+                      const Ev& ev = Ev());
+// Loss summary of a full-sequence forward in one block, summed in a fixed order:
+// out = {sum nll_nt[0..m_nt), sum nll_mb[0..m_mb), L_LM = lam0 sum_nt + lam1 sum_mb,
+// L_BP = max(k/T - alpha, 0) + max(beta - k/T, 0), L_LM + lam2 L_BP, k}.
+hipError_t launch_losses(const float* nll_nt, int m_nt, const float* nll_mb, int m_mb, int k, int T, float lam0,
+                         float lam1, float lam2, float alpha, float beta, float* out, hipStream_t st,
+                         const Ev& ev = Ev());
 // out[dst_idx[i]] = RMSNorm(src[src_idx[i]]) * gain; null index arrays mean i.
 hipError_t launch_norm_rows(const float* src, const int32_t* src_idx, const float* gain, float eps,
                             float* out, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev = Ev());

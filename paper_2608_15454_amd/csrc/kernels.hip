@@ -562,13 +562,30 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
   __shared__ float Ks[64][DH + 1];
   __shared__ float Vs[64][DH + 1];
   __shared__ float Ps[64][65];
+  __shared__ int32_t Gs[64];
   const int r = tid >> 2, cq = tid & 3;
   float q[DH];
+  const int rr = r < cnt ? r : 0;
   {
-    const int rr = r < cnt ? r : 0;
     const float* qp = a.Q + (size_t)(t0 + rr) * a.ldq + h * DH;
 #pragma unroll
     for (int e = 0; e < DH; ++e) q[e] = qp[e] * a.scale;
+  }
+  // LCA mask (group table set): slot j is visible to row i when its group is the
+  // row's own or the one before (slots ascend in group, so j <= i gives the rest);
+  // the tile's keys start at the first slot of the group before its first row's
+  const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
+  const int g_row = gt != nullptr ? a.tok.grp[t0 + rr] : 0;
+  int k_begin = 0;
+  if (gt != nullptr) {
+    const int need = a.tok.grp[t0] - 1;
+    int lo = 0, hi = slot0;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (gt[mid] < need) lo = mid + 1;
+      else hi = mid;
+    }
+    k_begin = lo;
   }
   const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH;
   const KV* kb = reinterpret_cast<const KV*>(a.kc) + base;
@@ -577,13 +594,14 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
 #pragma unroll
   for (int od = 0; od < OD; ++od) o[od] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
-  for (int k0 = 0; k0 < kvmax; k0 += 64) {
+  for (int k0 = k_begin; k0 < kvmax; k0 += 64) {
     __syncthreads();
     for (int idx = tid; idx < 64 * DH; idx += 256) {
       const int c = idx / DH, e = idx - c * DH, j = k0 + c;
       Ks[c][e] = j < kvmax ? WT<KV>::ld(kb, (size_t)j * DH + e) : 0.f;
       Vs[c][e] = j < kvmax ? WT<KV>::ld(vb, (size_t)j * DH + e) : 0.f;
     }
+    if (tid < 64) Gs[tid] = (gt != nullptr && k0 + tid < kvmax) ? gt[k0 + tid] : 0;
     __syncthreads();
     float sc[16];
     float mx = -INFINITY;
@@ -591,7 +609,7 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
     for (int cc = 0; cc < 16; ++cc) {
       const int c = cq * 16 + cc, j = k0 + c;
       float sv = -INFINITY;
-      if (j < kvmax && j <= slot0 + r) {
+      if (j < kvmax && j <= slot0 + r && Gs[c] >= g_row - 1) {
         float dot = 0.f;
 #pragma unroll
         for (int e = 0; e < DH; ++e) dot += q[e] * Ks[c][e];
@@ -671,6 +689,53 @@ __global__ void pool_kernel(const float* src, const int32_t* lo, const int32_t* 
       v = s / (float)c;
     }
     dst[di + k] = v;
+  }
+}
+
+// One wave per row of 256 logits: four per lane.
+__global__ __launch_bounds__(256) void nll_kernel(const float* logits, const int32_t* target, float* nll, int M,
+                                                  int M_total) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= M_total) return;
+  if (i >= M) {  // no target: the row's entry is 0
+    if (lane == 0) nll[i] = 0.f;
+    return;
+  }
+  const float4 v = reinterpret_cast<const float4*>(logits + (size_t)i * 256)[lane];
+  const float mx = group_max<64>(fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+  const float se = group_sum<64>(expf(v.x - mx) + expf(v.y - mx) + expf(v.z - mx) + expf(v.w - mx));
+  if (lane == 0) nll[i] = mx + logf(se) - logits[(size_t)i * 256 + target[i]];
+}
+
+// One block: each thread sums a strided share, then a tree over the block (the same
+// order on every call).
+__global__ __launch_bounds__(256) void losses_kernel(const float* nll_nt, int m_nt, const float* nll_mb, int m_mb,
+                                                     int k, int T, float lam0, float lam1, float lam2, float alpha,
+                                                     float beta, float* out) {
+  __shared__ float red[2][4];
+  const int tid = threadIdx.x;
+  float a = 0.f, b = 0.f;
+  for (int i = tid; i < m_nt; i += 256) a += nll_nt[i];
+  for (int i = tid; i < m_mb; i += 256) b += nll_mb[i];
+  a = wave_sum(a);
+  b = wave_sum(b);
+  if ((tid & 63) == 0) {
+    red[0][tid >> 6] = a;
+    red[1][tid >> 6] = b;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    const float s_nt = (red[0][0] + red[0][1]) + (red[0][2] + red[0][3]);
+    const float s_mb = (red[1][0] + red[1][1]) + (red[1][2] + red[1][3]);
+    const float rate = (float)k / (float)T;
+    const float l_lm = lam0 * s_nt + lam1 * s_mb;
+    const float l_bp = fmaxf(rate - alpha, 0.f) + fmaxf(beta - rate, 0.f);
+    out[0] = s_nt;
+    out[1] = s_mb;
+    out[2] = l_lm;
+    out[3] = l_bp;
+    out[4] = l_lm + lam2 * l_bp;
+    out[5] = (float)k;
   }
 }
 
@@ -1220,6 +1285,19 @@ hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, 
                        const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
   return klaunch(pool_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, lo, cnt, bos, dst, dst_idx, d);
+}
+
+hipError_t launch_nll(const float* logits, const int32_t* target, float* nll, int M, int M_total, hipStream_t st,
+                      const Ev& ev) {
+  if (M_total <= 0) return hipSuccess;
+  return klaunch(nll_kernel, dim3((M_total + 3) / 4), dim3(256), 0, st, ev.start, ev.stop, logits, target, nll,
+                 std::max(M, 0), M_total);
+}
+
+hipError_t launch_losses(const float* nll_nt, int m_nt, const float* nll_mb, int m_mb, int k, int T, float lam0,
+                         float lam1, float lam2, float alpha, float beta, float* out, hipStream_t st, const Ev& ev) {
+  return klaunch(losses_kernel, dim3(1), dim3(256), 0, st, ev.start, ev.stop, nll_nt, m_nt, nll_mb, m_mb, k, T, lam0,
+                 lam1, lam2, alpha, beta, out);
 }
 
 hipError_t launch_boundary_logits(const float* src, const int32_t* src_idx, const float* w, const float* b,

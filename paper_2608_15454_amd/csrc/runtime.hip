@@ -365,6 +365,7 @@ struct mbp_handle {
   const float* bp_w = nullptr;  // boundary predictor (boundary_mode 1), float32
   const float* bp_b = nullptr;
   float* h_bpz = nullptr;       // pinned [Mc] boundary logits of a commit's new bytes
+  float* fwd_h = nullptr;       // set during mbp_forward: NT outputs of every position go here
   const float* bos32;
   const float* g_nt;
   const float* g_mb;
@@ -888,8 +889,10 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
       he_row.push_back(b * s.Tcap + pos);
       max_kv_e = std::max(max_kv_e, pos + 1);
       kvr_e += pos + 1;
-      // the NT output of the last new byte of a row is its h1 row
-      h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
+      // the NT output of the last new byte of a row is its h1 row (in a full-sequence
+      // forward, every NT output is kept, at its position)
+      if (h->fwd_h) h1_dst.push_back(pos);
+      else h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
     }
     const int Me = te.size();
     const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
@@ -995,7 +998,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     ion.xb = he;
     ion.ib = p.at(o_he);
     ion.xo = X;
-    ion.xo2 = h->rows_base();
+    ion.xo2 = h->fwd_h ? h->fwd_h : h->rows_base();
     ion.oi2 = p.at(o_h1);
     RCK(run_pass(h, h->nt, h->kv_nt, &h->es_nt, ion, X, tok_e, nullptr, tiled_e, p.at(o_te),
                  (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
@@ -1423,9 +1426,7 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   return MBP_OK;
 }
 
-extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t* h_lens, int32_t batch) {
-  int rc = check_ready(h);
-  if (rc) return rc;
+int prefill_rows(mbp_handle* h, const uint8_t* h_bytes, const int32_t* h_lens, int32_t batch, bool fork_mb) {
   const Sizes& s = h->sz;
   if (!h_bytes || !h_lens || batch < 1 || batch > s.B) return fail(h, MBP_EINVAL, "bad prefill arguments");
   std::vector<std::vector<uint8_t>> add(batch);
@@ -1448,7 +1449,174 @@ extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t*
   for (int b = 0; b < batch; ++b) act[b] = 1;
   HIPCK(h, hipMemcpyAsync(h->R<int32_t>(h->rg.active), act.data(), s.B * 4, hipMemcpyHostToDevice, h->st));
   HIPCK(h, hipStreamSynchronize(h->st));
-  return commit(h, add, true);
+  return commit(h, add, fork_mb);
+}
+
+extern "C" int mbp_prefill(mbp_handle* h, const uint8_t* h_bytes, const int32_t* h_lens, int32_t batch) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  return prefill_rows(h, h_bytes, h_lens, batch, true);
+}
+
+// ------------------------------------------------------ full-sequence forward --
+
+// Regions of the caller's forward workspace for a sequence of T bytes.
+struct FwdLayout {
+  size_t h, logits, tgt, grp, kv_k, kv_v, total;
+};
+
+FwdLayout fwd_layout(const mbp_config& c, int32_t T) {
+  const Sizes s = sizes_of(c);
+  FwdLayout f{};
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off += (bytes + 255) / 256 * 256;
+    return o;
+  };
+  f.h = take((size_t)T * s.d * 4);       // NT outputs, then MB outputs, of every position
+  f.logits = take((size_t)T * 256 * 4);  // logits of one head
+  f.tgt = take((size_t)2 * T * 4);       // targets x_{t+1}, then x_{t+2}
+  f.grp = take((size_t)T * 4);           // group of every position (the LCA mask)
+  const size_t kv = (size_t)c.n_mb * T * s.d * s.es;
+  f.kv_k = take(kv);
+  f.kv_v = take(kv);
+  f.total = off;
+  return f;
+}
+
+// Forget every row (the forward leaves no decode state behind).
+void forget_rows(mbp_handle* h) {
+  h->rows.assign(h->sz.B, Row());
+  h->batch = 0;
+  h->pending = false;
+  h->pre_draft = false;
+  h->last_n = 0;
+  h->n_hint = std::min(3, h->cfg.max_n);
+}
+
+// logits[0..M) = unembed(RMSNorm(x[0..M)) * gain), in passes of at most Mc rows.
+int unembed_rows(mbp_handle* h, const float* x, int M, const float* gain, float* logits) {
+  const Sizes& s = h->sz;
+  for (int r0 = 0; r0 < M; r0 += s.Mc) {
+    Linear un{};
+    un.X = x + (size_t)r0 * s.d; un.ldx = s.d; un.M = std::min(s.Mc, M - r0); un.K = s.d; un.N = 256;
+    un.gain = gain; un.eps = h->cfg.rms_eps;
+    un.mats.m[0] = h->unembed; un.mats.rows = 256; un.mats.mode = MAT_SINGLE;
+    un.epi.kind = EPI_STORE; un.epi.Y = logits + (size_t)r0 * 256; un.epi.ldy = 256;
+    RCK(run_linear(h, un, h->sc_main, h->st));
+  }
+  return MBP_OK;
+}
+
+extern "C" size_t mbp_forward_workspace_bytes(const mbp_config* cfg, int32_t T) {
+  if (!valid_cfg(cfg, nullptr) || T < 1) return 0;
+  return fwd_layout(*cfg, T).total;
+}
+
+extern "C" int mbp_forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, const mbp_loss_params* lp,
+                           void* d_work, size_t work_bytes, float* d_nll, float* d_loss) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  const Sizes& s = h->sz;
+  const mbp_config& c = h->cfg;
+  if (!h_bytes || !lp || !d_work || !d_nll || !d_loss || T < 1) return fail(h, MBP_EINVAL, "bad forward arguments");
+  if (c.head != MBP_HEAD_LCA && c.n_mb > 0)
+    return fail(h, MBP_EINVAL, "the full-sequence forward covers the LCA head only");
+  if (T > s.Tcap) return fail(h, MBP_ECAPACITY, "sequence exceeds max_ctx");
+  const FwdLayout fl = fwd_layout(c, T);
+  if (work_bytes < fl.total) return fail(h, MBP_ECAPACITY, "forward workspace too small");
+  if (reinterpret_cast<uintptr_t>(d_work) % 256 != 0)
+    return fail(h, MBP_EINVAL, "forward workspace must be 256-byte aligned");
+  char* wk = static_cast<char*>(d_work);
+  float* hall = reinterpret_cast<float*>(wk + fl.h);
+  float* logits = reinterpret_cast<float*>(wk + fl.logits);
+  int32_t* tgt = reinterpret_cast<int32_t*>(wk + fl.tgt);
+  int32_t* grp = reinterpret_cast<int32_t*>(wk + fl.grp);
+
+  // trunk: encoder, segmentation, LM module and NT decoder as a prefill of row 0,
+  // with every NT output kept
+  h->fwd_h = hall;
+  rc = prefill_rows(h, h_bytes, &T, 1, false);
+  h->fwd_h = nullptr;
+  if (rc) {
+    forget_rows(h);
+    return rc;
+  }
+  const Row& r = h->rows[0];
+  const int K = (int)r.q.size();
+  std::vector<int32_t> tg((size_t)2 * T, 0), G(T);
+  for (int t = 0; t < T; ++t) {
+    if (t + 1 < T) tg[t] = h_bytes[t + 1];
+    if (t + 2 < T) tg[(size_t)T + t] = h_bytes[t + 2];
+    G[t] = group_of(r, t);
+  }
+  auto done = [&](int code) {
+    (void)hipStreamSynchronize(h->st);  // the host arrays below are read by queued copies
+    forget_rows(h);
+    return code;
+  };
+  if (hipMemcpyAsync(tgt, tg.data(), tg.size() * 4, hipMemcpyHostToDevice, h->st) != hipSuccess ||
+      hipMemcpyAsync(grp, G.data(), G.size() * 4, hipMemcpyHostToDevice, h->st) != hipSuccess)
+    return done(fail(h, MBP_EHIP, "forward upload failed"));
+
+  // next-byte head on every position (targets x_{t+1})
+  rc = unembed_rows(h, hall, T, h->g_nt, logits);
+  if (rc) return done(rc);
+  if (launch_nll(logits, tgt, d_nll, T - 1, T, h->st) != hipSuccess) return done(fail(h, MBP_EHIP, "nll launch"));
+
+  // MB head: the MB layers over every position at once under the full-sequence LCA
+  // mask, inputs z_{L(i)} = h'[L(i)] + LMin[L(i)] (targets x_{t+2})
+  const bool mb = c.n_mb > 0;
+  if (mb) {
+    KV kvf;
+    kvf.k = wk + fl.kv_k;
+    kvf.v = wk + fl.kv_v;
+    kvf.cap = T;
+    kvf.b_stride = (int64_t)s.H * T * s.dh;
+    kvf.layer_stride = kvf.b_stride;
+    const Scratch& sc = h->sc_main;
+    Plan& p = h->plan[0];
+    for (int c0 = 0; c0 < T; c0 += s.Mc) {
+      const int c1 = std::min(T, c0 + s.Mc);
+      if (c0 > 0 && hipStreamSynchronize(h->st) != hipSuccess)  // plan buffer reuse
+        return done(fail(h, MBP_EHIP, "forward synchronize"));
+      Toks tm;
+      std::vector<int32_t> zrow, orow;
+      double kvr = 0;
+      for (int i = c0; i < c1; ++i) {
+        tm.push(0, i, i, i + 1, G[i]);
+        zrow.push_back(G[i]);  // latent row of group G[i] in batch row 0
+        orow.push_back(i);
+        kvr += i + 1 - (G[i] >= 1 ? (G[i] >= 2 ? r.q[G[i] - 2] : 0) : 0);
+      }
+      const std::vector<int32_t> tiles = make_tiles(tm);
+      p.clear();
+      const TokOffs om = add_toks(p, tm);
+      const size_t o_z = p.add(zrow), o_o = p.add(orow), o_t = p.add(tiles);
+      rc = upload(h, p, h->st);
+      if (rc) return done(rc);
+      EIo io{};
+      io.xa = h->R<float>(h->rg.lat_out);
+      io.ia = p.at(o_z);
+      io.xb = h->R<float>(h->rg.lat_in);
+      io.ib = p.at(o_z);
+      io.xo = hall;
+      io.oi = p.at(o_o);
+      const int M = c1 - c0;
+      rc = run_pass(h, h->mb, kvf, nullptr, io, sc.X, dev_tok(p, om, M), grp, M >= 16, p.at(o_t),
+                    (int)tiles.size() / 2, c1, kvr, sc, h->st, p.at(om.first), p.at(om.first_slot), om.max_ns);
+      if (rc) return done(rc);
+    }
+    rc = unembed_rows(h, hall, T, h->g_mb, logits);
+    if (rc) return done(rc);
+  }
+  if (launch_nll(logits, tgt + T, d_nll + T, mb ? T - 2 : 0, T, h->st) != hipSuccess)
+    return done(fail(h, MBP_EHIP, "nll launch"));
+  if (launch_losses(d_nll, std::max(T - 1, 0), d_nll + T, mb ? std::max(T - 2, 0) : 0, K, T, lp->lambda0,
+                    lp->lambda1, lp->lambda2, lp->alpha, lp->beta, d_loss, h->st) != hipSuccess)
+    return done(fail(h, MBP_EHIP, "loss launch"));
+  return done(MBP_OK);
 }
 
 // Commits every row's pending bonus byte (external verification), so that the caches
