@@ -33,8 +33,8 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1024)
-    ap.add_argument("--warmup", type=int, default=16)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 1024; forward workloads 20)")
+    ap.add_argument("--warmup", type=int, default=None, help="untimed steps (default 16; forward workloads 3)")
     ap.add_argument("--workload", default="lca_d1024_b1")
     ap.add_argument("--n", type=int, default=None)
     ap.add_argument("--tau", type=float, default=None)
@@ -112,6 +112,125 @@ def run_external(dec, ver, steps, n, threshold):
         ver.accept()
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 / fp16 matrix cores, vendor figure
+VALU_FP32_PEAK_TFLOPS = 157.3   # MI355X fp32 vector
+
+
+def forward_flops(model, T, q):
+    """Algorithmic flops of one full-sequence forward: (linear, attention).  Linear:
+    2 per weight per row (encoder, NT and MB layers on T rows, the LM module on the
+    K+1 latent rows, the unembedding twice on T rows).  Attention: 4 d per visible
+    (query, key) pair (scores and the weighted sum): causal in the encoder, LM module
+    and NT decoder; under the LCA mask a position sees its own group up to itself and
+    the previous group."""
+    d, dff = model.d_model, model.d_ff
+    per_layer = 4 * d * d + 3 * d * dff
+    K1 = len(q) + 1
+    linear = 2.0 * per_layer * (T * (model.n_enc + model.n_nb + model.n_mb) + K1 * model.n_lm) + 2 * 2.0 * T * 256 * d
+    starts = [0] + list(q)  # first byte of each group
+    lca, g = 0, 0
+    for i in range(T):
+        while g < len(q) and q[g] <= i:
+            g += 1
+        lca += i + 1 - (starts[g - 1] if g >= 1 else 0)
+    causal = T * (T + 1) / 2
+    pairs = (model.n_enc + model.n_nb) * causal + model.n_lm * K1 * (K1 + 1) / 2 + model.n_mb * lca
+    return linear, 4.0 * d * pairs
+
+
+def bench_forward(args, wl):
+    """One step = one full-sequence forward of the workload's sequence (both heads at
+    every position, the losses); value = bytes of sequence processed per second."""
+    import numpy as np
+    import torch
+
+    import synth
+    from paper_2608_15454_amd import Decoder, make_config
+
+    model, T = wl.model, wl.prompt_len
+    K = 20 if args.steps is None else args.steps
+    W = 3 if args.warmup is None else args.warmup
+    log(f"[bench] workload {wl.name} T={T} steps={K} warmup={W}")
+    weights = synth.make_weights(model, seed=0, logit_gain=args.logit_gain)
+    x = synth.make_prompt(0, T)
+    dec = Decoder(make_config(model, max_batch=1, max_ctx=T + 8, engine=not args.no_engine), weights)
+    work = None
+    for _ in range(max(W, 1)):
+        nll, loss = dec.forward(x, work=work)
+        work = dec.fwork
+    dec.prefill([x])  # the segmentation, for the flop count (a host read, untimed)
+    q = [int(v) for v in dec.row_boundaries(0)]
+    dec.reset()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    w0 = time.perf_counter()
+    for _ in range(K):
+        nll, loss = dec.forward(x, work=work)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    elapsed = max(time.perf_counter() - w0, ev0.elapsed_time(ev1) / 1000.0)
+    value = K * T / elapsed
+    lv = loss.double().cpu().numpy()
+    log(f"[bench] timed: {K} forwards {elapsed * 1000:.1f} ms, {value:.0f} B/s, losses {lv}")
+
+    lin, att = forward_flops(model, T, q)
+    roofline, classes = None, {}
+    if not args.no_timing_pass:
+        dec.set_timing(True)
+        for _ in range(K):
+            dec.forward(x, work=work)
+        torch.cuda.synchronize()
+        classes = dec.read_timing()
+        dec.set_timing(False)
+        dom = max(classes, key=lambda c: classes[c][1])
+        launches, ms, _ = classes[dom]
+        flops = {"gemm": lin * K, "attention": att * K}.get(dom)
+        if flops is not None:
+            # bf16 weights: the linear layers run on bf16 MFMAs and the attention (float16
+            # caches, head size 64) on float16 MFMAs, both 2.5 PFLOP/s dense; float32
+            # models stay on the vector ALUs
+            mfma = model.dtype == "bf16" and (dom == "gemm" or model.d_head == 64)
+            peak = MFMA_BF16_PEAK_TFLOPS if mfma else VALU_FP32_PEAK_TFLOPS
+            achieved = flops / (ms / 1000.0) / 1e12
+            roofline = {"bound": "mfma" if mfma else "alu",
+                        "kernel": f"{dom} (all launches of the class in the timed forwards)",
+                        "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                        "frac": round(achieved / peak, 4), "traffic": None, "launches": launches,
+                        "avg_launch_us": round(ms * 1000.0 / max(launches, 1), 3),
+                        "flops_per_launch": round(flops / max(launches, 1))}
+        log("[bench] kernel classes: " + ", ".join(f"{k}: {v[0]} launches {v[1]:.1f} ms" for k, v in classes.items()))
+
+    cpu = None
+    if args.cpu_steps > 0:
+        import oracle
+
+        W64 = oracle.to_float64(weights)
+        Tc = 512
+        c0 = time.perf_counter()
+        oracle.forward_losses(W64, model, x[:Tc])
+        cs = time.perf_counter() - c0
+        cpu = {"value": round(Tc / cs, 2), "unit": "bytes/s", "cores": cpu_threads(), "kind": "oracle",
+               "sample": f"one forward of the first {Tc} bytes of the sequence (float64, {cs:.1f}s)"}
+        log(f"[bench] cpu oracle {Tc} bytes in {cs:.1f}s")
+    out = {
+        "metric": "full-sequence forward bytes/s", "value": round(value, 1), "unit": "bytes/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(elapsed * 1000.0 / K, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"{wl.name}: d={model.d_model} heads={model.n_heads} layers enc/lm/nt/mb="
+                               f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb}, one {T}-byte sequence, "
+                               f"{len(q)} segments, both heads at every position and the losses",
+                   "seq_len": T, "segments": len(q), "weights": model.dtype,
+                   "kv_cache": "f16" if model.dtype == "bf16" else "f32"},
+        "roofline": roofline, "cpu_baseline": cpu,
+        "flops_per_step": {"linear": lin, "attention": att},
+        "kernel_classes": {k: {"launches": v[0], "ms": round(v[1], 3)} for k, v in classes.items()},
+        "losses": [round(float(v), 4) for v in lv],
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -127,6 +246,10 @@ def main():
     from paper_2608_15454_amd import SELF_VERIFY, THRESHOLD, Decoder, make_config
 
     wl = synth.WORKLOADS[args.workload]
+    if wl.mode == "forward":
+        return bench_forward(args, wl)
+    args.steps = 1024 if args.steps is None else args.steps
+    args.warmup = 16 if args.warmup is None else args.warmup
     model = wl.model
     n = args.n or wl.n
     tau = wl.tau if args.tau is None else args.tau

@@ -651,6 +651,154 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
   }
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// The same attention on the matrix cores, for float16 caches and head size 64: a
+// block of two waves takes a tile of up to 64 query rows (32 per wave) and walks the
+// visible keys in blocks of 64.  S = Q K^T and O += P V are 32x32x16 float16 MFMAs
+// with float32 accumulation; Q and P enter as float16 pairs (hi + lo, two MFMAs), so
+// their rounding stays near float32, and K, V are the cache's own float16 values.
+// MFMA operand layout: lane l supplies row / column l % 32 and the 8 consecutive k
+// from 8 * (l / 32); accumulator element r of lane l is row 8 (r / 4) + 4 (l / 32) +
+// r % 4, column l % 32.  K is staged as [key][dim] and V transposed, [dim][key], so
+// every operand read is 8 consecutive halves; P goes through LDS from the
+// accumulator layout to the operand layout.
+__global__ __launch_bounds__(128) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
+  constexpr int DH = 64, LD = DH + 8;
+  const int tile = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int t0 = tiles[2 * tile], cnt = tiles[2 * tile + 1];
+  const int b = a.tok.b[t0], slot0 = a.tok.slot[t0];
+  const int kvmax = slot0 + cnt;
+  __shared__ __attribute__((aligned(16))) _Float16 Ks[64 * LD];
+  __shared__ __attribute__((aligned(16))) _Float16 Vt[DH * LD];
+  __shared__ __attribute__((aligned(16))) _Float16 Ph[2][32 * LD];
+  __shared__ __attribute__((aligned(16))) _Float16 Pl[2][32 * LD];
+  __shared__ int32_t Gs[64];
+  __shared__ int32_t Gq[64];
+  const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
+  if (tid < 64) Gq[tid] = gt != nullptr ? a.tok.grp[t0 + (tid < cnt ? tid : 0)] : 0;
+  int k_begin = 0;
+  if (gt != nullptr) {
+    const int need = a.tok.grp[t0] - 1;
+    int lo = 0, hi = slot0;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (gt[mid] < need) lo = mid + 1;
+      else hi = mid;
+    }
+    k_begin = lo;
+  }
+  const int col = lane & 31, half = lane >> 5;
+  // query fragments of this lane: row wave*32 + col, dims ks*16 + half*8 .. +7
+  f16x8 qh[4], ql[4];
+  {
+    const int qi = wave * 32 + col;
+    const float* qp = a.Q + (size_t)(t0 + (qi < cnt ? qi : 0)) * a.ldq + h * DH + half * 8;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = qp[ks * 16 + j] * a.scale;
+        const _Float16 hv = (_Float16)v;
+        qh[ks][j] = hv;
+        ql[ks][j] = (_Float16)(v - (float)hv);
+      }
+  }
+  const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH;
+  const _Float16* kb = reinterpret_cast<const _Float16*>(a.kc) + base;
+  const _Float16* vb = reinterpret_cast<const _Float16*>(a.vc) + base;
+  f32x16 o0, o1;
+  float m_run[16], l_run[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    o0[r] = 0.f;
+    o1[r] = 0.f;
+    m_run[r] = -INFINITY;
+    l_run[r] = 0.f;
+  }
+  __syncthreads();  // Gq
+  for (int k0 = k_begin; k0 < kvmax; k0 += 64) {
+    __syncthreads();  // the previous block's K, V and P are consumed
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7, j = k0 + c;
+      uint4 kv4 = make_uint4(0, 0, 0, 0), vv4 = make_uint4(0, 0, 0, 0);
+      if (j < kvmax) {
+        kv4 = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH + part * 8);
+        vv4 = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH + part * 8);
+      }
+      *reinterpret_cast<uint4*>(&Ks[c * LD + part * 8]) = kv4;
+      const _Float16* ve = reinterpret_cast<const _Float16*>(&vv4);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) Vt[(part * 8 + e) * LD + c] = ve[e];
+    }
+    if (tid < 64) Gs[tid] = (gt != nullptr && k0 + tid < kvmax) ? gt[k0 + tid] : 0;
+    __syncthreads();
+    f32x16 s0, s1;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      s0[r] = 0.f;
+      s1[r] = 0.f;
+    }
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const f16x8 b0 = *reinterpret_cast<const f16x8*>(&Ks[col * LD + ks * 16 + half * 8]);
+      const f16x8 b1 = *reinterpret_cast<const f16x8*>(&Ks[(32 + col) * LD + ks * 16 + half * 8]);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[ks], b0, s0, 0, 0, 0);
+      s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[ks], b0, s0, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[ks], b1, s1, 0, 0, 0);
+      s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[ks], b1, s1, 0, 0, 0);
+    }
+    const int j0 = k0 + col, j1 = k0 + 32 + col;
+    const int g0 = Gs[col], g1 = Gs[32 + col];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = 8 * (r >> 2) + 4 * half + (r & 3), qi = wave * 32 + row;
+      const int islot = slot0 + qi, gq = Gq[qi < 64 ? qi : 0];
+      const float v0 = (j0 < kvmax && j0 <= islot && g0 >= gq - 1) ? s0[r] : -INFINITY;
+      const float v1 = (j1 < kvmax && j1 <= islot && g1 >= gq - 1) ? s1[r] : -INFINITY;
+      const float mx = group_max<32>(fmaxf(v0, v1));
+      const float m_new = fmaxf(m_run[r], mx);
+      const float alpha = (m_run[r] == -INFINITY) ? 0.f : expf(m_run[r] - m_new);
+      const float p0 = (v0 == -INFINITY) ? 0.f : expf(v0 - m_new);
+      const float p1 = (v1 == -INFINITY) ? 0.f : expf(v1 - m_new);
+      const float ls = group_sum<32>(p0 + p1);
+      if (m_new != -INFINITY) {
+        l_run[r] = l_run[r] * alpha + ls;
+        m_run[r] = m_new;
+        o0[r] *= alpha;
+        o1[r] *= alpha;
+      }
+      const _Float16 h0 = (_Float16)p0, h1 = (_Float16)p1;
+      Ph[wave][row * LD + col] = h0;
+      Ph[wave][row * LD + 32 + col] = h1;
+      Pl[wave][row * LD + col] = (_Float16)(p0 - (float)h0);
+      Pl[wave][row * LD + 32 + col] = (_Float16)(p1 - (float)h1);
+    }
+    __syncthreads();  // P in LDS
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      const f16x8 ph = *reinterpret_cast<const f16x8*>(&Ph[wave][col * LD + ks * 16 + half * 8]);
+      const f16x8 pl = *reinterpret_cast<const f16x8*>(&Pl[wave][col * LD + ks * 16 + half * 8]);
+      const f16x8 v0 = *reinterpret_cast<const f16x8*>(&Vt[col * LD + ks * 16 + half * 8]);
+      const f16x8 v1 = *reinterpret_cast<const f16x8*>(&Vt[(32 + col) * LD + ks * 16 + half * 8]);
+      o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ph, v0, o0, 0, 0, 0);
+      o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(pl, v0, o0, 0, 0, 0);
+      o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ph, v1, o1, 0, 0, 0);
+      o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(pl, v1, o1, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int qi = wave * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+    if (qi < cnt) {
+      float* op = a.O + (size_t)(t0 + qi) * a.ldo + h * DH;
+      op[col] = o0[r] / l_run[r];
+      op[32 + col] = o1[r] / l_run[r];
+    }
+  }
+}
+
 // ------------------------------------------------------------ row kernels ------
 template <typename W>
 __global__ void embed_kernel(const W* emb, const int32_t* bytes, float* X, int d) {
@@ -1233,6 +1381,8 @@ hipError_t attn_decode_t(const Attn& a, int max_kv, float* part, int64_t part_fl
 template <typename KV>
 hipError_t attn_prefill_t(const Attn& a, const int32_t* tiles, int ntiles, hipStream_t st, const Ev& ev) {
   const dim3 grid(ntiles, a.H);
+  if constexpr (std::is_same<KV, _Float16>::value)
+    if (a.dh == 64) return klaunch(attn_prefill_mfma_kernel, grid, dim3(128), 0, st, ev.start, ev.stop, a, tiles);
   if (a.dh == 64) return klaunch(attn_prefill_kernel<KV, 64>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
   return klaunch(attn_prefill_kernel<KV, 32>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
 }

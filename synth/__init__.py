@@ -88,7 +88,7 @@ class Workload:
     gen_len: int
     n: int
     tau: float
-    mode: str = "threshold"  # "threshold" | "verify" | "external"
+    mode: str = "threshold"  # "threshold" | "verify" | "external" | "forward" (full-sequence)
     verifier: "ModelConfig" = None  # mode "external": the next-byte model checking the drafts
     temperature: float = 0.0  # > 0: sampled decoding at this temperature (0: greedy)
     top_p: float = 1.0        # nucleus of sampled decoding
@@ -125,6 +125,10 @@ WORKLOADS = {
     # the MBP d=1024 model drafts n = 7 candidates, the FxT d=1024 model verifies them
     "extverify_d1024_b1": Workload("extverify_d1024_b1", _D1024_LCA, batch=1, prompt_len=4096, gen_len=1024, n=7,
                                    tau=0.75, mode="external", verifier=D1024_FXT),
+    # the training-form forward over one whole 4096-byte sequence (both heads at every
+    # position, the MB layers under the full LCA mask, the losses)
+    "forward_d1024_t4096": Workload("forward_d1024_t4096", _D1024_LCA, batch=1, prompt_len=4096, gen_len=0, n=0,
+                                    tau=0.0, mode="forward"),
     # segments from the learned boundary predictor instead of the space rule; the probe
     # is scaled to confident logits (std about 1 on this model's encoder states) and
     # biased so that about one byte in three ends a segment where decoding runs (the
