@@ -142,3 +142,17 @@ def test_forward_d1024_bf16():
     x = synth.make_prompt(0, 4096)[:1024]
     ref = check(dec, W, model, x, base_tol(model))
     print("k", ref["k"], "sum_nt", ref["sum_nt"], "sum_mb", ref["sum_mb"])
+
+
+@pytest.mark.timeout(600)
+def test_forward_d1024_full_sequence():
+    """The benchmarked configuration: the d=1024 model on the whole 4096-byte sequence,
+    the launch shapes the forward bench times (one 4096-row pass per stack), every
+    position against the oracle."""
+    wl = synth.WORKLOADS["forward_d1024_t4096"]
+    model = wl.model
+    raw = synth.make_weights(model, seed=0)
+    W = oracle.to_float64(raw)
+    dec = new_decoder(model, raw, 1, wl.prompt_len + 8)
+    ref = check(dec, W, model, synth.make_prompt(0, wl.prompt_len), base_tol(model))
+    print("k", ref["k"], "sum_nt", ref["sum_nt"], "sum_mb", ref["sum_mb"])
