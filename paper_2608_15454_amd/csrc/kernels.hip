@@ -265,9 +265,11 @@ constexpr int kMfmaBK = 64, kMfmaLD = kMfmaBK + 8;  // LDS row pitch in bf16 ele
 // to L.part after the [ksplit][M][N] partials, written by the blocks of column 0).
 __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   constexpr int BM = 64, BN = 64, BK = kMfmaBK, LD = kMfmaLD;
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][BM * LD];  // hi halves of X
-  __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LD];  // lo halves of X
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LD];
+  // one LDS buffer (28 KB): more blocks per compute unit hide the fetch latency; the
+  // next step's fetch into registers still overlaps this step's MFMAs
+  __shared__ __attribute__((aligned(16))) uint16_t As[1][BM * LD];  // hi halves of X
+  __shared__ __attribute__((aligned(16))) uint16_t Al[1][BM * LD];  // lo halves of X
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[1][BN * LD];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
   // loads: thread t stages 16 consecutive k of row t/4 of both tiles
@@ -324,7 +326,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   stage(0);
   __syncthreads();
   for (int kt = kt0; kt < kt1; ++kt) {
-    const int cur = (kt - kt0) & 1;
+    const int cur = 0;
     if (kt + 1 < kt1) fetch((kt + 1) * BK);  // in flight during this step's MFMAs
     const int aoff = (wm * 32 + (lane & 31)) * LD + (lane >> 5) * 8;
     const uint16_t* ab = &As[cur][aoff];
@@ -338,7 +340,10 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa, fb, acc, 0, 0, 0);
       acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fl, fb, acc, 0, 0, 0);
     }
-    if (kt + 1 < kt1) stage(cur ^ 1);
+    if (kt + 1 < kt1) {
+      __syncthreads();  // every wave has read this step's tiles
+      stage(0);
+    }
     __syncthreads();
   }
   const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
