@@ -667,8 +667,9 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // from 8 * (l / 32); accumulator element r of lane l is row 8 (r / 4) + 4 (l / 32) +
 // r % 4, column l % 32.  K is staged as [key][dim] and V transposed, [dim][key], so
 // every operand read is 8 consecutive halves; P goes through LDS from the
-// accumulator layout to the operand layout.
-__global__ __launch_bounds__(128) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
+// accumulator layout to the operand layout.  Two waves per SIMD (the register budget
+// that allows, 256, holds it without spills; four blocks fit the LDS).
+__global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
   constexpr int DH = 64, LD = DH + 8;
   const int tile = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int t0 = tiles[2 * tile], cnt = tiles[2 * tile + 1];
