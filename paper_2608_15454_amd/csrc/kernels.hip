@@ -271,7 +271,18 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   __shared__ __attribute__((aligned(16))) uint16_t Al[1][BM * LD];  // lo halves of X
   __shared__ __attribute__((aligned(16))) uint16_t Bs[1][BN * LD];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  // Workgroups go to the 8 XCDs round-robin by linear id.  Without split-K and with a
+  // multiple of 8 row blocks, XCD k takes row blocks k, k+8, ... (its activation rows
+  // stay in its own L2) and walks them fastest, so a weight tile is reused by the
+  // XCD's row blocks while it is resident.
+  int bx = blockIdx.x, by = blockIdx.y;
+  if (gridDim.z == 1 && (gridDim.y & 7) == 0) {
+    const int bid = blockIdx.y * gridDim.x + blockIdx.x, xcd = bid & 7, l = bid >> 3;
+    const int rows_per = gridDim.y >> 3;
+    by = xcd + 8 * (l % rows_per);
+    bx = l / rows_per;
+  }
+  const int m0 = by * BM, n0 = bx * BN;
   // loads: thread t stages 16 consecutive k of row t/4 of both tiles
   const int lr = tid >> 2, lk = (tid & 3) * 16;
   const int am = m0 + lr;
