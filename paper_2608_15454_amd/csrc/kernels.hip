@@ -682,7 +682,16 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // that allows, 256, holds it without spills; four blocks fit the LDS).
 __global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
   constexpr int DH = 64, LD = DH + 8;
-  const int tile = blockIdx.x, h = blockIdx.y, tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // XCD-aware order (workgroups go to the 8 XCDs round-robin by linear id): with a
+  // multiple of 8 heads, XCD k takes heads k, k+8, ..., so it reads only their keys and
+  // values, which its L2 can hold
+  int tile = blockIdx.x, h = blockIdx.y;
+  if ((gridDim.y & 7) == 0) {
+    const int bid = blockIdx.y * gridDim.x + blockIdx.x, l = bid >> 3;
+    h = (bid & 7) + 8 * (l / gridDim.x);
+    tile = l % gridDim.x;
+  }
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int t0 = tiles[2 * tile], cnt = tiles[2 * tile + 1];
   const int b = a.tok.b[t0], slot0 = a.tok.slot[t0];
   const int kvmax = slot0 + cnt;
