@@ -671,16 +671,20 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // The same attention on the matrix cores, for float16 caches and head size 64: a
 // block of two waves takes a tile of up to 64 query rows (32 per wave) and walks the
-// visible keys in blocks of 64.  S = Q K^T and O += P V are 32x32x16 float16 MFMAs
-// with float32 accumulation; Q and P enter as float16 pairs (hi + lo, two MFMAs), so
-// their rounding stays near float32, and K, V are the cache's own float16 values.
-// MFMA operand layout: lane l supplies row / column l % 32 and the 8 consecutive k
-// from 8 * (l / 32); accumulator element r of lane l is row 8 (r / 4) + 4 (l / 32) +
-// r % 4, column l % 32.  K is staged as [key][dim] and V transposed, [dim][key], so
-// every operand read is 8 consecutive halves; P goes through LDS from the
-// accumulator layout to the operand layout.  Two waves per SIMD (the register budget
-// that allows, 256, holds it without spills; four blocks fit the LDS).
-__global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
+// visible keys in blocks of 64.  Everything is computed transposed, S^T = K Q^T and
+// O^T += V^T P^T (32x32x16 float16 MFMAs, float32 accumulation), so that each lane
+// owns one query: lane l holds query l % 32 and, in its accumulator registers, the
+// keys 8 (r / 4) + 4 (l / 32) + r % 4 of each 32-key block.  The softmax's max and sum
+// over a query's keys are then in-lane plus one exchange between the wave's halves,
+// and P^T feeds the second product straight from the registers: a contraction may
+// take its k positions in any order, so V^T is read in the key order the registers
+// hold (two runs of 4 keys per operand).  Q and P enter as float16 pairs (hi + lo,
+// two MFMAs each), so their rounding stays near float32; K and V are the cache's own
+// float16 values, staged in LDS as [key][dim] and [dim][key].
+// MFMA operand layout: lane l supplies row / column l % 32 and the 8 k positions
+// 8 (l / 32) .. +7 of each 16-wide k step.  Three waves per SIMD: 147 VGPRs, no
+// spills, six blocks in the LDS (a budget for four spills).
+__global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
   constexpr int DH = 64, LD = DH + 8;
   // XCD-aware order (workgroups go to the 8 XCDs round-robin by linear id): with a
   // multiple of 8 heads, XCD k takes heads k, k+8, ..., so it reads only their keys and
@@ -697,12 +701,8 @@ __global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const
   const int kvmax = slot0 + cnt;
   __shared__ __attribute__((aligned(16))) _Float16 Ks[64 * LD];
   __shared__ __attribute__((aligned(16))) _Float16 Vt[DH * LD];
-  __shared__ __attribute__((aligned(16))) _Float16 Ph[2][32 * LD];
-  __shared__ __attribute__((aligned(16))) _Float16 Pl[2][32 * LD];
   __shared__ int32_t Gs[64];
-  __shared__ int32_t Gq[64];
   const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
-  if (tid < 64) Gq[tid] = gt != nullptr ? a.tok.grp[t0 + (tid < cnt ? tid : 0)] : 0;
   int k_begin = 0;
   if (gt != nullptr) {
     const int need = a.tok.grp[t0] - 1;
@@ -715,11 +715,15 @@ __global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const
     k_begin = lo;
   }
   const int col = lane & 31, half = lane >> 5;
-  // query fragments of this lane: row wave*32 + col, dims ks*16 + half*8 .. +7
+  // this lane's query: row qi of the tile (padding rows repeat row 0 and are not stored)
+  const int qi = wave * 32 + col;
+  const int qrow = t0 + (qi < cnt ? qi : 0);
+  const int islot = slot0 + qi;
+  const int gq = gt != nullptr ? a.tok.grp[qrow] : 0;
+  // Q^T fragments (the B operand of S^T): query qi, dims ks*16 + half*8 .. +7
   f16x8 qh[4], ql[4];
   {
-    const int qi = wave * 32 + col;
-    const float* qp = a.Q + (size_t)(t0 + (qi < cnt ? qi : 0)) * a.ldq + h * DH + half * 8;
+    const float* qp = a.Q + (size_t)qrow * a.ldq + h * DH + half * 8;
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
 #pragma unroll
@@ -733,18 +737,15 @@ __global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const
   const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH;
   const _Float16* kb = reinterpret_cast<const _Float16*>(a.kc) + base;
   const _Float16* vb = reinterpret_cast<const _Float16*>(a.vc) + base;
-  f32x16 o0, o1;
-  float m_run[16], l_run[16];
+  f32x16 o0, o1;  // O^T: dims 32 db + 8 (r / 4) + 4 half + r % 4 of this lane's query
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     o0[r] = 0.f;
     o1[r] = 0.f;
-    m_run[r] = -INFINITY;
-    l_run[r] = 0.f;
   }
-  __syncthreads();  // Gq
+  float m_run = -INFINITY, l_run = 0.f;
   for (int k0 = k_begin; k0 < kvmax; k0 += 64) {
-    __syncthreads();  // the previous block's K, V and P are consumed
+    __syncthreads();  // the previous block's K and V are consumed
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7, j = k0 + c;
@@ -760,67 +761,90 @@ __global__ __launch_bounds__(128, 2) void attn_prefill_mfma_kernel(Attn a, const
     }
     if (tid < 64) Gs[tid] = (gt != nullptr && k0 + tid < kvmax) ? gt[k0 + tid] : 0;
     __syncthreads();
-    f32x16 s0, s1;
+    // S^T blocks: keys 32 cb + (row of the accumulator), this lane's query
+    f32x16 s[2];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = 0.f;
-      s1[r] = 0.f;
+    for (int cb = 0; cb < 2; ++cb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[cb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) {
+        const f16x8 kf = *reinterpret_cast<const f16x8*>(&Ks[(32 * cb + col) * LD + ks * 16 + half * 8]);
+        s[cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, qh[ks], s[cb], 0, 0, 0);
+        s[cb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(kf, ql[ks], s[cb], 0, 0, 0);
+      }
     }
+    float mx = -INFINITY;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const f16x8 b0 = *reinterpret_cast<const f16x8*>(&Ks[col * LD + ks * 16 + half * 8]);
-      const f16x8 b1 = *reinterpret_cast<const f16x8*>(&Ks[(32 + col) * LD + ks * 16 + half * 8]);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[ks], b0, s0, 0, 0, 0);
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[ks], b0, s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(qh[ks], b1, s1, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ql[ks], b1, s1, 0, 0, 0);
-    }
-    const int j0 = k0 + col, j1 = k0 + 32 + col;
-    const int g0 = Gs[col], g1 = Gs[32 + col];
+    for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = 8 * (r >> 2) + 4 * half + (r & 3), qi = wave * 32 + row;
-      const int islot = slot0 + qi, gq = Gq[qi < 64 ? qi : 0];
-      const float v0 = (j0 < kvmax && j0 <= islot && g0 >= gq - 1) ? s0[r] : -INFINITY;
-      const float v1 = (j1 < kvmax && j1 <= islot && g1 >= gq - 1) ? s1[r] : -INFINITY;
-      const float mx = group_max<32>(fmaxf(v0, v1));
-      const float m_new = fmaxf(m_run[r], mx);
-      const float alpha = (m_run[r] == -INFINITY) ? 0.f : expf(m_run[r] - m_new);
-      const float p0 = (v0 == -INFINITY) ? 0.f : expf(v0 - m_new);
-      const float p1 = (v1 == -INFINITY) ? 0.f : expf(v1 - m_new);
-      const float ls = group_sum<32>(p0 + p1);
-      if (m_new != -INFINITY) {
-        l_run[r] = l_run[r] * alpha + ls;
-        m_run[r] = m_new;
+      for (int r = 0; r < 16; ++r) {
+        const int kk = 32 * cb + 8 * (r >> 2) + 4 * half + (r & 3), j = k0 + kk;
+        const bool vis = j < kvmax && j <= islot && Gs[kk] >= gq - 1;
+        s[cb][r] = vis ? s[cb][r] : -INFINITY;
+        mx = fmaxf(mx, s[cb][r]);
+      }
+    mx = pair_max<32>(mx);  // the other half of the wave holds the query's other keys
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = (s[cb][r] == -INFINITY) ? 0.f : expf(s[cb][r] - m_new);
+        s[cb][r] = pv;
+        ls += pv;
+      }
+    ls = pair_sum<32>(ls);
+    if (m_new != -INFINITY) {
+      l_run = l_run * alpha + ls;
+      m_run = m_new;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
         o0[r] *= alpha;
         o1[r] *= alpha;
       }
-      const _Float16 h0 = (_Float16)p0, h1 = (_Float16)p1;
-      Ph[wave][row * LD + col] = h0;
-      Ph[wave][row * LD + 32 + col] = h1;
-      Pl[wave][row * LD + col] = (_Float16)(p0 - (float)h0);
-      Pl[wave][row * LD + 32 + col] = (_Float16)(p1 - (float)h1);
     }
-    __syncthreads();  // P in LDS
+    // O^T += V^T P^T, k steps of 16 keys: step (cb, t) takes registers 8t .. 8t+7 of
+    // block cb, i.e. keys 32 cb + 16 t + 4 half + {0..3} and + 8 + {0..3}
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const f16x8 ph = *reinterpret_cast<const f16x8*>(&Ph[wave][col * LD + ks * 16 + half * 8]);
-      const f16x8 pl = *reinterpret_cast<const f16x8*>(&Pl[wave][col * LD + ks * 16 + half * 8]);
-      const f16x8 v0 = *reinterpret_cast<const f16x8*>(&Vt[col * LD + ks * 16 + half * 8]);
-      const f16x8 v1 = *reinterpret_cast<const f16x8*>(&Vt[(32 + col) * LD + ks * 16 + half * 8]);
-      o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ph, v0, o0, 0, 0, 0);
-      o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(pl, v0, o0, 0, 0, 0);
-      o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(ph, v1, o1, 0, 0, 0);
-      o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(pl, v1, o1, 0, 0, 0);
-    }
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        f16x8 ph, pl;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float pv = s[cb][8 * t + j];
+          const _Float16 hv = (_Float16)pv;
+          ph[j] = hv;
+          pl[j] = (_Float16)(pv - (float)hv);
+        }
+        const int kc = 32 * cb + 16 * t + 4 * half;
+        f16x8 v0, v1;
+        {
+          const uint2 a0 = *reinterpret_cast<const uint2*>(&Vt[col * LD + kc]);
+          const uint2 a1 = *reinterpret_cast<const uint2*>(&Vt[col * LD + kc + 8]);
+          const uint2 c0 = *reinterpret_cast<const uint2*>(&Vt[(32 + col) * LD + kc]);
+          const uint2 c1 = *reinterpret_cast<const uint2*>(&Vt[(32 + col) * LD + kc + 8]);
+          const uint4 va = make_uint4(a0.x, a0.y, a1.x, a1.y), vc = make_uint4(c0.x, c0.y, c1.x, c1.y);
+          v0 = *reinterpret_cast<const f16x8*>(&va);
+          v1 = *reinterpret_cast<const f16x8*>(&vc);
+        }
+        o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v0, ph, o0, 0, 0, 0);
+        o0 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v0, pl, o0, 0, 0, 0);
+        o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v1, ph, o1, 0, 0, 0);
+        o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v1, pl, o1, 0, 0, 0);
+      }
   }
+  if (qi < cnt) {
+    float* op = a.O + (size_t)(t0 + qi) * a.ldo + h * DH;
+    const float inv = 1.0f / l_run;
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const int qi = wave * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-    if (qi < cnt) {
-      float* op = a.O + (size_t)(t0 + qi) * a.ldo + h * DH;
-      op[col] = o0[r] / l_run[r];
-      op[32 + col] = o1[r] / l_run[r];
+    for (int r = 0; r < 16; ++r) {
+      const int dd = 8 * (r >> 2) + 4 * half + (r & 3);
+      op[dd] = o0[r] * inv;
+      op[32 + dd] = o1[r] * inv;
     }
   }
 }
