@@ -20,6 +20,12 @@ reason, in the design notes of this repository):
 * Self-verify: c_1 is the next-byte greedy byte; c_m (m >= 2) is kept while it equals
   the greedy byte after x ++ c_1..c_{m-1}.  The correction byte at the first mismatch
   is the next step's c_1, so the emitted sequence is the greedy one.
+* Learned boundaries: the predictor is a linear probe on the RMS-normalized encoder
+  state, logit = w . h_e / RMS(h_e) + b; at inference byte i ends a segment when its
+  logit is >= 0 (probability >= 0.5, no Gumbel noise), or at max_patch bytes.
+* Training objective: sums over positions of the next-byte and MB negative
+  log-likelihoods (MB row t predicts x_{t+2} under the full-sequence LCA mask), plus
+  lambda_2 L_BP with k = the number of segment ends.
 """
 from __future__ import annotations
 
