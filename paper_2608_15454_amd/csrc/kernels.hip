@@ -396,14 +396,25 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) 
   if (idx >= (int64_t)L.M * per_row) return;
   const int m = (int)(idx / per_row);
   const int n = (int)(idx - (int64_t)m * per_row) * (pair ? 2 : 1);
+  // The splits are added in order z = 0, 1, ...; the unrolled loops only issue several
+  // splits' loads before the first add (a pair is one 8-byte load: n and N are even).
   float a0 = 0.f, a1 = 0.f;
-  for (int z = 0; z < ksplit; ++z) {
-    const float* pp = L.part + ((size_t)z * L.M + m) * L.N + n;
-    a0 += pp[0];
-    if (pair) a1 += pp[1];
+  const float* pp = L.part + (size_t)m * L.N + n;
+  const size_t zs = (size_t)L.M * L.N;
+  if (pair) {
+#pragma unroll 8
+    for (int z = 0; z < ksplit; ++z) {
+      const float2 t = *reinterpret_cast<const float2*>(pp + z * zs);
+      a0 += t.x;
+      a1 += t.y;
+    }
+  } else {
+#pragma unroll 8
+    for (int z = 0; z < ksplit; ++z) a0 += pp[z * zs];
   }
   if (L.gain != nullptr) {  // RMSNorm: 1/RMS of the row from the splits' sums of squares
     float ss = 0.f;
+#pragma unroll 8
     for (int z = 0; z < ksplit; ++z) ss += L.part[(size_t)ksplit * L.M * L.N + (size_t)z * L.M + m];
     const float sc = 1.0f / sqrtf(ss / (float)L.K + L.eps);
     a0 *= sc;
