@@ -1354,9 +1354,8 @@ bool gemv_fits(const Linear& L) {
   return L.N % r == 0 && !(pair && r % 2 != 0);
 }
 
-template <typename W, int KC>
-hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
-  constexpr int R = gemv_r(KC);
+template <typename W, int KC, int R>
+hipError_t gemv_launch_r(const Linear& L, hipStream_t st, const Ev& ev) {
   constexpr int MRMAX = gemv_mr(KC);
   const dim3 grid((L.N / R + 3) / 4);
   if (L.M == 1) return klaunch(gemv_kernel<W, 1, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
@@ -1365,6 +1364,18 @@ hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
   }
   if constexpr (MRMAX >= 4) return klaunch(gemv_kernel<W, 4, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
   return klaunch(gemv_kernel<W, 1, R, KC>, grid, dim3(256), 0, st, ev.start, ev.stop, L);
+}
+
+// A narrow product (few output rows, such as the 256-row unembedding) at R rows per
+// wave leaves most compute units idle; one row per wave gives it four times the waves.
+template <typename W, int KC>
+hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
+  constexpr int R = gemv_r(KC);
+  if constexpr (R > 1) {
+    const bool single = L.epi.kind == EPI_STORE || L.epi.kind == EPI_RESID;
+    if (single && (L.N / R + 3) / 4 < 64) return gemv_launch_r<W, KC, 1>(L, st, ev);
+  }
+  return gemv_launch_r<W, KC, R>(L, st, ev);
 }
 
 // Linears of more rows than this use the matrix cores (bfloat16 weights).
