@@ -869,12 +869,26 @@ __global__ void embed_kernel(const W* emb, const int32_t* bytes, float* X, int d
 }
 
 __global__ void copy_rows_kernel(const float* src, const int32_t* src_idx, const float* src2,
-                                 const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d) {
+                                 const int32_t* src2_idx, float* dst, const int32_t* dst_idx, int d, int vec4) {
   const int i = blockIdx.x;
   if (dst_idx != nullptr && dst_idx[i] < 0) return;  // row not copied
   const size_t si = (size_t)(src_idx ? src_idx[i] : i) * d;
   const size_t di = (size_t)(dst_idx ? dst_idx[i] : i) * d;
   const size_t s2 = src2 ? (size_t)(src2_idx ? src2_idx[i] : i) * d : 0;
+  if (vec4) {  // d % 4 == 0 and 16-byte aligned buffers (checked by the launcher)
+    for (int k4 = threadIdx.x; k4 < d / 4; k4 += blockDim.x) {
+      float4 v = reinterpret_cast<const float4*>(src + si)[k4];
+      if (src2) {
+        const float4 t = reinterpret_cast<const float4*>(src2 + s2)[k4];
+        v.x += t.x;
+        v.y += t.y;
+        v.z += t.z;
+        v.w += t.w;
+      }
+      reinterpret_cast<float4*>(dst + di)[k4] = v;
+    }
+    return;
+  }
   for (int k = threadIdx.x; k < d; k += blockDim.x) {
     float v = src[si + k];
     if (src2) v += src2[s2 + k];
@@ -1524,8 +1538,9 @@ hipError_t launch_embed(const void* emb, int wdt, const int32_t* bytes, float* X
 hipError_t launch_copy_rows(const float* src, const int32_t* src_idx, const float* src2, const int32_t* src2_idx,
                             float* dst, const int32_t* dst_idx, int d, int M, hipStream_t st, const Ev& ev) {
   if (M <= 0) return hipSuccess;
+  const int vec4 = (d % 4 == 0) && (((uintptr_t)src | (uintptr_t)src2 | (uintptr_t)dst) & 15) == 0;
   return klaunch(copy_rows_kernel, dim3(M), dim3(256), 0, st, ev.start, ev.stop, src, src_idx, src2, src2_idx, dst,
-                 dst_idx, d);
+                 dst_idx, d, vec4);
 }
 
 hipError_t launch_pool(const float* src, const int32_t* lo, const int32_t* cnt, const float* bos, float* dst,
