@@ -180,11 +180,71 @@ def test_block_with_zero_weights_is_identity():
     np.testing.assert_array_equal(oracle.block(u, P, oracle.causal_mask(4), np.arange(4), TINY.replace(n_heads=2, d_model=8)), u)
 
 
-# ------------------------------------------------------------ segmentation --
-
 def _golden(name):
     with open(os.path.join(GOLDEN, name)) as f:
         return json.load(f)
+
+
+def _hand_block():
+    """The hand-derived block fixture: its config (eps = 0 as derived) and parameters."""
+    g = _golden("block_stack.json")
+    cfg = TINY.replace(d_model=g["d_model"], n_heads=g["n_heads"], d_ff=2, rms_eps=0.0)
+    P = [{k: np.asarray(v, np.float64) for k, v in g[name].items()} for name in ("P0", "P1")]
+    return g, cfg, P
+
+
+def test_block_hand_derived_one_token():
+    """A one-token block: the softmax over a single key is 1, so attention reduces to
+    W_o W_v (RMSNorm(u) g_attn); the expected vector is derived by hand in the fixture.
+    Swapping the two norm gains, normalizing u instead of a before the FFN, a
+    post-norm block or a dropped residual all change it."""
+    g, cfg, (P0, _) = _hand_block()
+    u = np.asarray(g["one_token"]["u"], np.float64)
+    got = oracle.block(u, P0, oracle.causal_mask(1), np.arange(1), cfg)
+    np.testing.assert_allclose(got, g["one_token"]["block_P0"], rtol=1e-14, atol=1e-14)
+    # the same at the model's eps = 1e-6: the norms move by O(eps) only
+    got_eps = oracle.block(u, P0, oracle.causal_mask(1), np.arange(1), cfg.replace(rms_eps=1e-6))
+    np.testing.assert_allclose(got_eps, g["one_token"]["block_P0"], rtol=0, atol=1e-5)
+    assert np.max(np.abs(got_eps - got)) > 0  # eps reaches the norms
+    # a query attends to one key whatever its position: RoPE cannot change it
+    got_p = oracle.block(u, P0, oracle.causal_mask(1), np.array([37]), cfg)
+    np.testing.assert_allclose(got_p, got, rtol=1e-14, atol=1e-14)
+
+
+def test_block_hand_derived_two_tokens_causal():
+    """Two tokens with zero queries: every visible key gets the same weight, so row 0
+    (which sees only itself under the causal mask) repeats the one-token result and
+    row 1 averages both values; expected rows derived by hand in the fixture."""
+    g, cfg, (P0, _) = _hand_block()
+    P = dict(P0, wq=np.zeros_like(P0["wq"]))
+    u = np.asarray(g["two_tokens"]["u"], np.float64)
+    got = oracle.block(u, P, oracle.causal_mask(2), np.arange(2), cfg)
+    np.testing.assert_allclose(got, g["two_tokens"]["block_P0_wq0"], rtol=1e-14, atol=1e-14)
+
+
+def test_stack_applies_each_layers_own_parameters_in_order():
+    """A two-layer stack with different parameters per layer equals the hand-derived
+    composition block(block(u, P0), P1); reusing layer 0's parameters, reversing the
+    order or skipping a layer each gives a different vector."""
+    g, cfg, (P0, P1) = _hand_block()
+    W = {}
+    for i, P in enumerate((P0, P1)):
+        for k, v in P.items():
+            W[f"s.{i}.{k}"] = v
+    u = np.asarray(g["one_token"]["u"], np.float64)
+    want = np.asarray(g["one_token"]["stack_P0_P1"])
+    got = oracle.stack(u, W, "s", 2, oracle.causal_mask(1), np.arange(1), cfg)
+    np.testing.assert_allclose(got, want, rtol=1e-14, atol=1e-14)
+    one = oracle.stack(u, W, "s", 1, oracle.causal_mask(1), np.arange(1), cfg)
+    np.testing.assert_allclose(one, g["one_token"]["block_P0"], rtol=1e-14, atol=1e-14)
+    # the wrong compositions are far from the expected vector
+    m, pos = oracle.causal_mask(1), np.arange(1)
+    for wrong in (oracle.block(oracle.block(u, P0, m, pos, cfg), P0, m, pos, cfg),
+                  oracle.block(oracle.block(u, P1, m, pos, cfg), P0, m, pos, cfg)):
+        assert np.max(np.abs(wrong - want)) > 0.1
+
+
+# ------------------------------------------------------------ segmentation --
 
 
 @pytest.mark.parametrize("case", _golden("segmentation.json")["cases"])
