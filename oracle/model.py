@@ -100,13 +100,15 @@ def attention(x, P, mask, pos, n_heads, rope_base, attn_scale):
     q = rope(q, pos, rope_base).transpose(1, 0, 2)  # [H, T, dh]
     k = rope(k, pos, rope_base).transpose(1, 0, 2)
     v = v.transpose(1, 0, 2)
-    scores = (q @ k.transpose(0, 2, 1)) * (attn_scale / np.sqrt(dh))  # [H, T(query), T(key)]
-    scores = np.where(mask[None, :, :], scores, -np.inf)
-    scores = scores - scores.max(axis=-1, keepdims=True)
-    p = np.exp(scores)
-    p = p / p.sum(axis=-1, keepdims=True)
-    o = (p @ v).transpose(1, 0, 2).reshape(T, d)
-    return o @ P["wo"].T
+    o = np.empty((T, n_heads, dh))
+    for h in range(n_heads):  # one head at a time: a [T(query), T(key)] score matrix
+        scores = (q[h] @ k[h].T) * (attn_scale / np.sqrt(dh))
+        scores = np.where(mask, scores, -np.inf)
+        scores = scores - scores.max(axis=-1, keepdims=True)
+        p = np.exp(scores)
+        p = p / p.sum(axis=-1, keepdims=True)
+        o[:, h, :] = p @ v[h]
+    return o.reshape(T, d) @ P["wo"].T
 
 
 def silu(x):
@@ -323,21 +325,29 @@ def step(W, cfg, x, n, tau):
     return {"logits": logits, "cand": cand, "prob": prob, "k": threshold_accept(prob, tau)}
 
 
-def _greedy_byte(W, cfg, x):
+def _nt_logits(W, cfg, x):
+    """Next-byte head logits after the byte sequence x."""
     tr = trunk(W, cfg, x)
-    l1 = head_logits(tr["h1"][len(x) - 1], W["nt_norm"], W, cfg.rms_eps)
-    return int(top1(l1[None, :])[0][0])
+    return head_logits(tr["h1"][len(x) - 1], W["nt_norm"], W, cfg.rms_eps)
 
 
-def verify_drafts(W, cfg, x, drafts):
+def _greedy_byte(W, cfg, x):
+    return int(top1(_nt_logits(W, cfg, x)[None, :])[0][0])
+
+
+def verify_drafts(W, cfg, x, drafts, seen=None):
     """Greedy speculative verification (Section 6.2, following Leviathan et al.): draft
     c_1 is kept; c_m (m >= 2) is kept while it equals the next-byte greedy byte after
-    x ++ c_1..c_{m-1}.  Returns the number of kept drafts j and the greedy bytes seen."""
+    x ++ c_1..c_{m-1}.  Returns the number of kept drafts j and the greedy bytes seen
+    (and appends the next-byte logits they came from to ``seen`` when it is a list)."""
     drafts = np.asarray(drafts, np.int64)
     j = 1
     gammas = []
     for m in range(2, len(drafts) + 1):
-        gm = _greedy_byte(W, cfg, np.concatenate([np.asarray(x, np.int64), drafts[: m - 1]]))
+        lm = _nt_logits(W, cfg, np.concatenate([np.asarray(x, np.int64), drafts[: m - 1]]))
+        if seen is not None:
+            seen.append(lm)
+        gm = int(top1(lm[None, :])[0][0])
         gammas.append(gm)
         if gm != int(drafts[m - 1]):
             break
@@ -347,10 +357,13 @@ def verify_drafts(W, cfg, x, drafts):
 
 def verify_step(W, cfg, x, n):
     """Self-verification step: drafts c_1..c_n from the next-byte and MB heads (c_1 is
-    the greedy byte), verified by extra next-byte passes."""
+    the greedy byte), verified by extra next-byte passes.  ``nt_seen`` holds the
+    next-byte logits after each verified draft prefix."""
     s = step(W, cfg, x, n, tau=2.0)
-    j, gammas = verify_drafts(W, cfg, x, s["cand"])
-    return {"logits": s["logits"], "cand": s["cand"], "prob": s["prob"], "k": j, "gamma": gammas}
+    seen = []
+    j, gammas = verify_drafts(W, cfg, x, s["cand"], seen)
+    return {"logits": s["logits"], "cand": s["cand"], "prob": s["prob"], "k": j, "gamma": gammas,
+            "nt_seen": np.array(seen).reshape(len(seen), 256)}
 
 
 def verify_external(W, cfg, x, drafts):
