@@ -233,7 +233,8 @@ int mbp_get_logits(mbp_handle *h, float *d_logits);
 /* Kernel-class timing, for roofline reporting.  While enabled, every kernel launch
  * the library enqueues is bracketed by a pair of HIP events on the handle's stream,
  * and the algorithmic bytes the launch must move are recorded with it (weights and
- * activations read and written by a linear layer; K/V rows read by attention).
+ * activations read and written by a linear layer; the K/V rows attention must
+ * read, counted once per sequence and layer however many of its rows query them).
  * Classes: weight-streaming GEMV (<= 64 rows), tiled GEMM, attention, other, and
  * persistent-engine launches (a whole transformer stack; their bytes are the
  * weights, activations and K/V rows of every layer they run). */

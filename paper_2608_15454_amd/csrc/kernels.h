@@ -17,6 +17,10 @@ struct Tok {
   const int32_t* kvlen;
   const int32_t* grp;
   int32_t M;
+  // query groups of the decode attention: pairs (first row, rows), each up to 16
+  // consecutive rows of one batch row; nullptr: one query per attention block
+  const int32_t* qg;
+  int32_t nqg;
 };
 
 // Weight rows of one linear layer.  SINGLE: N rows of m[0].  QKV: rows [0,rows) of

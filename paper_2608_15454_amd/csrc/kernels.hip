@@ -860,6 +860,227 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
   }
 }
 
+// Decode attention of several query rows of one sequence on the matrix cores
+// (float16 caches, head size 64).  Block (split s, head h, group g) of four waves: the
+// group is up to 16 consecutive pass rows of one batch row (Tok::qg), and every key
+// and value the block reads serves all of them, so a sequence's K/V leaves HBM once
+// per split however many of its rows the pass holds.  Wave w takes the 32-key tiles
+// at s*chunk + 32w, +128, ...; each tile is loaded with eight lanes per 128-byte key
+// row (four 16-byte loads per lane for the keys, four for the values) and staged in
+// the wave's own LDS tile: keys as [key][dim], values transposed as [dim][key].
+// Then, on v_mfma_f32_16x16x32_f16 (lane l supplies row / column l % 16 and the 8 k
+// positions 8 (l / 16) .. +7 of each 32-wide k step; the accumulator holds rows
+// 4 (l / 16) .. +3 of column l % 16):
+//   S^T [16 keys x 16 queries] = K Q^T per 16-key block, Q^T from registers as
+//     float16 hi + lo (two MFMAs), so lane l owns query l % 16 and keys
+//     4 (l / 16) .. +3 of each block;
+//   the softmax's max and sum over a query's keys: in-lane, then across the four
+//     lanes of the query (lane ^ 16, lane ^ 32);
+//   O^T [16 dims x 16 queries] += V^T P^T over the tile's 32 keys: P^T straight from
+//     the registers (the lane's keys of the two blocks, in the order it holds them: a
+//     contraction may take its k positions in any order), V^T read from the LDS tile
+//     in the same key order.
+// Partials per (query row, head, split) as attn_decode_kernel's; attn_merge_kernel
+// combines the splits.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMqTile = 32;          // keys per wave and round
+constexpr int kMqRound = 4 * kMqTile;  // keys per block and round
+
+__global__ __launch_bounds__(256, 3) void attn_decode_mq_kernel(Attn a, int chunk, int S, float* part) {
+  constexpr int DH = 64, LDK = DH + 8, LDV = kMqTile + 4;  // LDS row pitches in float16 elements
+  // the waves' key and value tiles, and after the key loop their partial outputs
+  __shared__ __attribute__((aligned(16))) union {
+    struct {
+      _Float16 k[4][kMqTile * LDK];
+      _Float16 v[4][DH * LDV];
+    } t;
+    float o[4][16][DH + 1];
+  } lds;
+  __shared__ __attribute__((aligned(16))) int32_t Gs[4][kMqTile];
+  __shared__ float wm[4][16], wl[4][16];
+  const int s = blockIdx.x, h = blockIdx.y, grp = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int col = lane & 15, g4 = lane >> 4;
+  const int t0 = a.tok.qg[2 * grp], cnt = a.tok.qg[2 * grp + 1];
+  const int b = a.tok.b[t0];
+  // this lane's query: row t0 + col of the pass (padding columns repeat row t0 and see
+  // no key)
+  const bool qvalid = col < cnt;
+  const int qrow = t0 + (qvalid ? col : 0);
+  const int kvlen = qvalid ? a.tok.kvlen[qrow] : 0;
+  int kvmax = kvlen;
+  kvmax = max(kvmax, __shfl_xor(kvmax, 1));
+  kvmax = max(kvmax, __shfl_xor(kvmax, 2));
+  kvmax = max(kvmax, __shfl_xor(kvmax, 4));
+  kvmax = max(kvmax, __shfl_xor(kvmax, 8));
+  const int lo = s * chunk, hi = min(lo + chunk, kvmax);
+  const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
+  const int gq = gt != nullptr ? a.tok.grp[qrow] : 0;
+  // Q^T fragments (the B operand of S^T): query col, dims 32 ks + 8 g4 .. +7
+  f16x8 qh[2], ql[2];
+  {
+    const float* qp = a.Q + (size_t)qrow * a.ldq + h * DH + g4 * 8;
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float v = qp[ks * 32 + j] * a.scale;
+        const _Float16 hv = (_Float16)v;
+        qh[ks][j] = hv;
+        ql[ks][j] = (_Float16)(v - (float)hv);
+      }
+  }
+  const size_t base = (size_t)b * a.b_stride + (size_t)h * a.cap * DH;
+  const _Float16* kb = reinterpret_cast<const _Float16*>(a.kc) + base;
+  const _Float16* vb = reinterpret_cast<const _Float16*>(a.vc) + base;
+  _Float16* kt = lds.t.k[wave];
+  _Float16* vt = lds.t.v[wave];
+  // load pattern: lane l takes the 16-byte chunk l % 8 (dims 8 (l % 8) .. +7) of key
+  // pairs (2 (l / 8) + 16 r, + 1), r = 0, 1
+  const int lc = lane & 7, lp = lane >> 3;
+  f32x4 o[4];  // O^T: dims 16 db + 4 g4 + r of query col
+#pragma unroll
+  for (int db = 0; db < 4; ++db) o[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  for (int k0 = lo + kMqTile * wave; k0 < hi; k0 += kMqRound) {
+    uint4 kr[2][2], vr[2][2];
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int j = k0 + 2 * lp + 16 * r + e;
+        if (j < hi) {
+          kr[r][e] = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH + 8 * lc);
+          vr[r][e] = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH + 8 * lc);
+        } else {  // past the split: zeros (no NaN from unwritten slots reaches the sums)
+          kr[r][e] = make_uint4(0u, 0u, 0u, 0u);
+          vr[r][e] = make_uint4(0u, 0u, 0u, 0u);
+        }
+      }
+    if (gt != nullptr && lane < kMqTile) Gs[wave][lane] = k0 + lane < hi ? gt[k0 + lane] : 0;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int kk = 2 * lp + 16 * r;
+#pragma unroll
+      for (int e = 0; e < 2; ++e) *reinterpret_cast<uint4*>(kt + (kk + e) * LDK + 8 * lc) = kr[r][e];
+      // the key pair's values of one dim share a 4-byte word of the transposed tile
+      const uint32_t* v0 = reinterpret_cast<const uint32_t*>(&vr[r][0]);
+      const uint32_t* v1 = reinterpret_cast<const uint32_t*>(&vr[r][1]);
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t lo2 = (v0[w] & 0xffffu) | (v1[w] << 16), hi2 = (v0[w] >> 16) | (v1[w] & 0xffff0000u);
+        *reinterpret_cast<uint32_t*>(vt + (8 * lc + 2 * w) * LDV + kk) = lo2;
+        *reinterpret_cast<uint32_t*>(vt + (8 * lc + 2 * w + 1) * LDV + kk) = hi2;
+      }
+    }
+    // the tile's LDS writes complete before any lane of the wave reads them
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    f32x4 sc[2];
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2) {
+      sc[kb2] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < 2; ++ks) {
+        const f16x8 kf = *reinterpret_cast<const f16x8*>(kt + (16 * kb2 + col) * LDK + 32 * ks + 8 * g4);
+        sc[kb2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, qh[ks], sc[kb2], 0, 0, 0);
+        sc[kb2] = __builtin_amdgcn_mfma_f32_16x16x32_f16(kf, ql[ks], sc[kb2], 0, 0, 0);
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int kk = 16 * kb2 + 4 * g4 + r, j = k0 + kk;
+        bool vis = j < hi && j < kvlen;
+        if (vis && gt != nullptr) {
+          const int gj = Gs[wave][kk];
+          vis = gj == gq || gj == gq - 1;
+        }
+        sc[kb2][r] = vis ? sc[kb2][r] : -INFINITY;
+        mx = fmaxf(mx, sc[kb2][r]);
+      }
+    mx = dev::pair_max<16>(dev::pair_max<32>(mx));  // the query's other keys are in lanes ^ 16, ^ 32
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+    float ls = 0.f;
+#pragma unroll
+    for (int kb2 = 0; kb2 < 2; ++kb2)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const float pv = (sc[kb2][r] == -INFINITY) ? 0.f : expf(sc[kb2][r] - m_new);
+        sc[kb2][r] = pv;
+        ls += pv;
+      }
+    ls = dev::pair_sum<16>(dev::pair_sum<32>(ls));
+    l_run = l_run * alpha + ls;
+    m_run = m_new;
+    // O^T += V^T P^T: k position 8 g4 + j is key 4 g4 + j (j < 4) or 16 + 4 g4 + j - 4
+    f16x8 ph, pl;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float pv = sc[j >> 2][j & 3];
+      const _Float16 hv = (_Float16)pv;
+      ph[j] = hv;
+      pl[j] = (_Float16)(pv - (float)hv);
+    }
+#pragma unroll
+    for (int db = 0; db < 4; ++db) {
+      o[db] *= alpha;
+      const _Float16* row = vt + (16 * db + col) * LDV + 4 * g4;
+      const uint2 v0 = *reinterpret_cast<const uint2*>(row);
+      const uint2 v1 = *reinterpret_cast<const uint2*>(row + 16);
+      const f16x8 vf = __builtin_bit_cast(f16x8, make_uint4(v0.x, v0.y, v1.x, v1.y));
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, ph, o[db], 0, 0, 0);
+      o[db] = __builtin_amdgcn_mfma_f32_16x16x32_f16(vf, pl, o[db], 0, 0, 0);
+    }
+    // every lane's reads of this tile are done before the next round overwrites it
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // the four waves' partial results meet in LDS (over the tiles)
+  __syncthreads();
+  auto& wo = lds.o;
+#pragma unroll
+  for (int db = 0; db < 4; ++db)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) wo[wave][col][16 * db + 4 * g4 + r] = o[db][r];
+  if (g4 == 0) {
+    wm[wave][col] = m_run;
+    wl[wave][col] = l_run;
+  }
+  __syncthreads();
+  for (int e = tid; e < 16 * DH; e += 256) {
+    const int q = e / DH, dd = e % DH;
+    if (q >= cnt) continue;
+    const float mb = fmaxf(fmaxf(wm[0][q], wm[1][q]), fmaxf(wm[2][q], wm[3][q]));
+    float num = 0.f, den = 0.f;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      if (wm[w][q] != -INFINITY) {
+        const float ew = expf(wm[w][q] - mb);
+        num += ew * wo[w][q][dd];
+        den += ew * wl[w][q];
+      }
+    }
+    const int i = t0 + q;
+    if (S == 1) {
+      a.O[(size_t)i * a.ldo + h * DH + dd] = den > 0.f ? num / den : 0.f;
+    } else {
+      float* pp = part + (((size_t)i * a.H + h) * S + s) * (DH + 2);
+      pp[dd] = num;
+      if (dd == 0) {
+        pp[DH] = mb;
+        pp[DH + 1] = den;
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ row kernels ------
 template <typename W>
 __global__ void embed_kernel(const W* emb, const int32_t* bytes, float* X, int d) {
@@ -1483,8 +1704,39 @@ hipError_t attn_decode_dh(const Attn& a, int max_kv, float* part, int64_t part_f
                  a.O, a.ldo);
 }
 
+// The multi-query kernel: splits sized so that about 2048 blocks (splits x heads x
+// query groups) stream the keys, each split a multiple of the keys the four waves
+// take per round.
+hipError_t attn_decode_mq(const Attn& a, int max_kv, float* part, int64_t part_floats, hipStream_t st,
+                          const Ev& ev) {
+  constexpr int DH = 64;
+  const int M = a.tok.M, items = a.H * a.tok.nqg;
+  int S = std::max(1, std::min((max_kv + kMqRound - 1) / kMqRound, (2048 + items - 1) / items));
+  int chunk = ((max_kv + S - 1) / S + kMqRound - 1) / kMqRound * kMqRound;
+  S = std::max(1, (max_kv + chunk - 1) / chunk);
+  while (S > 1 && (S > kMaxSplits || (int64_t)M * a.H * S * (DH + 2) > part_floats)) {
+    chunk *= 2;
+    S = (max_kv + chunk - 1) / chunk;
+  }
+  if (S <= 1) {
+    return klaunch(attn_decode_mq_kernel, dim3(1, a.H, a.tok.nqg), dim3(256), 0, st, ev.start, ev.stop, a,
+                   std::max(max_kv, 1), 1, part);
+  }
+  hipError_t e = klaunch(attn_decode_mq_kernel, dim3(S, a.H, a.tok.nqg), dim3(256), 0, st, ev.start, nullptr, a,
+                         chunk, S, part);
+  if (e != hipSuccess) return e;
+  return klaunch(attn_merge_kernel<DH>, dim3(a.H, M), dim3(256), 0, st, nullptr, ev.stop, (const float*)part, S, a.H,
+                 a.O, a.ldo);
+}
+
 template <typename KV>
 hipError_t attn_decode_t(const Attn& a, int max_kv, float* part, int64_t part_floats, hipStream_t st, const Ev& ev) {
+  // the multi-query kernel once the pass holds at least two rows per sequence on
+  // average; with one row per sequence every key is read once either way, and the
+  // one-query kernel's short blocks stream them faster
+  if constexpr (std::is_same<KV, _Float16>::value)
+    if (a.dh == 64 && a.tok.qg != nullptr && a.tok.nqg > 0 && a.tok.M >= 2 * a.tok.nqg)
+      return attn_decode_mq(a, max_kv, part, part_floats, st, ev);
   if (a.dh == 64) return attn_decode_dh<KV, 64>(a, max_kv, part, part_floats, st, ev);
   return attn_decode_dh<KV, 32>(a, max_kv, part, part_floats, st, ev);
 }

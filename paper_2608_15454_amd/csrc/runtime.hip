@@ -333,6 +333,8 @@ struct EngStack {
 
 struct TokOffs {
   size_t b, pos, slot, kvlen, grp;
+  size_t qg;    // query groups of the decode attention (Tok::qg)
+  int32_t nqg;
   size_t first;       // index of the first token of the same batch row (rows are contiguous)
   size_t first_slot;  // slot of that token
   int32_t max_ns;     // largest such slot
@@ -536,6 +538,18 @@ TokOffs add_toks(Plan& p, const Toks& t) {
   }
   o.first = p.add(first);
   o.first_slot = p.add(first_slot);
+  // runs of up to 16 consecutive rows of one batch row share their keys in the
+  // decode attention
+  std::vector<int32_t> qg;
+  for (int i = 0; i < t.size();) {
+    int j = i + 1;
+    while (j < t.size() && j - i < 16 && t.b[j] == t.b[i]) ++j;
+    qg.push_back(i);
+    qg.push_back(j - i);
+    i = j;
+  }
+  o.qg = p.add(qg);
+  o.nqg = (int32_t)qg.size() / 2;
   return o;
 }
 
@@ -547,6 +561,8 @@ Tok dev_tok(const Plan& p, const TokOffs& o, int M) {
   t.kvlen = p.at(o.kvlen);
   t.grp = p.at(o.grp);
   t.M = M;
+  t.qg = p.at(o.qg);
+  t.nqg = o.nqg;
   return t;
 }
 
@@ -566,7 +582,8 @@ std::vector<int32_t> make_tiles(const Toks& t) {
 }
 
 // Algorithmic bytes of one pass of M rows through a stack: every linear layer's
-// weights, inputs and outputs, and the K/V rows the queries read.
+// weights, inputs and outputs, and the K/V rows of each batch row's visible keys
+// (once per sequence and layer, however many of its rows the pass holds).
 double stack_bytes(const mbp_handle* h, int nlayers, int M, double kv_rows) {
   const Sizes& s = h->sz;
   const double wb = h->wdt ? 2.0 : 4.0, d = s.d, f = s.dff;
@@ -602,8 +619,9 @@ int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, co
 }
 
 // One transformer stack over the token rows in X (residual stream, [M, d]) on stream
-// st with scratch sc, one kernel per operation.  kv_rows: total visible cache rows
-// over the pass's queries.
+// st with scratch sc, one kernel per operation.  kv_rows: cache rows the pass must
+// read, counted once per batch row (the keys its last query sees), whatever number of
+// its queries see them.
 int run_stack(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, float* X, const Tok& tok,
               const int32_t* grp_tab, bool tiled, const int32_t* tiles, int ntiles, int max_kv, double kv_rows,
               const Scratch& sc, hipStream_t st) {
@@ -778,8 +796,8 @@ int mb_prepare(mbp_handle* h, int n, Plan& p, bool clamp, MbPass* out) {
       zrow.push_back(b * s.Kcap + G);
       wrow.push_back(rg.row_mbh + b * s.Wcap + w);
       max_w = std::max(max_w, w + 1);
-      kvr_m += w + 1;
     }
+    if (W > r.win_valid) kvr_m += W;  // the row's window keys, read once for all its new rows
     r.win_valid = std::max(r.win_valid, W);
   }
   if (tm.size() == 0) return MBP_OK;
@@ -888,11 +906,12 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
       bytes.push_back(byte);
       he_row.push_back(b * s.Tcap + pos);
       max_kv_e = std::max(max_kv_e, pos + 1);
-      kvr_e += pos + 1;
+      const bool row_last = it + 1 == last || items[it + 1].b != b;
+      if (row_last) kvr_e += pos + 1;  // the row's keys, read once for all its new bytes
       // the NT output of the last new byte of a row is its h1 row (in a full-sequence
       // forward, every NT output is kept, at its position)
       if (h->fwd_h) h1_dst.push_back(pos);
-      else h1_dst.push_back(it + 1 == last || items[it + 1].b != b ? h->rg.row_h1 + b : -1);
+      else h1_dst.push_back(row_last ? h->rg.row_h1 + b : -1);
     }
     const int Me = te.size();
     const bool tiled_e = Me >= 16 * (int)rows_in_chunk.size();
@@ -925,7 +944,9 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
       HIPCK(h, hipMemcpyAsync(h->h_bpz, X, (size_t)Me * 4, hipMemcpyDeviceToHost, h->st));
       HIPCK(h, hipStreamSynchronize(h->st));
     }
-    // segmentation: a closed segment becomes an LM token (BOS first on a fresh row)
+    // segmentation: a closed segment becomes an LM token (BOS first on a fresh row);
+    // lm_keys[b]: latent keys row b's LM tokens see (read once for all of them)
+    std::vector<int32_t> lm_keys(h->batch, 0);
     for (size_t it = first; it < last; ++it) {
       const int k = (int)(it - first);
       const int b = items[it].b;
@@ -938,7 +959,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
         r.lm_rows = 1;
         r.epoch++;
         max_kv_l = std::max(max_kv_l, 1);
-        kvr_l += 1;
+        lm_keys[b] = 1;
       }
       const int32_t pos = te.pos[k];
       const int32_t prev = r.q.empty() ? -1 : r.q.back();
@@ -953,10 +974,11 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
         r.lm_rows = j + 1;
         r.epoch++;
         max_kv_l = std::max(max_kv_l, j + 1);
-        kvr_l += j + 1;
+        lm_keys[b] = j + 1;
       }
       nt_src.push_back(b * s.Kcap + (int32_t)r.q.size());  // the latent of this byte's group
     }
+    for (int32_t v : lm_keys) kvr_l += v;
     const int Ml = tl.size();
     const bool tiled_l = Ml >= 16 * (int)rows_in_chunk.size();
     std::vector<int32_t> tiles_l = make_tiles(tl);
@@ -1583,12 +1605,13 @@ extern "C" int mbp_forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, con
         return done(fail(h, MBP_EHIP, "forward synchronize"));
       Toks tm;
       std::vector<int32_t> zrow, orow;
-      double kvr = 0;
+      // keys the chunk's queries see: from the first byte of the group before the
+      // chunk's first query's group up to its last query
+      const double kvr = c1 - (G[c0] >= 2 ? r.q[G[c0] - 2] : 0);
       for (int i = c0; i < c1; ++i) {
         tm.push(0, i, i, i + 1, G[i]);
         zrow.push_back(G[i]);  // latent row of group G[i] in batch row 0
         orow.push_back(i);
-        kvr += i + 1 - (G[i] >= 1 ? (G[i] >= 2 ? r.q[G[i] - 2] : 0) : 0);
       }
       const std::vector<int32_t> tiles = make_tiles(tm);
       p.clear();
