@@ -290,6 +290,24 @@ size_t mbp_forward_workspace_bytes(const mbp_config *cfg, int32_t T);
 int mbp_forward(mbp_handle *h, const uint8_t *h_bytes, int32_t T, const mbp_loss_params *lp, void *d_work,
                 size_t work_bytes, float *d_nll, float *d_loss);
 
+/* mbp_forward for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same forward,
+ * with its scratch taken from a fixed device array inside the library instead of a
+ * caller workspace.  The array holds mbp_forward_static_max_bytes() bytes (64 MiB);
+ * a sequence whose mbp_forward_workspace_bytes(cfg, T) exceeds that is rejected with
+ * MBP_ECAPACITY before any device work.  The call allocates nothing: no hipMalloc,
+ * hipFree or allocating library routine.  Each GPU holds one copy of the array for
+ * the life of the process, shared by every call on that GPU from every handle: calls
+ * that overlap on one GPU (different streams, handles or threads) race on it, so the
+ * caller keeps them ordered.  Every byte of it that a call reads is written earlier
+ * in the same call.  Arguments, results and errors as mbp_forward (MBP_EHIP if the
+ * array's device address could not be obtained at mbp_init). */
+int mbp_forward_static(mbp_handle *h, const uint8_t *h_bytes, int32_t T, const mbp_loss_params *lp, float *d_nll,
+                       float *d_loss);
+
+/* Size in bytes of the fixed scratch array of mbp_forward_static. */
+size_t mbp_forward_static_max_bytes(void);
+
 /* Segment ends of row r (Section 2.2, encoder module): the 0-based positions of the
  * bytes that closed a segment, ascending, among the bytes segmented so far (a byte
  * the verifier appended stays unsegmented until the next step commits it).  Writes

@@ -101,6 +101,10 @@ def lib():
     L.mbp_forward_workspace_bytes.restype = ctypes.c_size_t
     L.mbp_forward.argtypes = [P, P, ctypes.c_int32, P, P, ctypes.c_size_t, P, P]
     L.mbp_forward.restype = ctypes.c_int
+    L.mbp_forward_static.argtypes = [P, P, ctypes.c_int32, P, P, P]
+    L.mbp_forward_static.restype = ctypes.c_int
+    L.mbp_forward_static_max_bytes.argtypes = []
+    L.mbp_forward_static_max_bytes.restype = ctypes.c_size_t
     L.mbp_reset.argtypes = [P]
     L.mbp_reset.restype = ctypes.c_int
     L.mbp_destroy.argtypes = [P]
@@ -243,6 +247,20 @@ class Decoder:
         self._check(self.L.mbp_forward(self.h, seq.ctypes.data, T, ctypes.byref(lp),
                                        ctypes.c_void_p(work.data_ptr()), work.numel(),
                                        ctypes.c_void_p(nll.data_ptr()), ctypes.c_void_p(loss.data_ptr())))
+        self.batch = 0
+        return nll, loss
+
+    def forward_static(self, seq, lam0=1.0, lam1=1.0, lam2=1.0, alpha=1.0, beta=0.0):
+        """forward() on the library's fixed scratch array (mbp_forward_static): no
+        workspace is passed or allocated.  Returns device tensors nll [2, T], loss [6]."""
+        torch = self.torch
+        seq = np.ascontiguousarray(seq, dtype=np.uint8)
+        T = len(seq)
+        nll = torch.zeros((2, T), dtype=torch.float32, device=self.device)
+        loss = torch.zeros((6,), dtype=torch.float32, device=self.device)
+        lp = LossParams(lam0, lam1, lam2, alpha, beta)
+        self._check(self.L.mbp_forward_static(self.h, seq.ctypes.data, T, ctypes.byref(lp),
+                                              ctypes.c_void_p(nll.data_ptr()), ctypes.c_void_p(loss.data_ptr())))
         self.batch = 0
         return nll, loss
 

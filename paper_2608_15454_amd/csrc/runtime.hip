@@ -20,6 +20,7 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -29,7 +30,35 @@
 
 using namespace mbp;
 
+// Scratch of mbp_forward_static: a fixed device array in place of the caller's
+// workspace, for callers that cannot allocate device memory.  Each GPU the library
+// runs on holds its own copy until the process ends.  Host code never passes the
+// array's name to a kernel or copy: it uses the device address that
+// hipGetSymbolAddress returns for the current device (static_scratch()).
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+static __device__ __align__(256) unsigned char scratch[kStaticScratchBytes];
+
 namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+
+// Device address of `scratch` on device dev, which must be current; looked up once
+// per device.
+hipError_t static_scratch(int dev, void** out) {
+  *out = nullptr;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev] == nullptr) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return hipSuccess;
+}
 
 constexpr int kMaxN = 8;
 constexpr int kParts = 9;  // tensors per transformer block in the manifest
@@ -361,6 +390,10 @@ struct mbp_handle {
   char* ws;
   bool poisoned = false;
   std::string err;
+  // device address of the static scratch on the handle's device (nullptr when the
+  // lookup failed at mbp_init; scratch_err says why)
+  void* scratch = nullptr;
+  std::string scratch_err;
 
   const void* emb;
   const void* unembed;
@@ -1337,6 +1370,16 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
     mbp_destroy(h);
     return MBP_EHIP;
   };
+  {
+    int dev = -1;
+    hipError_t se = hipGetDevice(&dev);
+    if (se == hipSuccess) se = static_scratch(dev, &h->scratch);
+    if (se != hipSuccess) {
+      h->scratch = nullptr;
+      h->scratch_err = std::string("static scratch unavailable: ") + hipGetErrorString(se);
+      (void)hipGetLastError();  // the failed lookup must not surface in a later call
+    }
+  }
   hipError_t e = hipStreamCreateWithFlags(&h->st2, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_mb, hipEventDisableTiming);
@@ -1536,8 +1579,8 @@ extern "C" size_t mbp_forward_workspace_bytes(const mbp_config* cfg, int32_t T) 
   return fwd_layout(*cfg, T).total;
 }
 
-extern "C" int mbp_forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, const mbp_loss_params* lp,
-                           void* d_work, size_t work_bytes, float* d_nll, float* d_loss) {
+static int forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, const mbp_loss_params* lp, void* d_work,
+                   size_t work_bytes, float* d_nll, float* d_loss) {
   int rc = check_ready(h);
   if (rc) return rc;
   const Sizes& s = h->sz;
@@ -1640,6 +1683,27 @@ extern "C" int mbp_forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, con
                     lp->lambda1, lp->lambda2, lp->alpha, lp->beta, d_loss, h->st) != hipSuccess)
     return done(fail(h, MBP_EHIP, "loss launch"));
   return done(MBP_OK);
+}
+
+extern "C" int mbp_forward(mbp_handle* h, const uint8_t* h_bytes, int32_t T, const mbp_loss_params* lp,
+                           void* d_work, size_t work_bytes, float* d_nll, float* d_loss) {
+  return forward(h, h_bytes, T, lp, d_work, work_bytes, d_nll, d_loss);
+}
+
+extern "C" size_t mbp_forward_static_max_bytes(void) { return kStaticScratchBytes; }
+
+extern "C" int mbp_forward_static(mbp_handle* h, const uint8_t* h_bytes, int32_t T, const mbp_loss_params* lp,
+                                  float* d_nll, float* d_loss) {
+  int rc = check_ready(h);
+  if (rc) return rc;
+  if (h->scratch == nullptr) return fail(h, MBP_EHIP, h->scratch_err);
+  if (!h_bytes || !lp || !d_nll || !d_loss || T < 1) return fail(h, MBP_EINVAL, "bad forward arguments");
+  const size_t need = fwd_layout(h->cfg, T).total;
+  if (need > kStaticScratchBytes)
+    return fail(h, MBP_ECAPACITY, "forward of " + std::to_string(T) + " bytes needs " + std::to_string(need) +
+                                      " bytes of scratch; the static scratch holds " +
+                                      std::to_string(kStaticScratchBytes));
+  return forward(h, h_bytes, T, lp, h->scratch, kStaticScratchBytes, d_nll, d_loss);
 }
 
 // Commits every row's pending bonus byte (external verification), so that the caches
