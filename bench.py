@@ -39,7 +39,11 @@ def parse():
     ap.add_argument("--n", type=int, default=None)
     ap.add_argument("--tau", type=float, default=None)
     ap.add_argument("--logit-gain", type=float, default=1.0)
-    ap.add_argument("--cpu-steps", type=int, default=2, help="oracle steps timed for cpu_baseline (0 = skip)")
+    ap.add_argument("--cpu-steps", type=int, default=1,
+                    help="float64 full-recompute oracle steps timed beside the cached CPU baseline (0 = skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="seconds of float32 KV-cached CPU decoding timed, on all cores and on one (0 = skip)")
+    ap.add_argument("--no-batch64", action="store_true", help="default workload only: skip the batch-64 runs")
     ap.add_argument("--no-timing-pass", action="store_true")
     ap.add_argument("--no-engine", action="store_true", help="one kernel launch per layer operation")
     return ap.parse_args()
@@ -224,7 +228,7 @@ def bench_forward(args, wl):
     out = {
         "metric": "full-sequence forward bytes/s", "value": round(value, 1), "unit": "bytes/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(elapsed * 1000.0 / K, 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "scaling": "weak", "vs_baseline": None, "dtype": model.dtype, "data": "synthetic",
         "config": {"workload": f"{wl.name}: d={model.d_model} heads={model.n_heads} layers enc/lm/nt/mb="
                                f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb}, one {T}-byte sequence, "
                                f"{len(q)} segments, both heads at every position and the losses",
@@ -238,42 +242,82 @@ def bench_forward(args, wl):
     print(json.dumps(out), flush=True)
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU; the decode rows are independent and would shard "
-              "by batch row with no per-step exchange, but no multi-GPU run is provided.", file=sys.stderr)
-        sys.exit(2)
+def prefill_flops(model, lens, qs):
+    """Algorithmic flops of a batch prefill: (linear, attention).  Linear: 2 per weight
+    per row (encoder and NT layers on every prompt byte, the LM module on BOS and every
+    closed segment).  Attention: 4 d per visible (query, key) pair, causal per row in
+    the encoder, NT decoder and LM module."""
+    d, dff = model.d_model, model.d_ff
+    per_layer = 4 * d * d + 3 * d * dff
+    T = sum(lens)
+    K1 = [len(q) + 1 for q in qs]
+    linear = 2.0 * per_layer * (T * (model.n_enc + model.n_nb) + sum(K1) * model.n_lm)
+    pairs = sum((model.n_enc + model.n_nb) * L * (L + 1) / 2 + model.n_lm * k * (k + 1) / 2 for L, k in zip(lens, K1))
+    return linear, 4.0 * d * pairs
 
-    import numpy as np
+
+def cpu_cached_baseline(model, weights, prompt, n, tau, mode, seconds):
+    """The float32 KV-cached CPU decoder (oracle/cached.py) on row 0 of the workload:
+    one prefill (reported, untimed), then steps for about ``seconds`` on all BLAS
+    threads, and from the same prefilled state again on one thread."""
+    import copy
+
+    from threadpoolctl import threadpool_limits
+
+    from oracle.cached import CachedDecoder
+
+    dec = CachedDecoder(weights, model, cap=len(prompt) + 4096)
+    p0 = time.perf_counter()
+    dec.prefill([int(b) for b in prompt])
+    pre = time.perf_counter() - p0
+    start = copy.deepcopy(dec)
+    out = {"prefill_s": pre}
+    for label, threads in (("all", None), ("one", 1)):
+        d = copy.deepcopy(start)
+        with threadpool_limits(limits=threads):
+            got, steps = 0, 0
+            c0 = time.perf_counter()
+            while time.perf_counter() - c0 < seconds:
+                if mode == "verify":
+                    got += d.verify_step(n)["k"]
+                else:
+                    r = d.step(n, tau)
+                    acc = [int(c) for c in r["cand"][: r["k"]]]
+                    d.accept(acc)
+                    got += len(acc)
+                steps += 1
+            cs = time.perf_counter() - c0
+        out[label] = {"value": got / cs, "steps": steps, "seconds": cs, "cores": cpu_threads() if threads is None else 1}
+    return out
+
+
+def bench_decode(args, wl, K, W, logit_gain, cpu_seconds=0.0, weights=None):
+    """The decode loop of one workload: value, roofline of the dominant kernel class,
+    the batch prefill's matrix-core figure, and (cpu_seconds > 0) the CPU baselines."""
     import torch
 
     import synth
     from paper_2608_15454_amd import SELF_VERIFY, THRESHOLD, Decoder, make_config
 
-    wl = synth.WORKLOADS[args.workload]
-    if wl.mode == "forward":
-        return bench_forward(args, wl)
-    args.steps = 1024 if args.steps is None else args.steps
-    args.warmup = 16 if args.warmup is None else args.warmup
     model = wl.model
     n = args.n or wl.n
     tau = wl.tau if args.tau is None else args.tau
     mode = SELF_VERIFY if wl.mode == "verify" else THRESHOLD
     ext = wl.mode == "external"
-    B, K, W = wl.batch, args.steps, args.warmup
-    log(f"[bench] workload {wl.name} B={B} prompt={wl.prompt_len} n={n} tau={tau} steps={K} warmup={W}")
+    B = wl.batch
+    log(f"[bench] workload {wl.name} B={B} prompt={wl.prompt_len} n={n} tau={tau} logit_gain={logit_gain} "
+        f"steps={K} warmup={W}")
 
     t0 = time.time()
-    weights = synth.make_weights(model, seed=0, logit_gain=args.logit_gain)
+    if weights is None:
+        weights = synth.make_weights(model, seed=0, logit_gain=logit_gain)
     prompts = [synth.make_prompt(r, wl.prompt_len) for r in range(B)]
     max_ctx = wl.prompt_len + (max(K, W) + 2) * (n + 1) + 16
     max_n = max(n + 1 if ext else n, 8)
     dec = Decoder(make_config(model, max_batch=B, max_ctx=max_ctx, max_n=max_n, engine=not args.no_engine), weights)
     ver, vweights = None, None
     if ext:
-        vweights = synth.make_weights(wl.verifier, seed=1, logit_gain=args.logit_gain)
+        vweights = synth.make_weights(wl.verifier, seed=1, logit_gain=logit_gain)
         ver = Decoder(make_config(wl.verifier, max_batch=B, max_ctx=max_ctx, max_n=max_n, engine=not args.no_engine),
                       vweights)
     decs = [dec] + ([ver] if ext else [])
@@ -293,42 +337,66 @@ def main():
         else:
             run_steps(dec, steps, n, tau, mode, samp)
 
-    t0 = time.time()
-    for d in decs:
-        d.prefill(prompts)
-    torch.cuda.synchronize()
-    log(f"[bench] prefill {time.time() - t0:.2f}s")
+    stream = torch.cuda.current_stream()
+
+    def timed(fn):
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        ev0.record(stream)
+        w0 = time.perf_counter()
+        fn()
+        ev1.record(stream)
+        torch.cuda.synchronize()
+        return max(time.perf_counter() - w0, ev0.elapsed_time(ev1) / 1000.0)
+
+    pre_s = timed(lambda: [d.prefill(prompts) for d in decs])
+    log(f"[bench] prefill {pre_s * 1000:.1f} ms")
     run(W)
     torch.cuda.synchronize()
     log("[bench] warm-up done")
 
-    # ---- timed pass
+    # ---- prefill again, timed, then the timed decode steps
     for d in decs:
         d.reset()
-        d.prefill(prompts)
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    w0 = time.perf_counter()
-    run(K)
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - w0
-    gpu_ms = ev0.elapsed_time(ev1)
+    pre_s = timed(lambda: [d.prefill(prompts) for d in decs])
+    elapsed = timed(lambda: run(K))
     lens = [(ver if ext else dec).row_length(b) for b in range(B)]
     accepted = sum(L - wl.prompt_len for L in lens)
-    elapsed = max(wall, gpu_ms / 1000.0)
     value = accepted / elapsed
     log(f"[bench] timed: {K} steps {elapsed * 1000:.1f} ms, accepted {accepted} bytes, {value:.1f} B/s")
 
-    # ---- kernel timing pass (identical steps, launches bracketed by HIP events)
-    roofline, classes, timing_step_ms = None, {}, None
+    # ---- kernel timing pass (identical prefill and steps, launches bracketed by HIP events)
+    roofline, classes, timing_step_ms, prefill = None, {}, None, None
     if not args.no_timing_pass:
         for d in decs:
             d.reset()
-            d.prefill(prompts)
             d.set_timing(True)
+        for d in decs:
+            d.prefill(prompts)
+        pcls = {}
+        for d in decs:
+            for k, v in d.read_timing().items():
+                c = pcls.get(k, (0, 0.0, 0.0))
+                pcls[k] = (c[0] + v[0], c[1] + v[1], c[2] + v[2])
+            d.set_timing(False)
+            d.set_timing(True)  # clears the totals: the decode steps are counted alone
+        qs = [[int(v) for v in dec.row_boundaries(b)] for b in range(B)]
+        lin, att = prefill_flops(model, [wl.prompt_len] * B, qs)
+        mfma = model.dtype == "bf16"
+        peak = MFMA_BF16_PEAK_TFLOPS if mfma else VALU_FP32_PEAK_TFLOPS
+        gemm_ms = pcls["gemm"][1]
+        prefill = {
+            "ms": round(pre_s * 1000.0, 3), "tflop": round((lin + att) / 1e12, 3),
+            "achieved_tflops": round((lin + att) / pre_s / 1e12, 2),
+            "frac_of_peak": round((lin + att) / pre_s / 1e12 / peak, 4),
+            "linear": {"tflop": round(lin / 1e12, 3), "kernel_ms": round(gemm_ms, 3),
+                       "achieved_tflops": round(lin / (gemm_ms / 1000.0) / 1e12, 2) if gemm_ms > 0 else None,
+                       "frac_of_peak": round(lin / (gemm_ms / 1000.0) / 1e12 / peak, 4) if gemm_ms > 0 else None},
+            "peak_tflops": peak, "unit": "TFLOP/s", "bound": "mfma" if mfma else "alu",
+            "kernel_classes": {k: {"launches": v[0], "ms": round(v[1], 3)} for k, v in pcls.items()},
+        }
+        log(f"[bench] prefill {prefill['tflop']} TFLOP in {prefill['ms']} ms: {prefill['achieved_tflops']} TFLOP/s; "
+            f"linear layers {prefill['linear']['achieved_tflops']} TFLOP/s in their kernels")
         cal_src = torch.empty(COPY_CAL_BYTES // 4, dtype=torch.float32, device="cuda").fill_(1.0)
         cal_dst = torch.empty_like(cal_src)
         torch.cuda.synchronize()
@@ -358,9 +426,20 @@ def main():
         log(f"[bench] kernel classes: " + ", ".join(f"{k}: {v[0]} launches {v[1]:.1f} ms {v[2] / 1e9:.2f} GB"
                                                      for k, v in classes.items()))
 
-    # ---- CPU oracle beside it
+    # ---- CPU baselines beside it
     cpu = None
-    if args.cpu_steps > 0:
+    if cpu_seconds > 0 and not ext and not samp and model.boundary == "space":
+        c = cpu_cached_baseline(model, weights, prompts[0], n, tau, wl.mode, cpu_seconds)
+        cpu = {"value": round(c["all"]["value"], 3), "unit": "accepted bytes/s", "cores": c["all"]["cores"],
+               "kind": "oracle",
+               "sample": f"batch row 0 of the same workload: {c['all']['steps']} steps ({c['all']['seconds']:.1f}s) "
+                         f"after its {wl.prompt_len}-byte prefill ({c['prefill_s']:.1f}s, untimed), float32 "
+                         f"KV-cached decoder of the oracle package (oracle/cached.py)",
+               "one_core": {"value": round(c["one"]["value"], 3), "cores": 1, "steps": c["one"]["steps"],
+                            "seconds": round(c["one"]["seconds"], 2)}}
+        log(f"[bench] cpu cached decoder: {cpu['value']} B/s on {cpu['cores']} threads, "
+            f"{cpu['one_core']['value']} B/s on one")
+    if cpu_seconds > 0 and args.cpu_steps > 0:
         import oracle
 
         W64 = oracle.to_float64(weights)
@@ -368,7 +447,8 @@ def main():
         got = 0
         c0 = time.perf_counter()
         V64 = oracle.to_float64(vweights) if ext else None
-        for got_steps in range(args.cpu_steps if not ext else min(args.cpu_steps, 1)):
+        nsteps = args.cpu_steps if not ext else min(args.cpu_steps, 1)
+        for got_steps in range(nsteps):
             if ext:
                 r = oracle.verify_external(V64, wl.verifier, x, oracle.step(W64, model, x, n, tau)["cand"])
                 acc = [int(c) for c in r["bytes"]]
@@ -386,25 +466,19 @@ def main():
             x += acc
             got += len(acc)
         cs = time.perf_counter() - c0
-        cpu = {"value": round(got / cs, 4), "unit": "accepted bytes/s", "cores": cpu_threads(), "kind": "oracle",
-               "sample": f"{1 if ext else args.cpu_steps} steps of batch row 0 of the same workload (float64 full "
-                         f"recompute, {cs:.1f}s)"}
-        log(f"[bench] cpu oracle {got} bytes in {cs:.1f}s")
+        full = {"value": round(got / cs, 4), "unit": "accepted bytes/s", "cores": cpu_threads(), "kind": "oracle",
+                "sample": f"{nsteps} steps of batch row 0 of the same workload (float64 full recompute, {cs:.1f}s)"}
+        log(f"[bench] cpu oracle (full recompute) {got} bytes in {cs:.1f}s")
+        if cpu is None:
+            cpu = full
+        else:
+            cpu["full_recompute"] = full
 
     step_bytes = sum(v[2] for v in classes.values()) / K if classes else None
-    out = {
-        "metric": "accepted bytes/sec per MI355X (MBP decode)",
+    return {
         "value": round(value, 2),
-        "unit": "accepted bytes/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
         "ms_per_step": round(elapsed * 1000.0 / K, 4),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
+        "steps": K, "warmup": W,
         "config": {
             "workload": f"{wl.name}: d={model.d_model} heads={model.n_heads} layers enc/lm/nt/mb="
                         f"{model.n_enc}/{model.n_lm}/{model.n_nb}/{model.n_mb} head={model.head}, "
@@ -415,11 +489,12 @@ def main():
                            if model.boundary == "learned" else "")
                         + f"batch {B}, prompt {wl.prompt_len} bytes, n={n}, tau={tau}",
             "batch": B, "prompt_len": wl.prompt_len, "n": n, "tau": tau, "mode": wl.mode,
-            "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32",
-            "logit_gain": args.logit_gain, "max_patch": model.max_patch, "boundary": model.boundary,
+            "weights": model.dtype, "kv_cache": "f16" if model.dtype == "bf16" else "f32", "accumulate": "f32",
+            "logit_gain": logit_gain, "max_patch": model.max_patch, "boundary": model.boundary,
         },
         "roofline": roofline,
         "cpu_baseline": cpu,
+        "prefill": prefill,
         "steps_per_s": round(K / elapsed, 2),
         "mean_accepted_per_step": round(accepted / (K * B), 4),
         "step_algorithmic_bytes": round(step_bytes) if step_bytes else None,
@@ -427,7 +502,42 @@ def main():
         "timing_pass_ms_per_step": round(timing_step_ms, 4) if timing_step_ms else None,
         "kernel_classes": {k: {"launches": v[0], "ms": round(v[1], 3), "GB": round(v[2] / 1e9, 4)}
                            for k, v in classes.items()},
+        "_weights": weights,
     }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py: this build measures one GPU; the decode rows are independent and would shard "
+              "by batch row with no per-step exchange, but no multi-GPU run is provided.", file=sys.stderr)
+        sys.exit(2)
+
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    if wl.mode == "forward":
+        return bench_forward(args, wl)
+    K = 1024 if args.steps is None else args.steps
+    W = 16 if args.warmup is None else args.warmup
+    head = bench_decode(args, wl, K, W, args.logit_gain, cpu_seconds=args.cpu_seconds)
+    weights = head.pop("_weights")
+    out = {"metric": "accepted bytes/sec per MI355X (MBP decode)", "value": head.pop("value"),
+           "unit": "accepted bytes/s", "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": head.pop("ms_per_step"),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.model.dtype,
+           "data": "synthetic"}
+    head.pop("steps"), head.pop("warmup")
+    out.update(head)
+    if args.workload == "lca_d1024_b1" and not args.no_batch64:
+        # the metric's batch-64 half: the same model and weights at batch 64, as the
+        # workload specifies it (logit gain 1), and with ragged acceptance (gain 8)
+        b64 = synth.WORKLOADS["lca_d1024_b64"]
+        for key, gain in (("batch64", args.logit_gain), ("batch64_ragged", 8.0)):
+            r = bench_decode(args, b64, K, W, gain, weights=weights if gain == args.logit_gain else None)
+            r.pop("_weights")
+            r.pop("cpu_baseline")
+            out[key] = r
     print(json.dumps(out), flush=True)
 
 
