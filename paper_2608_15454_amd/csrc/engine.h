@@ -130,5 +130,16 @@ int engine_grid(int shape);
 // while it runs (the caller keeps the engine's launches on one stream).
 hipError_t launch_engine(int shape, const EOp* ops, int nlayers, const ECall& call, uint32_t base, int* err,
                          hipStream_t st, const Ev& ev = Ev());
+// Blocks of a launch of two stacks side by side (launch_engine_split), 0 if unavailable.
+int engine_split_grid(int shape);
+// Two independent single-row stack passes (call.M == 1 each) in one launch: blocks
+// [0, nbA) run A's operations and the other blocks B's (e.g. the next-byte decoder
+// and the next step's MB window update, both of which read only rows written before
+// the launch).  Each call's attention splits must be sized for its own part of the
+// grid.  The op lists must use disjoint tagged buffers; tags are relative to baseA /
+// baseB.  Same waiting and timeout rules as launch_engine.
+hipError_t launch_engine_split(int shape, const EOp* opsA, int nA, const ECall& cA, uint32_t baseA, int nbA,
+                               const EOp* opsB, int nB, const ECall& cB, uint32_t baseB, int* err, hipStream_t st,
+                               const Ev& ev = Ev());
 
 }  // namespace mbp

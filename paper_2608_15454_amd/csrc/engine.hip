@@ -311,6 +311,12 @@ __device__ __forceinline__ uint32_t touch_lines(const CONST_AS EOp* op, bool att
   return attn ? (w[50] ^ w[73]) : (w[2] ^ w[18] ^ w[34] ^ w[49]);
 }
 
+// The blocks a stack pass runs on: block bid of nb (the whole grid, or one part of
+// it when a launch runs two stacks side by side).
+struct VG {
+  int bid, nb;
+};
+
 // ------------------------------------------------------------------ linear ----
 // A block computes tiles of RB = (EW / NS) * R consecutive output rows.  The waves of
 // a block form EW / NS row groups of NS waves; wave (group g, slice s) holds rows
@@ -494,11 +500,11 @@ __device__ __forceinline__ void load_g(const ELinear& L, int kc0, float4 (&gv)[G
 }
 
 template <typename W, int KC, int NS, int R, bool NORM>
-__device__ __forceinline__ void weights_ahead(const ELinear& L, WPre<W, KC, NS, R, NORM>& p) {
+__device__ __forceinline__ void weights_ahead(const ELinear& L, WPre<W, KC, NS, R, NORM>& p, const VG& g) {
   constexpr int RB = (EW / NS) * R, KCW = KC / NS;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int kc0 = (wave % NS) * KCW;
-  load_w<W, R, KCW>(L, blockIdx.x * RB + (wave / NS) * R, kc0, p.wv);
+  load_w<W, R, KCW>(L, g.bid * RB + (wave / NS) * R, kc0, p.wv);
   if (NORM) load_g<W, KCW>(L, kc0, p.gv);
 }
 
@@ -510,13 +516,13 @@ struct Item0 {
 };
 
 template <int RB>
-__device__ __forceinline__ Item0 item0(int M, int K, int N, bool pair) {
+__device__ __forceinline__ Item0 item0(int M, int K, int N, bool pair, const VG& g) {
   const int mcap = min(min(M, kEngineMaxRows), (kStage - kPartFloats) / K);
   const int mc0 = min(mcap, M);
   Item0 it;
   it.m = threadIdx.x % mc0;
   it.rr = (threadIdx.x / mc0) * (pair ? 2 : 1);
-  it.live = (int)threadIdx.x < (pair ? RB / 2 : RB) * mc0 && (int)blockIdx.x * RB + it.rr < N;
+  it.live = (int)threadIdx.x < (pair ? RB / 2 : RB) * mc0 && g.bid * RB + it.rr < N;
   return it;
 }
 
@@ -537,7 +543,7 @@ struct QkvItem {
 template <typename W, int KC, int NS, int R, int MR, bool NORM, class Next = NoHook>
 __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint32_t base, uint32_t tag, int* err,
                                           float* lds, const WPre<W, KC, NS, R, NORM>& pre, const QkvItem* qi,
-                                          uint32_t tz, Next&& next = Next()) {
+                                          uint32_t tz, const VG& g, Next&& next = Next()) {
   constexpr int KCW = KC / NS, GD = NORM ? KCW : 1;
   constexpr int RB = (EW / NS) * R;
   static_assert(KC % NS == 0 && EW % NS == 0 && NS * RB * 16 <= kPartFloats, "linear tiling");
@@ -551,14 +557,14 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
   const int mcap = min(min(M, kEngineMaxRows), (kStage - kPartFloats) / L.K);
   const int nch = (M + mcap - 1) / mcap;
   const int ntiles = (L.N + RB - 1) / RB;
-  const int rounds = (ntiles + gridDim.x - 1) / gridDim.x;
+  const int rounds = (ntiles + g.nb - 1) / g.nb;
   const bool pair = L.epi == EPI_SWIGLU || L.epi == EPI_QKV;
   // the residual operand of this thread's first item (at most one item per thread
   // and chunk: RB * 16 <= EB), requested before the input poll
-  const Item0 i0 = item0<RB>(M, L.K, L.N, pair);
+  const Item0 i0 = item0<RB>(M, L.K, L.N, pair, g);
   uint64_t e0_res = 0;
   if (i0.live && L.epi == EPI_RESID) {
-    const int n = blockIdx.x * RB + i0.rr;
+    const int n = g.bid * RB + i0.rr;
     if (L.resid.ll != nullptr) {
       e0_res = ll_load(L.resid.ll + (size_t)i0.m * L.resid.ld + n);
     } else {
@@ -570,7 +576,7 @@ __device__ __forceinline__ void op_linear(const ELinear& L, const ECall& c, uint
   // case of one round and one chunk, where next() runs right after the dot products
   // (otherwise after the last round, so that no weights stay live across the loops)
   auto round = [&](int t, bool fast) {
-    const int tile = blockIdx.x + t * gridDim.x;
+    const int tile = g.bid + t * g.nb;
     const int nt0 = tile * RB;  // first row of the tile (>= N: no rows)
     uint4 wv[R][KCW];
     float4 gv[GD][WT<W>::VEC / 4];
@@ -691,10 +697,10 @@ __device__ __forceinline__ AttnRow attn_row(const ECall& c, int i) {
 // split over this pass's keys (read from kvn), waves 1..EW-1 take one load round
 // each.  The waves' (max, sum,
 // numerator) are combined in LDS and the block writes one partial.  r0: the rows of
-// the block's first item (it = blockIdx.x), loaded once per launch.
+// the block's first item (it = the block index), loaded once per launch.
 template <typename KV, int DH, class Late = NoHook>
 __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t base, uint32_t tag, int* err,
-                                        float* lds, const AttnRow& r0, Late&& late = Late()) {
+                                        float* lds, const AttnRow& r0, const VG& vg, Late&& late = Late()) {
   constexpr int VEC = WT<KV>::VEC;
   constexpr int G = DH / VEC;                        // lanes per key row
   constexpr int KPR = 64 / G;                        // keys per load round
@@ -711,9 +717,9 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
   const int items = c.M * H * S;
   const uint32_t ktag = base + a.kvn_tag;
   bool hooked = false;
-  for (int it = blockIdx.x; it < items; it += gridDim.x) {
+  for (int it = vg.bid; it < items; it += vg.nb) {
     const int s = it % S, h = (it / S) % H, i = it / (S * H);
-    const AttnRow rw = it == (int)blockIdx.x ? r0 : attn_row(c, i);
+    const AttnRow rw = it == vg.bid ? r0 : attn_row(c, i);
     const int b = rw.b, kvlen = rw.kvlen, ns = rw.ns, gq = rw.gq;
     const int f = gld(c.first + i);
     const int32_t* gt = c.grp_tab != nullptr ? c.grp_tab + (size_t)b * a.cap : nullptr;
@@ -890,9 +896,10 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
 
 // One wave per (row, head): combine the S split partials (S <= 64).
 template <int DH>
-__device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32_t base, uint32_t tag, int* err) {
+__device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32_t base, uint32_t tag, int* err,
+                                         const VG& vg) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int gw = blockIdx.x * EW + wave, nw = gridDim.x * EW;
+  const int gw = vg.bid * EW + wave, nw = vg.nb * EW;
   const int S = c.S;
   const uint32_t ptag = base + g.part_tag;
   for (int it = gw; it < c.M * g.H; it += nw) {
@@ -966,17 +973,17 @@ constexpr int mr_of() {
 // Epilogue operands of the thread's first QKV item (see QkvItem); the weight slice
 // of the first layer's QKV projection is requested between the two loads.
 template <class SH, class PQ>
-__device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ& pq) {
+__device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ& pq, const VG& g) {
   constexpr int RB = (EW / SH::NSQ) * SH::RQ;
-  const Item0 it = item0<RB>(c.M, SH::D, 3 * SH::D, true);
+  const Item0 it = item0<RB>(c.M, SH::D, 3 * SH::D, true, g);
   QkvItem q{0, 0, 0, make_float2(1.f, 0.f)};
   if (it.live) {
     q.pos = gld(c.tok.pos + it.m);
     q.b = gld(c.tok.b + it.m);
     q.slot = gld(c.tok.slot + it.m);
   }
-  weights_ahead(L, pq);
-  const int n = blockIdx.x * RB + it.rr;
+  weights_ahead(L, pq, g);
+  const int n = g.bid * RB + it.rr;
   if (it.live && n < 2 * SH::D) {
     const int ee = (n % SH::D) % SH::DH;
     const v2f cs = *(const GLOBAL v2f*)(L.rope + (size_t)q.pos * (SH::DH / 2) + (ee >> 1));
@@ -997,12 +1004,11 @@ __device__ __forceinline__ QkvItem qkv_item(const ELinear& L, const ECall& c, PQ
 // right before a poll delays that poll until the burst has arrived; the early
 // requests move the two largest bursts away from the gate/up and down polls.
 template <class SH, bool MULTI>
-__global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops, int nlayers, ECall c, uint32_t base,
-                                                    int* err) {
+__device__ __forceinline__ void stack_pass(const EOp* __restrict__ ops, int nlayers, const ECall& c, uint32_t base,
+                                           int* err, float* lds, const VG g) {
   using W = typename SH::W;
   using KV = typename SH::KV;
   static_assert(SH::D % 256 == 0 && SH::F % 256 == 0, "a staged load must not straddle two rows");
-  __shared__ float lds[kLdsFloats];
   WPre<W, SH::KCD, SH::NSQ, SH::RQ, true> pq;
   WPre<W, SH::KCD, SH::NSO, SH::RO, false> po;
   WPre<W, SH::KCD, SH::NSG, SH::RG, true> pg;
@@ -1012,41 +1018,65 @@ __global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops,
   auto att = [&](int i) -> const EAttn& { return *(const EAttn*)&cops[i].at; };
   auto mrg = [&](int i) -> const EMerge& { return *(const EMerge*)&cops[i].mg; };
   constexpr bool kAhead = SH::AH == 2 || (SH::AH == 1 && !MULTI);
-  const QkvItem qi = qkv_item<SH>(lin(0), c, pq);
-  const AttnRow ar = blockIdx.x < (unsigned)(c.M * att(1).H * c.S) ? attn_row(c, blockIdx.x / (att(1).H * c.S))
-                                                                  : AttnRow{0, 0, 0, 0};
+  const QkvItem qi = qkv_item<SH>(lin(0), c, pq, g);
+  const AttnRow ar = g.bid < c.M * att(1).H * c.S ? attn_row(c, g.bid / (att(1).H * c.S)) : AttnRow{0, 0, 0, 0};
 #pragma unroll 1
   for (int l = 0; l < nlayers; ++l) {
     const int o = 6 * l;
-    if (l > 0) weights_ahead(lin(o), pq);
+    if (l > 0) weights_ahead(lin(o), pq, g);
     op_linear<W, SH::KCD, SH::NSQ, SH::RQ, mr_of<SH::RQ, SH::KCD / SH::NSQ, MULTI>(), true>(
         lin(o), c, base, base + cops[o].tag, err, lds, pq, &qi,
-        (touch_lines(cops + o) ^ touch_lines(cops + o + 1, true)) & c.zero);
+        (touch_lines(cops + o) ^ touch_lines(cops + o + 1, true)) & c.zero, g);
     lds_barrier();
-    op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, ar);
-    weights_ahead(lin(o + 3), po);
+    op_attn<KV, SH::DH>(att(o + 1), c, base, base + cops[o + 1].tag, err, lds, ar, g);
+    weights_ahead(lin(o + 3), po, g);
     if constexpr (kAhead) {
-      weights_ahead(lin(o + 4), pg);
-      weights_ahead(lin(o + 5), pd);
+      weights_ahead(lin(o + 4), pg, g);
+      weights_ahead(lin(o + 5), pd, g);
     }
     lds_barrier();
-    op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err);
+    op_merge<SH::DH>(mrg(o + 2), c, base, base + cops[o + 2].tag, err, g);
     op_linear<W, SH::KCD, SH::NSO, SH::RO, mr_of<SH::RO, SH::KCD / SH::NSO, MULTI>(), false>(
         lin(o + 3), c, base, base + cops[o + 3].tag, err, lds, po, nullptr,
-        (touch_lines(cops + o + 3) ^ touch_lines(cops + o + 4)) & c.zero, [&] {
-          if constexpr (!kAhead) weights_ahead(lin(o + 4), pg);
+        (touch_lines(cops + o + 3) ^ touch_lines(cops + o + 4)) & c.zero, g, [&] {
+          if constexpr (!kAhead) weights_ahead(lin(o + 4), pg, g);
         });
     lds_barrier();
     op_linear<W, SH::KCD, SH::NSG, SH::RG, mr_of<SH::RG, SH::KCD / SH::NSG, MULTI>(), true>(
         lin(o + 4), c, base, base + cops[o + 4].tag, err, lds, pg, nullptr,
-        (touch_lines(cops + o + 4) ^ touch_lines(cops + o + 5)) & c.zero, [&] {
-          if constexpr (!kAhead) weights_ahead(lin(o + 5), pd);
+        (touch_lines(cops + o + 4) ^ touch_lines(cops + o + 5)) & c.zero, g, [&] {
+          if constexpr (!kAhead) weights_ahead(lin(o + 5), pd, g);
         });
     lds_barrier();
     op_linear<W, SH::KCF, SH::NSD, SH::RD, mr_of<SH::RD, SH::KCF / SH::NSD, MULTI>(), false>(
         lin(o + 5), c, base, base + cops[o + 5].tag, err, lds, pd, nullptr,
-        (touch_lines(cops + o + 5) ^ touch_lines(cops + (l + 1 < nlayers ? o + 6 : o + 5))) & c.zero);
+        (touch_lines(cops + o + 5) ^ touch_lines(cops + (l + 1 < nlayers ? o + 6 : o + 5))) & c.zero, g);
     lds_barrier();
+  }
+}
+
+template <class SH, bool MULTI>
+__global__ __launch_bounds__(EB) void engine_kernel(const EOp* __restrict__ ops, int nlayers, ECall c, uint32_t base,
+                                                    int* err) {
+  __shared__ float lds[kLdsFloats];
+  stack_pass<SH, MULTI>(ops, nlayers, c, base, err, lds, VG{(int)blockIdx.x, (int)gridDim.x});
+}
+
+// Two independent single-row stack passes side by side in one launch: blocks
+// [0, nbA) run A, the rest B (e.g. the next-byte decoder and the next step's MB
+// window update of a decode step, which read only rows written before the launch).
+// Each pass is a chain of dependent steps whose waits for other blocks dominate its
+// time, so two chains on halves of the grid finish well before the same two one
+// after the other on the whole grid.  The op lists use disjoint tagged buffers.
+template <class SH>
+__global__ __launch_bounds__(EB) void engine_split_kernel(const EOp* __restrict__ opsA, int nA, ECall cA,
+                                                          uint32_t baseA, int nbA, const EOp* __restrict__ opsB,
+                                                          int nB, ECall cB, uint32_t baseB, int* err) {
+  __shared__ float lds[kLdsFloats];
+  if ((int)blockIdx.x < nbA) {
+    stack_pass<SH, false>(opsA, nA, cA, baseA, err, lds, VG{(int)blockIdx.x, nbA});
+  } else {
+    stack_pass<SH, false>(opsB, nB, cB, baseB, err, lds, VG{(int)blockIdx.x - nbA, (int)gridDim.x - nbA});
   }
 }
 
@@ -1090,6 +1120,37 @@ hipError_t launch_t(const EOp* ops, int nlayers, const ECall& call, uint32_t bas
 }
 
 template <class SH>
+int split_grid() {
+  static int grid = -1;
+  if (grid < 0) {
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, engine_split_kernel<SH>, EB, 0) != hipSuccess) {
+      grid = 0;
+    } else {
+      grid = per >= 1 ? cus : 0;
+    }
+  }
+  return grid;
+}
+
+template <class SH>
+hipError_t launch_split_t(const EOp* opsA, int nA, const ECall& cA, uint32_t baseA, int nbA, const EOp* opsB, int nB,
+                          const ECall& cB, uint32_t baseB, int* err, hipStream_t st, const Ev& ev) {
+  const int grid = split_grid<SH>();
+  if (grid <= 0 || nbA <= 0 || nbA >= grid) return hipErrorInvalidConfiguration;
+  auto kern = engine_split_kernel<SH>;
+  if (ev.start != nullptr || ev.stop != nullptr) {
+    hipExtLaunchKernelGGL(kern, dim3(grid), dim3(EB), 0, st, ev.start, ev.stop, 0, opsA, nA, cA, baseA, nbA, opsB, nB,
+                          cB, baseB, err);
+  } else {
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(EB), 0, st, opsA, nA, cA, baseA, nbA, opsB, nB, cB, baseB, err);
+  }
+  return hipGetLastError();
+}
+
+template <class SH>
 hipError_t launch_s(const EOp* ops, int nlayers, const ECall& call, uint32_t base, int* err, hipStream_t st,
                     const Ev& ev) {
   if (call.M == 1) return launch_t<SH, false>(ops, nlayers, call, base, err, st, ev);
@@ -1117,6 +1178,23 @@ int engine_grid(int shape) {
   if (shape == 1) return std::min(grid_of<Shape1, false>(), grid_of<Shape1, true>());
   if (shape == 2) return std::min(grid_of<Shape2, false>(), grid_of<Shape2, true>());
   return 0;
+}
+
+int engine_split_grid(int shape) {
+  if (shape == 0) return split_grid<Shape0>();
+  if (shape == 1) return split_grid<Shape1>();
+  if (shape == 2) return split_grid<Shape2>();
+  return 0;
+}
+
+hipError_t launch_engine_split(int shape, const EOp* opsA, int nA, const ECall& cA, uint32_t baseA, int nbA,
+                               const EOp* opsB, int nB, const ECall& cB, uint32_t baseB, int* err, hipStream_t st,
+                               const Ev& ev) {
+  if (cA.M != 1 || cB.M != 1 || nA <= 0 || nB <= 0) return hipErrorInvalidValue;
+  if (shape == 0) return launch_split_t<Shape0>(opsA, nA, cA, baseA, nbA, opsB, nB, cB, baseB, err, st, ev);
+  if (shape == 1) return launch_split_t<Shape1>(opsA, nA, cA, baseA, nbA, opsB, nB, cB, baseB, err, st, ev);
+  if (shape == 2) return launch_split_t<Shape2>(opsA, nA, cA, baseA, nbA, opsB, nB, cB, baseB, err, st, ev);
+  return hipErrorInvalidValue;
 }
 
 hipError_t launch_engine(int shape, const EOp* ops, int nlayers, const ECall& call, uint32_t base, int* err,

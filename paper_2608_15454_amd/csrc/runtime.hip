@@ -109,7 +109,8 @@ struct Sizes {
   int64_t part_floats, part_floats_mb;
   size_t es;  // element size of the KV caches
   int Esplit;          // attention splits per (row, head) the engine buffers hold
-  int64_t ll_entries;  // tagged 8-byte entries of the engine buffers
+  int64_t ll_set;      // tagged 8-byte entries of one set of engine buffers
+  int64_t ll_entries;  // all sets
   int eng_ops;         // engine operations of all stacks
 };
 
@@ -193,7 +194,9 @@ Sizes sizes_of(const mbp_config& c) {
   s.es = c.kv_dtype == MBP_F32 ? 4 : 2;
   const int ex = kEngineMaxRows;
   s.Esplit = kEngineMaxSplits;
-  s.ll_entries = (int64_t)ex * s.d * 7 + (int64_t)ex * s.dff + (int64_t)ex * s.H * s.Esplit * (s.dh + 2);
+  s.ll_set = (int64_t)ex * s.d * 7 + (int64_t)ex * s.dff + (int64_t)ex * s.H * s.Esplit * (s.dh + 2);
+  // the MB window stack has a set of its own, so that it can run beside the NT decoder
+  s.ll_entries = s.ll_set * (c.head == MBP_HEAD_LCA && c.n_mb > 0 ? 2 : 1);
   s.eng_ops = 6 * (c.n_enc + c.n_lm + c.n_nb + (c.head == MBP_HEAD_LCA ? c.n_mb : 0));
   return s;
 }
@@ -436,6 +439,7 @@ struct mbp_handle {
   bool engine = false;
   int eng_shape = -1;
   int eng_grid = 0;  // blocks of an engine launch
+  int split_grid = 0;  // blocks of a launch of two stacks side by side (0: not available)
   EngStack es_enc, es_lm, es_nt, es_mb;
   uint32_t tag_base = 1;
   EOp* d_ops = nullptr;
@@ -627,27 +631,62 @@ double stack_bytes(const mbp_handle* h, int nlayers, int M, double kv_rows) {
   return per_layer * nlayers;
 }
 
-// One pass through a stack in the persistent engine (see engine.hip).
-int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const EIo& io, const Tok& tok, const int32_t* first,
-               const int32_t* first_slot, int S, int chunk, const int32_t* grp_tab, double kv_rows, hipStream_t st) {
-  ECall c;
-  c.io = io;
-  c.M = tok.M;
-  c.tok = tok;
-  c.first = first;
-  c.first_slot = first_slot;
-  c.grp_tab = grp_tab;
-  c.S = S;
-  c.chunk = chunk;
-  c.zero = 0;
-  if (h->tag_base > 0xF0000000u) {  // restart the tags before they wrap: clear the tagged buffers
+// The engine call of a pass over `grid` blocks: the cached keys per attention split
+// are as few as keep the (row, head, split) items within one per block, so the cache
+// reads are spread over every block.  False when the pass does not fit the engine.
+bool engine_call(const mbp_handle* h, const EngStack* es, const EIo& io, const Tok& tok, const int32_t* first,
+                 const int32_t* first_slot, int32_t max_ns, const int32_t* grp_tab, int grid, ECall* c) {
+  const Sizes& s = h->sz;
+  if (!h->engine || es == nullptr || es->nops == 0 || tok.M > kEngineMaxRows || grid <= 0) return false;
+  const int items_per_split = tok.M * s.H;
+  const int cached_splits = std::max(1, grid / items_per_split - 1);
+  const int chunk = std::max(64, (max_ns + cached_splits - 1) / cached_splits + 63) / 64 * 64;
+  const int S = (max_ns + chunk - 1) / chunk + 1;
+  if (S > s.Esplit) return false;
+  *c = ECall{};
+  c->io = io;
+  c->M = tok.M;
+  c->tok = tok;
+  c->first = first;
+  c->first_slot = first_slot;
+  c->grp_tab = grp_tab;
+  c->S = S;
+  c->chunk = chunk;
+  c->zero = 0;
+  return true;
+}
+
+// Tag base of a launch of nops operations (the tagged buffers are cleared before the
+// tags would wrap).
+int take_tags(mbp_handle* h, int nops, hipStream_t st, uint32_t* base) {
+  if (h->tag_base > 0xF0000000u) {
     HIPCK(h, hipMemsetAsync(h->R<uint64_t>(h->rg.ll), 0, (size_t)h->sz.ll_entries * 8, st));
     h->tag_base = 1;
   }
-  const uint32_t base = h->tag_base;
-  h->tag_base += (uint32_t)es.nops + 1;
-  TIMED(h, MBP_KCLASS_ENGINE, stack_bytes(h, nlayers, tok.M, kv_rows), launch_engine, h->eng_shape,
+  *base = h->tag_base;
+  h->tag_base += (uint32_t)nops + 1;
+  return MBP_OK;
+}
+
+// One pass through a stack in the persistent engine (see engine.hip).
+int run_engine(mbp_handle* h, const EngStack& es, int nlayers, const ECall& c, double kv_rows, hipStream_t st) {
+  uint32_t base;
+  RCK(take_tags(h, es.nops, st, &base));
+  TIMED(h, MBP_KCLASS_ENGINE, stack_bytes(h, nlayers, c.M, kv_rows), launch_engine, h->eng_shape,
         h->d_ops + es.first, es.nops / 6, c, base, h->d_err, st);
+  return MBP_OK;
+}
+
+// Two single-row passes side by side in one engine launch (launch_engine_split):
+// A on the first half of the grid, B on the rest.
+int run_engine_split(mbp_handle* h, const EngStack& ea, int la, const ECall& ca, double kva, const EngStack& eb, int lb,
+                     const ECall& cb, double kvb, hipStream_t st) {
+  uint32_t base_a, base_b;
+  RCK(take_tags(h, ea.nops, st, &base_a));
+  RCK(take_tags(h, eb.nops, st, &base_b));
+  const double bytes = stack_bytes(h, la, ca.M, kva) + stack_bytes(h, lb, cb.M, kvb);
+  TIMED(h, MBP_KCLASS_ENGINE, bytes, launch_engine_split, h->eng_shape, h->d_ops + ea.first, ea.nops / 6, ca, base_a,
+        h->split_grid / 2, h->d_ops + eb.first, eb.nops / 6, cb, base_b, h->d_err, st);
   return MBP_OK;
 }
 
@@ -720,16 +759,9 @@ int run_pass(mbp_handle* h, const std::vector<BlockW>& layers, const KV& kv, con
   const Sizes& s = h->sz;
   const int M = tok.M;
   if (M == 0) return MBP_OK;
-  if (h->engine && es != nullptr && es->nops > 0 && !tiled && M <= kEngineMaxRows) {
-    // cached keys per attention split: as few as keep the (row, head, split) items
-    // within one per block, so the cache reads are spread over every compute unit
-    const int items_per_split = M * s.H;
-    const int cached_splits = std::max(1, h->eng_grid / items_per_split - 1);
-    const int chunk = std::max(64, (max_ns + cached_splits - 1) / cached_splits + 63) / 64 * 64;
-    const int S = (max_ns + chunk - 1) / chunk + 1;
-    if (S <= s.Esplit)
-      return run_engine(h, *es, (int)layers.size(), io, tok, first, first_slot, S, chunk, grp_tab, kv_rows, st);
-  }
+  ECall ec;
+  if (!tiled && engine_call(h, es, io, tok, first, first_slot, max_ns, grp_tab, h->eng_grid, &ec))
+    return run_engine(h, *es, (int)layers.size(), ec, kv_rows, st);
   if (io.emb != nullptr) {
     OTHER(h, launch_embed, io.emb, h->wdt, io.ie, X, s.d, M, st);
   } else if (io.xa != X || io.ia != nullptr || io.xb != nullptr) {
@@ -843,20 +875,24 @@ int mb_prepare(mbp_handle* h, int n, Plan& p, bool clamp, MbPass* out) {
   return MBP_OK;
 }
 
-int mb_launch(mbp_handle* h, const Plan& p, const MbPass& mp, hipStream_t st) {
-  const Regions& rg = h->rg;
-  if (mp.tm.size() == 0) return MBP_OK;
-  const Tok tok = dev_tok(p, mp.om, mp.tm.size());
-  const Scratch& sc = h->sc_mb;
-  // window rows z_g = latent output + latent input of the row's group; outputs to the
-  // MB rows of the window
+// Input and output rows of a window update: z_g = latent output + latent input of
+// the row's group in; the MB rows of the window out.
+EIo mb_io(mbp_handle* h, const Plan& p, const MbPass& mp) {
   EIo io{};
-  io.xa = h->R<float>(rg.lat_out);
+  io.xa = h->R<float>(h->rg.lat_out);
   io.ia = p.at(mp.o_z);
-  io.xb = h->R<float>(rg.lat_in);
+  io.xb = h->R<float>(h->rg.lat_in);
   io.ib = p.at(mp.o_z);
   io.xo = h->rows_base();
   io.oi = p.at(mp.o_w);
+  return io;
+}
+
+int mb_launch(mbp_handle* h, const Plan& p, const MbPass& mp, hipStream_t st) {
+  if (mp.tm.size() == 0) return MBP_OK;
+  const Tok tok = dev_tok(p, mp.om, mp.tm.size());
+  const Scratch& sc = h->sc_mb;
+  const EIo io = mb_io(h, p, mp);
   return run_pass(h, h->mb, h->kv_mb, &h->es_mb, io, sc.X, tok, p.at(mp.o_g), false, nullptr, 0, mp.max_w, mp.kvr, sc,
                   st, p.at(mp.om.first), p.at(mp.om.first_slot), mp.om.max_ns);
 }
@@ -1055,10 +1091,27 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
     ion.xo = X;
     ion.xo2 = h->fwd_h ? h->fwd_h : h->rows_base();
     ion.oi2 = p.at(o_h1);
-    RCK(run_pass(h, h->nt, h->kv_nt, &h->es_nt, ion, X, tok_e, nullptr, tiled_e, p.at(o_te),
-                 (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot), oe.max_ns));
+    // a single-row NT pass and a single-row window update go side by side in one
+    // engine launch (each reads only rows written before it)
+    bool split = false;
+    if (pre_here && h->split_grid > 0 && Me == 1 && mp_next.tm.size() == 1 && !tiled_e) {
+      const int half = h->split_grid / 2;  // measured best of 96..224 blocks for the NT half
+      ECall cn, cm;
+      if (engine_call(h, &h->es_nt, ion, tok_e, p.at(oe.first), p.at(oe.first_slot), oe.max_ns, nullptr, half, &cn) &&
+          engine_call(h, &h->es_mb, mb_io(h, p, mp_next), dev_tok(p, mp_next.om, 1), p.at(mp_next.om.first),
+                      p.at(mp_next.om.first_slot), mp_next.om.max_ns, p.at(mp_next.o_g), h->split_grid - half,
+                      &cm)) {
+        RCK(run_engine_split(h, h->es_nt, (int)h->nt.size(), cn, kvr_e, h->es_mb, (int)h->mb.size(), cm,
+                             mp_next.kvr, h->st));
+        split = true;
+      }
+    }
+    if (!split)
+      RCK(run_pass(h, h->nt, h->kv_nt, &h->es_nt, ion, X, tok_e, nullptr, tiled_e, p.at(o_te),
+                   (int)tiles_e.size() / 2, max_kv_e, kvr_e, sc, h->st, p.at(oe.first), p.at(oe.first_slot),
+                   oe.max_ns));
     if (pre_here) {
-      RCK(mb_launch(h, p, mp_next, h->st));
+      if (!split) RCK(mb_launch(h, p, mp_next, h->st));
       h->pre_draft = true;
       h->pre_n = h->n_hint;
       h->pre_o_hr = o_hr;
@@ -1224,19 +1277,22 @@ int build_engine(mbp_handle* h) {
   if (shape < 0 || engine_grid(shape) <= 0) return MBP_OK;
   h->eng_shape = shape;
   h->eng_grid = engine_grid(shape);
+  const int sg = engine_split_grid(shape);
+  h->split_grid = (sg == h->eng_grid && sg >= 2 && s.ll_entries >= 2 * s.ll_set) ? sg : 0;
   const int ex = kEngineMaxRows;
-  uint64_t* x0 = h->R<uint64_t>(h->rg.ll);
-  uint64_t* x1 = x0 + (size_t)ex * s.d;
-  uint64_t* rr = x1 + (size_t)ex * s.d;
-  uint64_t* q = rr + (size_t)ex * s.d;
-  uint64_t* kvn = q + (size_t)ex * s.d;
-  uint64_t* a = kvn + (size_t)2 * ex * s.d;
-  uint64_t* hid = a + (size_t)ex * s.d;
-  uint64_t* part = hid + (size_t)ex * s.dff;
-  uint64_t* xb[2] = {x0, x1};
   const float scale = c.attn_scale / std::sqrt((float)s.dh);
   std::vector<EOp> ops;
-  auto stack = [&](const std::vector<BlockW>& layers, const KV& kv, EngStack& es) {
+  // set: which set of tagged buffers the stack's operations use
+  auto stack = [&](const std::vector<BlockW>& layers, const KV& kv, EngStack& es, int set) {
+    uint64_t* x0 = h->R<uint64_t>(h->rg.ll) + (size_t)set * s.ll_set;
+    uint64_t* x1 = x0 + (size_t)ex * s.d;
+    uint64_t* rr = x1 + (size_t)ex * s.d;
+    uint64_t* q = rr + (size_t)ex * s.d;
+    uint64_t* kvn = q + (size_t)ex * s.d;
+    uint64_t* a = kvn + (size_t)2 * ex * s.d;
+    uint64_t* hid = a + (size_t)ex * s.d;
+    uint64_t* part = hid + (size_t)ex * s.dff;
+    uint64_t* xb[2] = {x0, x1};
     es.first = (int)ops.size();
     const int L = (int)layers.size();
     for (int l = 0; l < L; ++l) {
@@ -1303,10 +1359,10 @@ int build_engine(mbp_handle* h) {
     }
     es.nops = (int)ops.size() - es.first;
   };
-  stack(h->enc, h->kv_enc, h->es_enc);
-  stack(h->lm, h->kv_lm, h->es_lm);
-  stack(h->nt, h->kv_nt, h->es_nt);
-  if (c.head == MBP_HEAD_LCA) stack(h->mb, h->kv_mb, h->es_mb);
+  stack(h->enc, h->kv_enc, h->es_enc, 0);
+  stack(h->lm, h->kv_lm, h->es_lm, 0);
+  stack(h->nt, h->kv_nt, h->es_nt, 0);
+  if (c.head == MBP_HEAD_LCA) stack(h->mb, h->kv_mb, h->es_mb, s.ll_entries >= 2 * s.ll_set ? 1 : 0);
   if ((int)ops.size() > s.eng_ops) return fail(h, MBP_ECAPACITY, "engine operation list exceeds its region");
   if (!ops.empty()) {
     HIPCK(h, hipMemcpyAsync(h->d_ops, ops.data(), ops.size() * sizeof(EOp), hipMemcpyHostToDevice, h->st));
