@@ -19,10 +19,13 @@
  *   - The caller owns all device memory: weights, the workspace and all output
  *     buffers.  The library never allocates or frees device memory; it carves the
  *     caller's workspace.  It keeps a small host-side state per handle, including
- *     pinned host staging buffers (hipHostMalloc) for its uploads and downloads, and
- *     one stream of its own on which part of a step runs concurrently.
- *   - All device work is enqueued on the stream given to mbp_init.  Device outputs
- *     are valid once the caller synchronizes that stream.  Calls that need host-side
+ *     pinned host staging buffers (hipHostMalloc) for its uploads and downloads.
+ *     Only when the persistent engine does not run the model (no_engine = 1, or a
+ *     shape it is not built for) does a handle with an LCA head create one stream of
+ *     its own, on which the next step's MB window update runs beside the NT decoder.
+ *   - All device work is enqueued on the stream given to mbp_init (the window update
+ *     on the library's own stream above waits for it and is joined back to it by an
+ *     event).  Device outputs are valid once the caller synchronizes that stream.  Calls that need host-side
  *     values (mbp_accept, mbp_decode_step in verify mode) synchronize it themselves.
  *   - Every function returns an mbp_status (0 = success) and never throws or exits.
  *     Arguments are validated before any device work; MBP_EINVAL / MBP_ECAPACITY
@@ -222,7 +225,9 @@ int mbp_last_accepted(mbp_handle *h, uint8_t *h_bytes, int32_t *h_lens);
  *     step they are already committed; this only closes the step).
  *   h_override != NULL: host [batch, max_n] bytes and h_override_len host [batch]
  *     counts (0..max_n) to commit instead (teacher forcing); a pending verify step
- *     is rolled back first.
+ *     is rolled back first.  A row's bonus byte left pending by an external
+ *     verification already closed with mbp_accept(h, NULL, NULL) is committed
+ *     before its override bytes.
  * MBP_ESTATE if no decode step is pending and no override is given; MBP_ECAPACITY if
  * a row would exceed max_ctx or max_latents. */
 int mbp_accept(mbp_handle *h, const uint8_t *h_override, const int32_t *h_override_len);

@@ -516,7 +516,7 @@ int t_drain(mbp_handle* h) {
 
 int sync_all(mbp_handle* h) {
   HIPCK(h, hipStreamSynchronize(h->st));
-  HIPCK(h, hipStreamSynchronize(h->st2));
+  if (h->st2) HIPCK(h, hipStreamSynchronize(h->st2));
   h->mb_pending = false;
   return MBP_OK;
 }
@@ -946,7 +946,8 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
   float* he = h->R<float>(h->rg.he);
   float* lat_in = h->R<float>(h->rg.lat_in);
   float* lat_out = h->R<float>(h->rg.lat_out);
-  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && !h->engine;
+  const bool fork = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && !h->engine &&
+                    h->st2 != nullptr;
   // with the engine, the next step's window update runs right after the NT decoder
   // on the same stream, prepared in the commit's plan (and the head rows with it)
   const bool pre = fork_mb && c.head == MBP_HEAD_LCA && c.n_mb > 0 && h->n_hint >= 2 && !items.empty() && h->engine;
@@ -1436,9 +1437,7 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
       (void)hipGetLastError();  // the failed lookup must not surface in a later call
     }
   }
-  hipError_t e = hipStreamCreateWithFlags(&h->st2, hipStreamNonBlocking);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_mb, hipEventDisableTiming);
+  hipError_t e = hipSuccess;
   // pinned host staging (host memory only): plans, step results
   for (int i = 0; i < kPlans && e == hipSuccess; ++i) {
     e = hipHostMalloc((void**)&h->plan[i].host, rg.plan_ints * 4, hipHostMallocDefault);
@@ -1543,6 +1542,15 @@ extern "C" int mbp_init(const mbp_config* cfg, const void* const* d_weights, int
   e = hipMemsetAsync(h->d_err, 0, 4, h->st);
   if (e == hipSuccess) e = hipMemsetAsync(h->R<uint64_t>(rg.ll), 0, (size_t)s.ll_entries * 8, h->st);
   if (e != hipSuccess || build_engine(h) != MBP_OK) return bail();
+  // without the engine, the next step's window update runs on a stream of the
+  // library's own beside the NT decoder (with it, every launch stays on the caller's
+  // stream)
+  if (!h->engine && cfg->head == MBP_HEAD_LCA && cfg->n_mb > 0) {
+    e = hipStreamCreateWithFlags(&h->st2, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventCreateWithFlags(&h->ev_mb, hipEventDisableTiming);
+    if (e != hipSuccess) return bail();
+  }
   *out = h;
   return MBP_OK;
 }
@@ -2024,18 +2032,20 @@ extern "C" int mbp_accept(mbp_handle* h, const uint8_t* h_override, const int32_
       if (h_override_len[b] < 0 || h_override_len[b] > s.nmax) return fail(h, MBP_EINVAL, "override length out of range");
     const bool rollback = h->pending && (h->last_mode == MBP_ACCEPT_SELF_VERIFY || h->last_mode == kModeExternal);
     for (int b = 0; b < B; ++b) {
-      add[b].assign(h_override + (size_t)b * s.nmax, h_override + (size_t)b * s.nmax + h_override_len[b]);
+      // a bonus byte left pending by a closed external verification was accepted
+      // before the override: it is committed first (a rolled-back step drops its own)
+      if (!rollback && h->rows[b].bonus >= 0) add[b].push_back((uint8_t)h->rows[b].bonus);
+      add[b].insert(add[b].end(), h_override + (size_t)b * s.nmax,
+                    h_override + (size_t)b * s.nmax + h_override_len[b]);
       Row sim = h->rows[b];
       if (rollback) truncate_row(sim, h->pre_len[b]);
       if ((int64_t)sim.x.size() + (int64_t)add[b].size() > s.Tcap) return fail(h, MBP_ECAPACITY, "row would exceed max_ctx");
       if (simulate_latents(h->cfg, sim, add[b].data(), (int)add[b].size()) > h->cfg.max_latents)
         return fail(h, MBP_ECAPACITY, "row would exceed max_latents");
     }
+    for (int b = 0; b < B; ++b) h->rows[b].bonus = -1;  // rolled back, or committed first above
     if (rollback) {
-      for (int b = 0; b < B; ++b) {
-        truncate_row(h->rows[b], h->pre_len[b]);
-        h->rows[b].bonus = -1;  // part of the rolled-back step
-      }
+      for (int b = 0; b < B; ++b) truncate_row(h->rows[b], h->pre_len[b]);
       HIPCK(h, hipMemcpyAsync(h->row_ptr(h->rg.row_h1), h->row_ptr(h->rg.row_h1s), (size_t)B * s.d * 4,
                               hipMemcpyDeviceToDevice, h->st));
     }
@@ -2104,7 +2114,7 @@ extern "C" int mbp_reset(mbp_handle* h) {
   if (!h) return MBP_EINVAL;
   // wait for enqueued work (errors are ignored: reset also recovers poisoned handles)
   (void)hipStreamSynchronize(h->st);
-  (void)hipStreamSynchronize(h->st2);
+  if (h->st2) (void)hipStreamSynchronize(h->st2);
   if (h->d_err) {  // forget an engine timeout
     (void)hipMemsetAsync(h->d_err, 0, 4, h->st);
     (void)hipStreamSynchronize(h->st);

@@ -137,6 +137,23 @@ def test_external_pending_bonus_decode_step_and_override():
     c3, _, _ = V.decode_step(1, 0.5, THRESHOLD)
     assert int(c3[0, 0].item()) == int(oracle.step(W, TINY, x, 1, 0.5)["cand"][0])
     V.accept()
+    x += [int(oracle.step(W, TINY, x, 1, 0.5)["cand"][0])]
+    # an override after a verification closed with accept(None): the verifier's pending
+    # bonus byte was accepted first, so it precedes the override bytes
+    D.reset()
+    D.prefill([np.array(x, np.uint8)])
+    cand, _, _ = D.decode_step(4, 1.0, THRESHOLD)
+    out, ln = V.verify_draft(cand)
+    acc = [int(b) for b in out[0, : int(ln[0].item())].cpu().numpy()]
+    assert acc == [int(b) for b in oracle.verify_external(W, TINY, x, cand[0].cpu().numpy())["bytes"]]
+    V.accept()
+    V.accept([[75, 76]])
+    x += acc + [75, 76]
+    assert V.row_length(0) == len(x)
+    c4, _, _ = V.decode_step(3, 0.5, THRESHOLD)
+    ref = oracle.step(W, TINY, x, 3, 0.5)
+    np.testing.assert_allclose(V.logits()[0].double().cpu().numpy(), ref["logits"], atol=base_tol(TINY) * 30)
+    V.accept()
 
 
 def test_external_verify_d1024_engine_equals_verifier_greedy():
