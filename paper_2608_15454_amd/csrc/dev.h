@@ -20,6 +20,16 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
   return (uint16_t)(u >> 16);
 }
 
+// bfloat16 hi / lo halves of two floats, packed as (x0 | x1 << 16): hi = bf16(x),
+// lo = bf16(x - hi), both rounded to nearest even by the gfx950 conversion
+// instruction (the compiler emits v_cvt_pk_bf16_f32 for these casts).
+__device__ __forceinline__ void bf16_hi_lo2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
+  const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
+  const __bf16 l0 = (__bf16)(x0 - (float)h0), l1 = (__bf16)(x1 - (float)h1);
+  hi = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
+  lo = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+}
+
 template <typename W>
 struct WT;
 

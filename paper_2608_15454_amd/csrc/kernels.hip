@@ -311,12 +311,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   auto stage = [&](int buf) {
     uint32_t p[8], q[8];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) {
-      const uint16_t h0 = f2bf(a[2 * v]), h1 = f2bf(a[2 * v + 1]);
-      const uint16_t l0 = f2bf(a[2 * v] - bf2f(h0)), l1 = f2bf(a[2 * v + 1] - bf2f(h1));
-      p[v] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-      q[v] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-    }
+    for (int v = 0; v < 8; ++v) bf16_hi_lo2(a[2 * v], a[2 * v + 1], p[v], q[v]);
     uint4* ad = reinterpret_cast<uint4*>(&As[buf][lr * LD + lk]);
     ad[0] = make_uint4(p[0], p[1], p[2], p[3]);
     ad[1] = make_uint4(p[4], p[5], p[6], p[7]);
@@ -422,6 +417,158 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) 
   }
   if (pair) epi_pair(L.epi, m, n, a0, a1);
   else epi_single(L.epi, m, n, a0);
+}
+
+// The same product for large M (prefill, long commits): a 128x128 output tile per
+// block of four waves, each wave a 64x64 quarter (2 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16, X in bfloat16 hi + lo as above), K in steps of 32.  Two LDS
+// stages and two register stages: the X and weight rows of step k+2 are requested
+// while step k's MFMAs run and step k+1 is staged, so each fetch has two steps to
+// arrive (the steps are latency-bound otherwise); one barrier per step.  Twice the
+// output per staged byte of the 64x64 tile.  Order: the blocks of XCD k (workgroups go
+// to the 8 XCDs round-robin) take groups of GR row blocks k, k+8, ... and walk the
+// column blocks with the group's rows fastest, so the group's X rows (GR x 128 rows)
+// stay in the XCD's L2 across the columns and each weight tile is used by the whole
+// group while it is resident.
+constexpr int kBigBM = 128, kBigBN = 128, kBigBK = 32, kBigLD = kBigBK + 8, kBigMaxGainK = 4096;
+
+__global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr) {
+  constexpr int BM = kBigBM, BN = kBigBN, BK = kBigBK, LD = kBigLD;
+  __shared__ __attribute__((aligned(16))) uint16_t Ah[2][BM * LD];
+  __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LD];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LD];
+  __shared__ float rs[BM];
+  __shared__ __attribute__((aligned(16))) float gs[kBigMaxGainK];  // the norm gain (one vector for every row)
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  int bx = blockIdx.x, by = blockIdx.y;
+  {
+    const int rb = gridDim.y, cb = gridDim.x;
+    if (gr > 0 && rb % (8 * gr) == 0) {
+      const int bid = blockIdx.y * cb + blockIdx.x, xcd = bid & 7, l = bid >> 3;
+      const int g = l / (gr * cb), rem = l - g * gr * cb;
+      bx = rem / gr;
+      by = xcd + 8 * (g * gr + rem % gr);
+    }
+  }
+  const int m0 = by * BM, n0 = bx * BN;
+  // loads: thread t stages 16 consecutive k of row t / 2 of both tiles
+  const int lr = tid >> 1, lk = (tid & 1) * 16;
+  const int am = m0 + lr;
+  const bool aok = am < L.M;
+  const float* arow = L.X + (size_t)(aok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx + lk;
+  const bool norm = L.gain != nullptr;
+  if (norm)
+    for (int k = tid * 4; k < L.K; k += 256 * 4) *reinterpret_cast<float4*>(&gs[k]) = *reinterpret_cast<const float4*>(L.gain + k);
+  const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K) + lk;
+  float ss = 0.f;
+  struct Fetch {
+    float4 a[4];
+    uint4 b0, b1;
+  };
+  Fetch f0, f1;
+  auto fetch = [&](Fetch& f, int k0) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v)
+      f.a[v] = aok ? *reinterpret_cast<const float4*>(arow + k0 + 4 * v) : make_float4(0.f, 0.f, 0.f, 0.f);
+    f.b0 = *reinterpret_cast<const uint4*>(brow + k0);
+    f.b1 = *reinterpret_cast<const uint4*>(brow + k0 + 8);
+  };
+  auto stage = [&](const Fetch& f, int k0, int buf) {
+    uint32_t p[8], q[8];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      float4 t = f.a[v];
+      if (norm && aok) {
+        ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+        const float4 g = *reinterpret_cast<const float4*>(&gs[lk + k0 + 4 * v]);
+        t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
+      }
+      bf16_hi_lo2(t.x, t.y, p[2 * v], q[2 * v]);
+      bf16_hi_lo2(t.z, t.w, p[2 * v + 1], q[2 * v + 1]);
+    }
+    uint4* ad = reinterpret_cast<uint4*>(&Ah[buf][lr * LD + lk]);
+    ad[0] = make_uint4(p[0], p[1], p[2], p[3]);
+    ad[1] = make_uint4(p[4], p[5], p[6], p[7]);
+    uint4* al = reinterpret_cast<uint4*>(&Al[buf][lr * LD + lk]);
+    al[0] = make_uint4(q[0], q[1], q[2], q[3]);
+    al[1] = make_uint4(q[4], q[5], q[6], q[7]);
+    uint4* bd = reinterpret_cast<uint4*>(&Bs[buf][lr * LD + lk]);
+    bd[0] = f.b0;
+    bd[1] = f.b1;
+  };
+  const int wm = wave >> 1, wn = wave & 1;
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  auto mfmas = [&](int cur) {
+#pragma unroll
+    for (int ks = 0; ks < BK; ks += 16) {
+      bf16x8 fh[2], fl[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        const int off = (wm * 64 + i * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8;
+        fh[i] = *reinterpret_cast<const bf16x8*>(&Ah[cur][off]);
+        fl[i] = *reinterpret_cast<const bf16x8*>(&Al[cur][off]);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+        fb[j] = *reinterpret_cast<const bf16x8*>(&Bs[cur][(wn * 64 + j * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8]);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fh[i], fb[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fl[i], fb[j], acc[i][j], 0, 0, 0);
+        }
+    }
+  };
+  const int nk = L.K / BK;  // >= 1
+  fetch(f0, 0);
+  if (nk > 1) fetch(f1, BK);
+  __syncthreads();  // the gain vector
+  stage(f0, 0, 0);
+  __syncthreads();
+  // step kt: request step kt + 2 into the register set step kt just left, run step
+  // kt's MFMAs, stage step kt + 1 (in the other set) into the other LDS stage
+  for (int kt = 0; kt < nk; kt += 2) {
+    if (kt + 2 < nk) fetch(f0, (kt + 2) * BK);
+    mfmas(0);
+    if (kt + 1 < nk) stage(f1, (kt + 1) * BK, 1);
+    __syncthreads();
+    if (kt + 1 >= nk) break;
+    if (kt + 3 < nk) fetch(f1, (kt + 3) * BK);
+    mfmas(1);
+    if (kt + 2 < nk) stage(f0, (kt + 2) * BK, 0);
+    __syncthreads();
+  }
+  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+  // the two threads of a staged row hold its sum of squares over K
+  ss += xor_lane<1>(ss);
+  if (norm && (tid & 1) == 0) rs[lr] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
+  __syncthreads();
+  const int jj = lane & 31;
+  auto out_block = [&](const f32x16& c, int i, int j) {
+    const int n = n0 + wn * 64 + j * 32 + jj;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ml = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int m = m0 + ml;
+      const float val = norm ? c[r] * rs[ml] : c[r];
+      const float partner = xor_lane<1>(val);  // column n + 1, same row (used by even columns)
+      if (m < L.M) {
+        if (!pair) epi_single(L.epi, m, n, val);
+        else if ((jj & 1) == 0) epi_pair(L.epi, m, n, val, partner);
+      }
+    }
+  };
+  out_block(acc[0][0], 0, 0);
+  out_block(acc[0][1], 0, 1);
+  out_block(acc[1][0], 1, 0);
+  out_block(acc[1][1], 1, 1);
 }
 
 // ------------------------------------------------------------- attention ------
@@ -1650,6 +1797,15 @@ bool mfma_fits(const Linear& L) {
 
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
+  // large M: the 128x128 tile, once its grid fills every compute unit twice
+  if (mfma_fits<W>(L) && L.N % kBigBN == 0 && L.K % kBigBK == 0 && L.gain2 == nullptr &&
+      (L.gain == nullptr || L.K <= kBigMaxGainK) &&
+      (int64_t)(L.N / kBigBN) * ((L.M + kBigBM - 1) / kBigBM) >= 512) {
+    // row blocks per L2 group: about 2 MiB of float32 X rows
+    const int gr = std::max(1, std::min(8, (int)((2 << 20) / ((int64_t)kBigBM * L.K * 4))));
+    const dim3 grid(L.N / kBigBN, (L.M + kBigBM - 1) / kBigBM);
+    return klaunch(gemm_mfma_big_kernel, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
+  }
   if (mfma_fits<W>(L)) {
     // split K until about kMfmaTargetBlocks blocks stream the weights (the partials
     // and the splits' sums of squares must fit)

@@ -183,7 +183,10 @@ Sizes sizes_of(const mbp_config& c) {
   s.Kcap = c.max_latents + 1;
   s.nmax = c.max_n;
   s.Wcap = c.max_window > 0 ? c.max_window : std::max(2 * c.max_patch + c.max_n - 2, c.max_n);
-  const int chunk = c.max_chunk > 0 ? c.max_chunk : 4096;
+  // default pass: the whole batch's context up to 32768 rows (larger passes keep the
+  // matrix cores busier; the scratch grows by about 32 d bytes per row)
+  const int chunk = c.max_chunk > 0 ? c.max_chunk
+                                    : (int)std::min<int64_t>(32768, std::max<int64_t>(4096, (int64_t)c.max_batch * c.max_ctx));
   s.Mc = std::max({chunk, s.B * s.nmax, s.B * s.Wcap});
   s.Ml = s.Mc + s.B;
   s.Mm = s.B * s.Wcap;
