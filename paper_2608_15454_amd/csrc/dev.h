@@ -22,12 +22,16 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 // bfloat16 hi / lo halves of two floats, packed as (x0 | x1 << 16): hi = bf16(x),
 // lo = bf16(x - hi), both rounded to nearest even by the gfx950 conversion
-// instruction (the compiler emits v_cvt_pk_bf16_f32 for these casts).
+// instruction (the compiler emits one v_cvt_pk_bf16_f32 per pair for these vector
+// conversions).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ void bf16_hi_lo2(float x0, float x1, uint32_t& hi, uint32_t& lo) {
-  const __bf16 h0 = (__bf16)x0, h1 = (__bf16)x1;
-  const __bf16 l0 = (__bf16)(x0 - (float)h0), l1 = (__bf16)(x1 - (float)h1);
-  hi = (uint32_t)__builtin_bit_cast(uint16_t, h0) | ((uint32_t)__builtin_bit_cast(uint16_t, h1) << 16);
-  lo = (uint32_t)__builtin_bit_cast(uint16_t, l0) | ((uint32_t)__builtin_bit_cast(uint16_t, l1) << 16);
+  const f32x2_t v = {x0, x1};
+  const bf16x2_t h = __builtin_convertvector(v, bf16x2_t);  // one packed conversion per pair
+  const bf16x2_t l = __builtin_convertvector(v - __builtin_convertvector(h, f32x2_t), bf16x2_t);
+  hi = __builtin_bit_cast(uint32_t, h);
+  lo = __builtin_bit_cast(uint32_t, l);
 }
 
 template <typename W>

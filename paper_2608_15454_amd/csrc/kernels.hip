@@ -432,6 +432,7 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) 
 // group while it is resident.
 constexpr int kBigBM = 128, kBigBN = 128, kBigBK = 32, kBigLD = kBigBK + 8, kBigMaxGainK = 4096;
 
+template <bool NORM>
 __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr) {
   constexpr int BM = kBigBM, BN = kBigBN, BK = kBigBK, LD = kBigLD;
   __shared__ __attribute__((aligned(16))) uint16_t Ah[2][BM * LD];
@@ -456,8 +457,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
   const int am = m0 + lr;
   const bool aok = am < L.M;
   const float* arow = L.X + (size_t)(aok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx + lk;
-  const bool norm = L.gain != nullptr;
-  if (norm)
+  if (NORM)
     for (int k = tid * 4; k < L.K; k += 256 * 4) *reinterpret_cast<float4*>(&gs[k]) = *reinterpret_cast<const float4*>(L.gain + k);
   const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K) + lk;
   float ss = 0.f;
@@ -477,8 +477,8 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
     uint32_t p[8], q[8];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      float4 t = f.a[v];
-      if (norm && aok) {
+      float4 t = f.a[v];  // rows past M hold zeros
+      if (NORM) {
         ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
         const float4 g = *reinterpret_cast<const float4*>(&gs[lk + k0 + 4 * v]);
         t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
@@ -528,18 +528,19 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
   };
   const int nk = L.K / BK;  // >= 1
   fetch(f0, 0);
-  if (nk > 1) fetch(f1, BK);
+  fetch(f1, BK);
   __syncthreads();  // the gain vector
   stage(f0, 0, 0);
   __syncthreads();
-  // step kt: request step kt + 2 into the register set step kt just left, run step
-  // kt's MFMAs, stage step kt + 1 (in the other set) into the other LDS stage
+  // step kt: request step kt + 2, run step kt's MFMAs, stage step kt + 1 (fetched a
+  // step earlier) into the other LDS stage
+  // (nk is even: two steps per iteration, each register set and LDS stage in a fixed
+  // place)
   for (int kt = 0; kt < nk; kt += 2) {
     if (kt + 2 < nk) fetch(f0, (kt + 2) * BK);
     mfmas(0);
-    if (kt + 1 < nk) stage(f1, (kt + 1) * BK, 1);
+    stage(f1, (kt + 1) * BK, 1);
     __syncthreads();
-    if (kt + 1 >= nk) break;
     if (kt + 3 < nk) fetch(f1, (kt + 3) * BK);
     mfmas(1);
     if (kt + 2 < nk) stage(f0, (kt + 2) * BK, 0);
@@ -548,7 +549,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
   const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
   // the two threads of a staged row hold its sum of squares over K
   ss += xor_lane<1>(ss);
-  if (norm && (tid & 1) == 0) rs[lr] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
+  if (NORM && (tid & 1) == 0) rs[lr] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
   __syncthreads();
   const int jj = lane & 31;
   auto out_block = [&](const f32x16& c, int i, int j) {
@@ -557,7 +558,7 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
     for (int r = 0; r < 16; ++r) {
       const int ml = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
       const int m = m0 + ml;
-      const float val = norm ? c[r] * rs[ml] : c[r];
+      const float val = NORM ? c[r] * rs[ml] : c[r];
       const float partner = xor_lane<1>(val);  // column n + 1, same row (used by even columns)
       if (m < L.M) {
         if (!pair) epi_single(L.epi, m, n, val);
@@ -1798,13 +1799,14 @@ bool mfma_fits(const Linear& L) {
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
   // large M: the 128x128 tile, once its grid fills every compute unit twice
-  if (mfma_fits<W>(L) && L.N % kBigBN == 0 && L.K % kBigBK == 0 && L.gain2 == nullptr &&
+  if (mfma_fits<W>(L) && L.N % kBigBN == 0 && L.K % (2 * kBigBK) == 0 && L.gain2 == nullptr &&
       (L.gain == nullptr || L.K <= kBigMaxGainK) &&
-      (int64_t)(L.N / kBigBN) * ((L.M + kBigBM - 1) / kBigBM) >= 512) {
+      (int64_t)(L.N / kBigBN) * ((L.M + kBigBM - 1) / kBigBM) >= 256) {
     // row blocks per L2 group: about 2 MiB of float32 X rows
     const int gr = std::max(1, std::min(8, (int)((2 << 20) / ((int64_t)kBigBM * L.K * 4))));
     const dim3 grid(L.N / kBigBN, (L.M + kBigBM - 1) / kBigBM);
-    return klaunch(gemm_mfma_big_kernel, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
+    if (L.gain != nullptr) return klaunch(gemm_mfma_big_kernel<true>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
+    return klaunch(gemm_mfma_big_kernel<false>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
   }
   if (mfma_fits<W>(L)) {
     // split K until about kMfmaTargetBlocks blocks stream the weights (the partials
