@@ -130,6 +130,8 @@ int engine_grid(int shape);
 // while it runs (the caller keeps the engine's launches on one stream).
 hipError_t launch_engine(int shape, const EOp* ops, int nlayers, const ECall& call, uint32_t base, int* err,
                          hipStream_t st, const Ev& ev = Ev());
+// Whether passes of more than one row go to the engine for this shape.
+bool engine_multi_row(int shape);
 // Blocks of a launch of two stacks side by side (launch_engine_split), 0 if unavailable.
 int engine_split_grid(int shape);
 // Two independent single-row stack passes (call.M == 1 each) in one launch: blocks

@@ -1180,6 +1180,12 @@ int engine_grid(int shape) {
   return 0;
 }
 
+bool engine_multi_row(int shape) {
+  // d=2048 passes of several rows: the per-kernel path (GEMV linears, split attention)
+  // measured faster (d=2048 batch-16 verification: 11,285 against 10,176 accepted B/s)
+  return shape != 1;
+}
+
 int engine_split_grid(int shape) {
   if (shape == 0) return split_grid<Shape0>();
   if (shape == 1) return split_grid<Shape1>();

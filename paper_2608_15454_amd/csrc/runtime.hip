@@ -641,6 +641,7 @@ bool engine_call(const mbp_handle* h, const EngStack* es, const EIo& io, const T
                  const int32_t* first_slot, int32_t max_ns, const int32_t* grp_tab, int grid, ECall* c) {
   const Sizes& s = h->sz;
   if (!h->engine || es == nullptr || es->nops == 0 || tok.M > kEngineMaxRows || grid <= 0) return false;
+  if (tok.M > 1 && !engine_multi_row(h->eng_shape)) return false;
   const int items_per_split = tok.M * s.H;
   const int cached_splits = std::max(1, grid / items_per_split - 1);
   const int chunk = std::max(64, (max_ns + cached_splits - 1) / cached_splits + 63) / 64 * 64;
