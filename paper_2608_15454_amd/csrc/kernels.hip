@@ -419,6 +419,164 @@ __global__ __launch_bounds__(256) void gemm_finish_kernel(Linear L, int ksplit) 
   else epi_single(L.epi, m, n, a0);
 }
 
+// Linears of 17..64 rows with bfloat16 weights and K = 8 x 32 x NSTEP (decode passes
+// of many rows: a batch's commits, its MB windows) in one launch, without split-K
+// partials.  A block of eight waves owns 32 output columns and MT x 32 rows; its waves
+// split K eight ways.  Each wave requests its whole operand slices at once -- the
+// weights (32 columns x 32*NSTEP, straight into the B-operand layout) and its X rows --
+// so it waits for one round trip, not one per step.  Products on
+// v_mfma_f32_16x16x32_bf16 (lane l supplies row / column l % 16 and k positions
+// 8 (l / 16) .. +7 of each 32-wide step; the accumulator holds rows 4 (l / 16) .. +3 of
+// column l % 16).  X (a few hundred KiB, re-read by every column tile from L2) is what
+// bounds the kernel, so it is read in row order -- eight lanes per 128-byte piece of a
+// row, eight rows per instruction -- which the L1 serves about three times faster than
+// the operand layout (16 rows per instruction); each step's 32 columns of the wave's
+// rows are scaled by the norm gain, split into bf16 hi + lo (as in the tiled kernel)
+// and written to the wave's own LDS tile, from which the A fragments are read back.
+// The eight slices are added in LDS (the tiles' memory) in wave order, and the block
+// runs the epilogue.  (Splitting K over blocks as well, with the last block adding
+// tagged partials, cost about 8 us per launch in memory round trips -- more than the
+// tiled kernel's second launch -- so wider K stays on that kernel.)
+constexpr int kRowsNW = 8, kRowsLD = 36, kRowsXL = 40;  // waves per block; LDS row pitches
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <int MT, int NSTEP, bool NORM>
+__global__ __launch_bounds__(512) void gemm_rows_kernel(Linear L) {
+  constexpr int NW = kRowsNW, LD = kRowsLD, XL = kRowsXL, ROWS = MT * 32, RT = ROWS / 16, KS = NSTEP * 32;
+  constexpr int XI = ROWS / 8;                                // X loads per lane and step
+  constexpr int CPT = ROWS * 32 / (NW * 64), TPR = 32 / CPT;  // columns per thread, threads per row
+  constexpr int TILE = 2 * ROWS * XL;                         // bf16 of a wave's X tile (hi, lo)
+  constexpr int BYTES = NW * TILE * 2 > NW * ROWS * LD * 4 ? NW * TILE * 2 : NW * ROWS * LD * 4;
+  __shared__ __attribute__((aligned(16))) char lds[BYTES];
+  __shared__ float ssl[NW][ROWS];
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int c = lane & 15, g = lane >> 4;        // operand layout
+  const int lr = lane >> 3, lk = (lane & 7) * 4;  // row-order X loads: row 8 i + lr, columns lk .. +3
+  const int n0 = blockIdx.x * 32;
+  const int k0 = wave * KS;  // the wave's K slice: k0 .. k0 + KS
+  uint16_t* xt = reinterpret_cast<uint16_t*>(lds) + wave * TILE;
+  // X row indices first (a gather's index loads are the only ones a later load
+  // waits for); rows past M read row M-1 and are zeroed when converted, so every
+  // operand load below is issued unconditionally
+  int xrow[XI];
+  if (L.xidx != nullptr) {
+#pragma unroll
+    for (int i = 0; i < XI; ++i) xrow[i] = L.xidx[min(8 * i + lr, L.M - 1)];
+  } else {
+#pragma unroll
+    for (int i = 0; i < XI; ++i) xrow[i] = min(8 * i + lr, L.M - 1);
+  }
+  // weight rows: the matrix of a fused row is chosen among the three pointers by
+  // selects (indexing the pointer array per lane would load it from memory first)
+  const uint16_t* m0p = reinterpret_cast<const uint16_t*>(L.mats.m[0]);
+  const uint16_t* m1p = reinterpret_cast<const uint16_t*>(L.mats.m[1]);
+  const uint16_t* m2p = reinterpret_cast<const uint16_t*>(L.mats.m[2]);
+  uint4 wf[NSTEP][2];
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const int n = n0 + ct * 16 + c;
+    int which, r;
+    if (L.mats.mode == MAT_SINGLE) {
+      which = 0; r = n;
+    } else if (L.mats.mode == MAT_QKV) {
+      which = n >= 2 * L.mats.rows ? 2 : (n >= L.mats.rows ? 1 : 0); r = n - which * L.mats.rows;
+    } else {
+      which = n & 1; r = n >> 1;
+    }
+    const uint16_t* wrow = (which == 0 ? m0p : (which == 1 ? m1p : m2p)) + (size_t)r * L.K + k0 + g * 8;
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) wf[s][ct] = *reinterpret_cast<const uint4*>(wrow + s * 32);
+  }
+  float4 xb[NSTEP][XI];
+#pragma unroll
+  for (int i = 0; i < XI; ++i) {
+    const float* xr = L.X + (size_t)xrow[i] * L.ldx + k0 + lk;
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) xb[s][i] = *reinterpret_cast<const float4*>(xr + s * 32);
+  }
+  float4 gq[NORM ? NSTEP : 1];
+  if (NORM) {
+#pragma unroll
+    for (int s = 0; s < NSTEP; ++s) gq[s] = *reinterpret_cast<const float4*>(L.gain + k0 + s * 32 + lk);
+  }
+  f32x4 acc[RT][2];
+  float ss[XI];
+#pragma unroll
+  for (int i = 0; i < XI; ++i) ss[i] = 0.f;
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) acc[rt][0] = acc[rt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NSTEP; ++s) {
+    // the step's 32 columns of the wave's rows, as bf16 hi + lo, into its LDS tile
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      float4 v = xb[s][i];
+      if (8 * i + lr >= L.M) v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (NORM) {
+        ss[i] += v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        v.x *= gq[s].x; v.y *= gq[s].y; v.z *= gq[s].z; v.w *= gq[s].w;
+      }
+      uint32_t h0, l0, h1, l1;
+      bf16_hi_lo2(v.x, v.y, h0, l0);
+      bf16_hi_lo2(v.z, v.w, h1, l1);
+      *reinterpret_cast<uint2*>(xt + (8 * i + lr) * XL + lk) = make_uint2(h0, h1);
+      *reinterpret_cast<uint2*>(xt + ROWS * XL + (8 * i + lr) * XL + lk) = make_uint2(l0, l1);
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): the tile is written (only this wave reads it)
+    __builtin_amdgcn_wave_barrier();
+    const bf16x8 b0 = __builtin_bit_cast(bf16x8, wf[s][0]);
+    const bf16x8 b1 = __builtin_bit_cast(bf16x8, wf[s][1]);
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      const bf16x8 ah = *reinterpret_cast<const bf16x8*>(xt + (rt * 16 + c) * XL + g * 8);
+      const bf16x8 al = *reinterpret_cast<const bf16x8*>(xt + ROWS * XL + (rt * 16 + c) * XL + g * 8);
+      acc[rt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b0, acc[rt][0], 0, 0, 0);
+      acc[rt][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b0, acc[rt][0], 0, 0, 0);
+      acc[rt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, b1, acc[rt][1], 0, 0, 0);
+      acc[rt][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, b1, acc[rt][1], 0, 0, 0);
+    }
+    __builtin_amdgcn_wave_barrier();  // the next step rewrites the tile after these reads
+  }
+  if (NORM) {  // a row's sum of squares over the wave's slice: its eight lanes
+#pragma unroll
+    for (int i = 0; i < XI; ++i) {
+      const float t = group_sum<8>(ss[i]);
+      if ((lane & 7) == 0) ssl[wave][8 * i + lr] = t;
+    }
+  }
+  __syncthreads();  // every wave is done with its tile: the memory now holds the slice sums
+  float* red = reinterpret_cast<float*>(lds);
+  // register i of lane (c, g) in tile (rt, ct) is row rt*16 + 4g + i, column ct*16 + c
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[(wave * ROWS + rt * 16 + 4 * g + i) * LD + ct * 16 + c] = acc[rt][ct][i];
+  __syncthreads();
+  // thread: row `row`, columns col0 .. col0 + CPT - 1 of the tile
+  const int row = tid / TPR, col0 = (tid % TPR) * CPT;
+  float v[CPT];
+#pragma unroll
+  for (int j = 0; j < CPT; ++j) v[j] = 0.f;
+  float sst = 0.f;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) v[j] += red[(w * ROWS + row) * LD + col0 + j];
+    if (NORM) sst += ssl[w][row];
+  }
+  if (row >= L.M) return;
+  const float sc = NORM ? 1.0f / sqrtf(sst / (float)L.K + L.eps) : 1.0f;
+  if (L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV) {
+#pragma unroll
+    for (int j = 0; j < CPT; j += 2) epi_pair(L.epi, row, n0 + col0 + j, v[j] * sc, v[j + 1] * sc);
+  } else {
+#pragma unroll
+    for (int j = 0; j < CPT; ++j) epi_single(L.epi, row, n0 + col0 + j, v[j] * sc);
+  }
+}
+
 // The same product for large M (prefill, long commits): a 128x128 output tile per
 // block of four waves, each wave a 64x64 quarter (2 x 2 blocks of
 // v_mfma_f32_32x32x16_bf16, X in bfloat16 hi + lo as above), K in steps of 32.  Two LDS
@@ -1030,7 +1188,6 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
 //     in the same key order.
 // Partials per (query row, head, split) as attn_decode_kernel's; attn_merge_kernel
 // combines the splits.
-typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMqTile = 32;          // keys per wave and round
 constexpr int kMqRound = 4 * kMqTile;  // keys per block and round
@@ -1796,6 +1953,31 @@ bool mfma_fits(const Linear& L) {
   return std::is_same<W, uint16_t>::value && L.M > kMfmaMinRows && L.N % 64 == 0 && L.K % kMfmaBK == 0;
 }
 
+// The row kernel: 17..64 rows, K a whole number of eight 32/64/128-column slices, no
+// per-row gain (the head's two norms), and enough 32-column tiles that its blocks
+// stream the weights from most compute units (with fewer, the tiled kernel's split-K
+// is faster).
+constexpr int kRowsMinTiles = 64;
+
+template <typename W>
+bool rows_fits(const Linear& L) {
+  return mfma_fits<W>(L) && L.M <= 64 && L.gain2 == nullptr && L.N % 32 == 0 && L.N / 32 >= kRowsMinTiles &&
+         (L.K == kRowsNW * 32 || L.K == kRowsNW * 64 || L.K == kRowsNW * 128);
+}
+
+template <int MT, int NSTEP>
+hipError_t rows_launch_t(const Linear& L, hipStream_t st, const Ev& ev) {
+  const dim3 grid(L.N / 32);
+  if (L.gain != nullptr) return klaunch(gemm_rows_kernel<MT, NSTEP, true>, grid, dim3(512), 0, st, ev.start, ev.stop, L);
+  return klaunch(gemm_rows_kernel<MT, NSTEP, false>, grid, dim3(512), 0, st, ev.start, ev.stop, L);
+}
+
+hipError_t rows_launch(const Linear& L, hipStream_t st, const Ev& ev) {
+  const int ns = L.K / (kRowsNW * 32);
+  if (L.M <= 32) return ns == 4 ? rows_launch_t<1, 4>(L, st, ev) : ns == 2 ? rows_launch_t<1, 2>(L, st, ev) : rows_launch_t<1, 1>(L, st, ev);
+  return ns == 4 ? rows_launch_t<2, 4>(L, st, ev) : ns == 2 ? rows_launch_t<2, 2>(L, st, ev) : rows_launch_t<2, 1>(L, st, ev);
+}
+
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
   // large M: the 128x128 tile, once its grid fills every compute unit twice
@@ -1808,6 +1990,7 @@ hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& e
     if (L.gain != nullptr) return klaunch(gemm_mfma_big_kernel<true>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
     return klaunch(gemm_mfma_big_kernel<false>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
   }
+  if (rows_fits<W>(L)) return rows_launch(L, st, ev);
   if (mfma_fits<W>(L)) {
     // split K until about kMfmaTargetBlocks blocks stream the weights (the partials
     // and the splits' sums of squares must fit)

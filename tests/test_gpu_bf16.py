@@ -69,6 +69,17 @@ def test_d1024_batched_ragged(w1024):
 
 
 @pytest.mark.timeout(900)
+def test_d1024_batch24_row_kernel(w1024_plain):
+    """24 rows: each step's commit (one byte per row at logit gain 1) runs 24-row
+    linear layers, the 32-row tiles of the one-launch row kernel."""
+    raw, W = w1024_plain
+    prompts = [synth.make_prompt(40 + r, 32 + r) for r in range(24)]
+    dec = new_decoder(D1024, raw, 24, 200)
+    st = forced_run(dec, W, D1024, prompts, 3, 3, 0.75, label="b24")
+    print(st)
+
+
+@pytest.mark.timeout(900)
 def test_d1024_full_prompt_sampled_steps(w1024_plain):
     """Full 4096-byte prompt of the batch-1 workload: the first steps compared."""
     raw, W = w1024_plain
