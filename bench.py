@@ -73,6 +73,12 @@ CLASS_SOURCE = {"engine": "engine.hip", "gemv": "kernels.hip", "gemm": "kernels.
                 "other": "kernels.hip"}
 
 
+def traffic_key(workload, logit_gain=1.0):
+    """The name a counter record is filed under: the workload, plus the logit gain when it
+    is not the workload's own (acceptance, and so the launches, differ with it)."""
+    return workload if logit_gain == 1.0 else f"{workload}_gain{logit_gain:g}"
+
+
 def measured_traffic(kernel_class, workload):
     """Bytes per launch recorded for kernel_class on workload, or None when there is no
     record or the class's source has changed since the counters were taken."""
@@ -419,7 +425,7 @@ def bench_decode(args, wl, K, W, logit_gain, cpu_seconds=0.0, weights=None):
         roofline = {
             "bound": "hbm", "kernel": f"{dom} (all launches of the class in the timed steps)",
             "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom, wl.name),
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom, traffic_key(wl.name, logit_gain)),
             "launches": launches, "avg_launch_us": round(ms * 1000.0 / max(launches, 1), 3),
             "bytes_per_launch": round(nbytes / max(launches, 1)),
         }
