@@ -145,6 +145,19 @@ def test_forward_d1024_bf16():
 
 
 @pytest.mark.timeout(600)
+@pytest.mark.parametrize("T", [24, 48])
+def test_forward_d1024_short(T):
+    """The d=1024 model on 24 and 48 bytes: every linear layer of the trunk is one pass
+    of 17..64 rows with K = 1024 (the one-launch row GEMM, 32- and 64-row tiles)."""
+    model = synth.WORKLOADS["lca_d1024_b1"].model
+    raw = synth.make_weights(model, seed=0, logit_gain=8.0)
+    W = oracle.to_float64(raw)
+    dec = new_decoder(model, raw, 1, 128)
+    ref = check(dec, W, model, synth.make_prompt(3, 256)[:T], base_tol(model))
+    print("k", ref["k"], "sum_nt", ref["sum_nt"], "sum_mb", ref["sum_mb"])
+
+
+@pytest.mark.timeout(600)
 def test_forward_d1024_full_sequence():
     """The benchmarked configuration: the d=1024 model on the whole 4096-byte sequence,
     the launch shapes the forward bench times (one 4096-row pass per stack), every
