@@ -79,8 +79,16 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *   rope_base, rms_eps, attn_scale   1e5, 1e-6 and 1.0 in the paper.  Attention
  *                             scores are q.k / sqrt(d_head) * attn_scale.
  *   window_mode               0: the MB layers run on the window of Algorithm 1 only
- *                             (previous + current group + n-2 virtual rows).  Other
- *                             values are rejected with MBP_EINVAL.
+ *                             (previous + current group + n-2 virtual rows), so at a
+ *                             segment end the previous group's rows are recomputed
+ *                             seeing only their own group.  1: the MB layers run over
+ *                             the whole sequence under the full LCA mask (the training
+ *                             mask of mbp_forward): rows keep the outputs they had when
+ *                             they were computed, each seeing its whole previous group.
+ *                             The two agree when n_mb = 1.  Mode 1 keeps MB rows and
+ *                             their caches for every position (max_window defaults to
+ *                             max_ctx + max_n; its first update runs the whole prefix).
+ *                             Other values: MBP_EINVAL.
  *   kv_dtype                  storage type of every KV cache: MBP_F32, MBP_BF16 or
  *                             MBP_F16.  MBP_F16 stores the same bytes as bf16 with 3
  *                             more mantissa bits; values beyond +-65504 saturate.

@@ -99,6 +99,9 @@ struct Row {
   int64_t epoch = 0;        // bumped whenever the latent list changes
   int64_t win_epoch = -1;   // epoch of the MB window cache
   int32_t win_s = 0, win_valid = 0;
+  // window mode 1: the lowest position whose cached MB rows are stale (a segment end
+  // there or a truncation below it moved the group of the rows from it on)
+  int32_t mb_stale = 0;
   // a byte accepted by external verification and not yet committed (-1: none); the
   // next tentative commit of drafts starts with it
   int32_t bonus = -1;
@@ -162,9 +165,10 @@ bool valid_cfg(const mbp_config* c, std::string* why) {
   if (c->max_n < 1 || c->max_n > kMaxN) return bad("max_n must be in [1, 8]");
   if (c->max_patch < 0) return bad("max_patch must be >= 0");
   if (c->max_window < 0) return bad("max_window must be >= 0");
-  if (c->max_window == 0 && c->max_patch == 0) return bad("max_window must be given when max_patch = 0");
+  if (c->max_window == 0 && c->max_patch == 0 && c->window_mode == 0)
+    return bad("max_window must be given when max_patch = 0");
   if (c->max_chunk < 0) return bad("max_chunk must be >= 0");
-  if (c->window_mode != 0) return bad("only window_mode 0 is implemented");
+  if (c->window_mode != 0 && c->window_mode != 1) return bad("window_mode must be 0 or 1");
   if (c->kv_dtype != MBP_F32 && c->kv_dtype != MBP_BF16 && c->kv_dtype != MBP_F16) return bad("bad kv_dtype");
   if (c->no_engine != 0 && c->no_engine != 1) return bad("no_engine must be 0 or 1");
   if (c->boundary_mode != 0 && c->boundary_mode != 1) return bad("boundary_mode must be 0 or 1");
@@ -182,7 +186,10 @@ Sizes sizes_of(const mbp_config& c) {
   s.Tcap = c.max_ctx;
   s.Kcap = c.max_latents + 1;
   s.nmax = c.max_n;
-  s.Wcap = c.max_window > 0 ? c.max_window : std::max(2 * c.max_patch + c.max_n - 2, c.max_n);
+  // window mode 1 keeps MB rows for the whole sequence (its window starts at byte 0)
+  s.Wcap = c.max_window > 0     ? c.max_window
+           : c.window_mode == 1 ? c.max_ctx + c.max_n
+                                : std::max(2 * c.max_patch + c.max_n - 2, c.max_n);
   // default pass: the whole batch's context up to 32768 rows (larger passes keep the
   // matrix cores busier; the scratch grows by about 32 d bytes per row)
   const int chunk = c.max_chunk > 0 ? c.max_chunk
@@ -808,10 +815,14 @@ void truncate_row(Row& r, int32_t T) {
     r.epoch++;
     r.lm_rows = (int32_t)r.q.size() + 1;
   }
+  r.mb_stale = std::min(r.mb_stale, T);
 }
 
-// Window start of a row: first byte of the previous group (byte 0 for groups 0, 1).
-int32_t window_start(const Row& r) {
+// Window start of a row: first byte of the previous group (byte 0 for groups 0, 1);
+// byte 0 in window mode 1 (the full-sequence LCA mask: a row of group j sees all of
+// group j-1, whose own rows saw group j-2, and so on).
+int32_t window_start(const mbp_config& c, const Row& r) {
+  if (c.window_mode == 1) return 0;
   const int32_t g = (int32_t)r.q.size();
   return g >= 2 ? r.q[g - 2] : 0;
 }
@@ -844,20 +855,34 @@ int mb_prepare(mbp_handle* h, int n, Plan& p, bool clamp, MbPass* out) {
     Row& r = h->rows[b];
     const int32_t t = (int32_t)r.x.size() - 1;
     const int32_t g = (int32_t)r.q.size();
-    const int32_t sw = window_start(r);
+    const int32_t sw = window_start(h->cfg, r);
     int32_t W = t + n - 1 - sw;
     if (W > s.Wcap) {
       if (!clamp) return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
       W = s.Wcap;
     }
-    if (r.win_epoch != r.epoch || r.win_s != sw) {
+    if (h->cfg.window_mode == 1) {
+      // rows keep their outputs across segment ends: only rows from the first
+      // position whose group moved on are recomputed
       r.win_epoch = r.epoch;
-      r.win_s = sw;
-      r.win_valid = 0;
-    }
-    for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
-      const int32_t pos = sw + w;
-      grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
+      r.win_s = 0;
+      r.win_valid = std::min(r.win_valid, r.mb_stale);
+      r.mb_stale = INT32_MAX;
+      int32_t j = 0;  // boundaries at or before pos, walked along the row
+      for (int32_t pos = 0; pos < std::max(W, r.win_valid); ++pos) {
+        while (j < g && r.q[j] <= pos) ++j;
+        grp_tab[(size_t)b * s.Wcap + pos] = pos <= t ? j : g;
+      }
+    } else {
+      if (r.win_epoch != r.epoch || r.win_s != sw) {
+        r.win_epoch = r.epoch;
+        r.win_s = sw;
+        r.win_valid = 0;
+      }
+      for (int32_t w = 0; w < std::max(W, r.win_valid); ++w) {
+        const int32_t pos = sw + w;
+        grp_tab[(size_t)b * s.Wcap + w] = pos <= t ? group_of(r, pos) : g;
+      }
     }
     for (int32_t w = r.win_valid; w < W; ++w) {
       const int32_t G = grp_tab[(size_t)b * s.Wcap + w];
@@ -1032,6 +1057,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
         lat_row.push_back(b * s.Kcap);
         r.lm_rows = 1;
         r.epoch++;
+        r.mb_stale = 0;
         max_kv_l = std::max(max_kv_l, 1);
         lm_keys[b] = 1;
       }
@@ -1047,6 +1073,7 @@ int commit(mbp_handle* h, const std::vector<std::vector<uint8_t>>& add, bool for
         lat_row.push_back(b * s.Kcap + j);
         r.lm_rows = j + 1;
         r.epoch++;
+        r.mb_stale = std::min(r.mb_stale, pos);
         max_kv_l = std::max(max_kv_l, j + 1);
         lm_keys[b] = j + 1;
       }
@@ -1809,7 +1836,7 @@ static int decode_step(mbp_handle* h, int32_t n, float tau, int32_t mode, const 
   if (c.head == MBP_HEAD_LCA && n >= 2) {
     for (int b = 0; b < B; ++b) {
       const Row& r = h->rows[b];
-      if ((int32_t)r.x.size() + n - 2 - window_start(r) > s.Wcap)
+      if ((int32_t)r.x.size() + n - 2 - window_start(c, r) > s.Wcap)
         return fail(h, MBP_ECAPACITY, "MB window exceeds max_window");
     }
   }

@@ -78,7 +78,7 @@ def test_workspace_bytes_positive_and_monotone(mbp):
 @pytest.mark.parametrize("field,value", [
     ("d_model", 0), ("n_heads", 3), ("d_ff", 100), ("n_lm", -1), ("head", 5), ("dtype", 7),
     ("max_batch", 0), ("max_ctx", 1), ("max_n", 0), ("max_n", 9), ("max_patch", -1),
-    ("window_mode", 1), ("rope_base", 0.0),
+    ("window_mode", 2), ("rope_base", 0.0),
 ])
 def test_invalid_configs_rejected(mbp, field, value):
     L = mbp.lib()
@@ -90,6 +90,19 @@ def test_invalid_configs_rejected(mbp, field, value):
     ptrs = (ctypes.c_void_p * 1)(1)
     assert L.mbp_init(ctypes.byref(cfg), ptrs, 1, ctypes.c_void_p(256), 1 << 40, None, ctypes.byref(h)) == mbp.EINVAL
     assert not h.value
+
+
+def test_window_mode_1_accepted(mbp):
+    """Window mode 1 keeps MB rows for the whole sequence: accepted with the pure space
+    rule and no max_window, with a larger workspace than mode 0."""
+    L = mbp.lib()
+    cfg = _cfg(mbp)
+    a = L.mbp_workspace_bytes(ctypes.byref(cfg))
+    cfg.window_mode = 1
+    b = L.mbp_workspace_bytes(ctypes.byref(cfg))
+    cfg.max_patch = 0
+    c = L.mbp_workspace_bytes(ctypes.byref(cfg))
+    assert 0 < a < b and c > 0
 
 
 def test_pure_space_rule_needs_max_window(mbp):
