@@ -516,7 +516,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py: this build measures one GPU; the decode rows are independent and would shard "
+        print("bench.py measures one GPU; the decode rows are independent and would shard "
               "by batch row with no per-step exchange, but no multi-GPU run is provided.", file=sys.stderr)
         sys.exit(2)
 
