@@ -113,6 +113,16 @@ __device__ __forceinline__ void swap_halves(float& a, float& b) {
   b = __builtin_bit_cast(float, ub);
 }
 
+// f(std::integral_constant<int, 0>()), ..., f(std::integral_constant<int, N - 1>()):
+// a loop whose index is a constant expression in every iteration.
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (N > 0) {
+    static_for<N - 1>(f);
+    f(std::integral_constant<int, N - 1>());
+  }
+}
+
 // x of lane (lane ^ O), O a power of two below 64.
 template <int O>
 __device__ __forceinline__ float xor_lane(float x) {

@@ -577,27 +577,41 @@ __global__ __launch_bounds__(512) void gemm_rows_kernel(Linear L) {
   }
 }
 
-// The same product for large M (prefill, long commits): a 128x128 output tile per
-// block of four waves, each wave a 64x64 quarter (2 x 2 blocks of
-// v_mfma_f32_32x32x16_bf16, X in bfloat16 hi + lo as above), K in steps of 32.  Two LDS
-// stages and two register stages: the X and weight rows of step k+2 are requested
+// The same product for large M (prefill, long commits, the full-sequence forward):
+// one output tile of BM x BN per block of WM x WN waves, each wave TI x TJ blocks of
+// v_mfma_f32_32x32x16_bf16 (X in bfloat16 hi + lo as above), K in steps of 32.  Two
+// LDS stages and two register stages: the X and weight rows of step k+2 are requested
 // while step k's MFMAs run and step k+1 is staged, so each fetch has two steps to
-// arrive (the steps are latency-bound otherwise); one barrier per step.  Twice the
-// output per staged byte of the 64x64 tile.  Order: the blocks of XCD k (workgroups go
-// to the 8 XCDs round-robin) take groups of GR row blocks k, k+8, ... and walk the
-// column blocks with the group's rows fastest, so the group's X rows (GR x 128 rows)
-// stay in the XCD's L2 across the columns and each weight tile is used by the whole
-// group while it is resident.
-constexpr int kBigBM = 128, kBigBN = 128, kBigBK = 32, kBigLD = kBigBK + 8, kBigMaxGainK = 4096;
+// arrive (the steps are latency-bound otherwise); one barrier per step.  Every thread
+// stages four 4-wide pieces of X rows and two 8-wide pieces of weight rows per step
+// (BM = BN = threads / 2).
+// Two shapes: 128 x 128 (four waves of 64 x 64, two blocks per CU) and 256 x 256 (eight
+// waves of 64 rows x 128 columns, one block per CU), which stages half the bytes per
+// flop and, since the hi / lo split doubles every X operand, reads the fewest LDS
+// bytes per MFMA with wave tiles twice as wide as tall.  Order: the blocks of XCD k
+// (workgroups go to the 8 XCDs round-robin) take groups of GR row blocks k, k+8, ...
+// and walk the column blocks with the group's rows fastest, so the group's X rows stay
+// in the XCD's L2 across the columns and each weight tile is used by the whole group
+// while it is resident.
+constexpr int kBigBK = 32, kBigLD = kBigBK + 8, kBigMaxGainK = 4096;
 
-template <bool NORM>
-__global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr) {
-  constexpr int BM = kBigBM, BN = kBigBN, BK = kBigBK, LD = kBigLD;
+template <int WM, int WN, int TI, int TJ>
+struct BigTile {
+  static constexpr int threads = 64 * WM * WN, BM = 32 * TI * WM, BN = 32 * TJ * WN;
+  static_assert(BM == threads / 2 && BN == threads / 2, "four X row pieces and two weight row pieces per thread");
+};
+using BigTile128 = BigTile<2, 2, 2, 2>;
+using BigTile256 = BigTile<4, 2, 2, 4>;
+
+template <int WM, int WN, int TI, int TJ, bool NORM>
+__global__ __launch_bounds__(64 * WM * WN, 2) void gemm_mfma_big_kernel(Linear L, int gr) {
+  using T = BigTile<WM, WN, TI, TJ>;
+  constexpr int BM = T::BM, BN = T::BN, NT = T::threads, BK = kBigBK, LD = kBigLD;
   __shared__ __attribute__((aligned(16))) uint16_t Ah[2][BM * LD];
   __shared__ __attribute__((aligned(16))) uint16_t Al[2][BM * LD];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2][BN * LD];
   __shared__ float rs[BM];
-  __shared__ __attribute__((aligned(16))) float gs[kBigMaxGainK];  // the norm gain (one vector for every row)
+  __shared__ __attribute__((aligned(16))) float gs[NORM ? kBigMaxGainK : 4];  // the norm gain (one vector for every row)
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   int bx = blockIdx.x, by = blockIdx.y;
   {
@@ -610,15 +624,38 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
     }
   }
   const int m0 = by * BM, n0 = bx * BN;
-  // loads: thread t stages 16 consecutive k of row t / 2 of both tiles
-  const int lr = tid >> 1, lk = (tid & 1) * 16;
-  const int am = m0 + lr;
-  const bool aok = am < L.M;
-  const float* arow = L.X + (size_t)(aok ? (L.xidx ? L.xidx[am] : am) : 0) * L.ldx + lk;
+  // loads in row order: eight lanes read the 128 bytes of one X row's step (rows
+  // t / 8 + NT / 8 * v), four lanes the 64 bytes of one weight row's step (rows
+  // t / 4 + NT / 4 * u), so each load instruction covers whole lines of few rows.  Rows
+  // past M load row 0 of X and are zeroed before staging.
+  constexpr int AR = NT / 8, BR = NT / 4;
+  const int ar = tid >> 3, ak = (tid & 7) * 4, br = tid >> 2, bk = (tid & 3) * 8;
+  const float* arow[4];
+  unsigned aok = 0;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int m = m0 + ar + AR * v;
+    const bool ok = m < L.M;
+    aok |= (ok ? 1u : 0u) << v;
+    arow[v] = L.X + (size_t)(ok ? (L.xidx ? L.xidx[m] : m) : 0) * L.ldx + ak;
+  }
   if (NORM)
-    for (int k = tid * 4; k < L.K; k += 256 * 4) *reinterpret_cast<float4*>(&gs[k]) = *reinterpret_cast<const float4*>(L.gain + k);
-  const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K) + lk;
-  float ss = 0.f;
+    for (int k = tid * 4; k < L.K; k += NT * 4) *reinterpret_cast<float4*>(&gs[k]) = *reinterpret_cast<const float4*>(L.gain + k);
+  // Pair epilogues (SwiGLU over interleaved gate / up rows, RoPE over (even, odd)
+  // columns of q and k) take columns (2p, 2p + 1) together.  Their weight rows are
+  // staged so that the first half of each wave's 32 TJ columns holds the even columns
+  // and the second half their odd partners: each lane then holds both values of its
+  // pairs.  Tile column c is global column n0 + 32 TJ (c / 32 TJ) + 2 (c % 16 TJ) +
+  // (c / 16 TJ) % 2.
+  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
+  auto bcol = [&](int c) {
+    if (!pair) return n0 + c;
+    const int cc = c % (32 * TJ);
+    return n0 + (c - cc) + 2 * (cc % (16 * TJ)) + cc / (16 * TJ);
+  };
+  const uint16_t* brow0 = mat_row<uint16_t>(L.mats, bcol(br), L.K) + bk;
+  const uint16_t* brow1 = mat_row<uint16_t>(L.mats, bcol(br + BR), L.K) + bk;
+  float ss[4] = {0.f, 0.f, 0.f, 0.f};
   struct Fetch {
     float4 a[4];
     uint4 b0, b1;
@@ -626,65 +663,67 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
   Fetch f0, f1;
   auto fetch = [&](Fetch& f, int k0) {
 #pragma unroll
-    for (int v = 0; v < 4; ++v)
-      f.a[v] = aok ? *reinterpret_cast<const float4*>(arow + k0 + 4 * v) : make_float4(0.f, 0.f, 0.f, 0.f);
-    f.b0 = *reinterpret_cast<const uint4*>(brow + k0);
-    f.b1 = *reinterpret_cast<const uint4*>(brow + k0 + 8);
+    for (int v = 0; v < 4; ++v) f.a[v] = *reinterpret_cast<const float4*>(arow[v] + k0);
+    f.b0 = *reinterpret_cast<const uint4*>(brow0 + k0);
+    f.b1 = *reinterpret_cast<const uint4*>(brow1 + k0);
   };
   auto stage = [&](const Fetch& f, int k0, int buf) {
-    uint32_t p[8], q[8];
+    float4 g;
+    if (NORM) g = *reinterpret_cast<const float4*>(&gs[k0 + ak]);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      float4 t = f.a[v];  // rows past M hold zeros
+      // rows past M: all bits cleared (a mask, not a branch, keeps the waits in order)
+      const uint32_t keep = 0u - ((aok >> v) & 1u);
+      float4 t;
+      t.x = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].x) & keep);
+      t.y = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].y) & keep);
+      t.z = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].z) & keep);
+      t.w = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].w) & keep);
       if (NORM) {
-        ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
-        const float4 g = *reinterpret_cast<const float4*>(&gs[lk + k0 + 4 * v]);
+        ss[v] += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
         t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
       }
-      bf16_hi_lo2(t.x, t.y, p[2 * v], q[2 * v]);
-      bf16_hi_lo2(t.z, t.w, p[2 * v + 1], q[2 * v + 1]);
+      uint32_t p0, p1, q0, q1;
+      bf16_hi_lo2(t.x, t.y, p0, q0);
+      bf16_hi_lo2(t.z, t.w, p1, q1);
+      const int off = (ar + AR * v) * LD + ak;
+      *reinterpret_cast<uint2*>(&Ah[buf][off]) = make_uint2(p0, p1);
+      *reinterpret_cast<uint2*>(&Al[buf][off]) = make_uint2(q0, q1);
     }
-    uint4* ad = reinterpret_cast<uint4*>(&Ah[buf][lr * LD + lk]);
-    ad[0] = make_uint4(p[0], p[1], p[2], p[3]);
-    ad[1] = make_uint4(p[4], p[5], p[6], p[7]);
-    uint4* al = reinterpret_cast<uint4*>(&Al[buf][lr * LD + lk]);
-    al[0] = make_uint4(q[0], q[1], q[2], q[3]);
-    al[1] = make_uint4(q[4], q[5], q[6], q[7]);
-    uint4* bd = reinterpret_cast<uint4*>(&Bs[buf][lr * LD + lk]);
-    bd[0] = f.b0;
-    bd[1] = f.b1;
+    *reinterpret_cast<uint4*>(&Bs[buf][br * LD + bk]) = f.b0;
+    *reinterpret_cast<uint4*>(&Bs[buf][(br + BR) * LD + bk]) = f.b1;
   };
-  const int wm = wave >> 1, wn = wave & 1;
-  f32x16 acc[2][2];
+  const int wm = wave / WN, wn = wave % WN;
+  f32x16 acc[TI][TJ];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < TI; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < TJ; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
   auto mfmas = [&](int cur) {
 #pragma unroll
     for (int ks = 0; ks < BK; ks += 16) {
-      bf16x8 fh[2], fl[2], fb[2];
+      bf16x8 fh[TI], fl[TI], fb[TJ];
 #pragma unroll
-      for (int i = 0; i < 2; ++i) {
-        const int off = (wm * 64 + i * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8;
+      for (int i = 0; i < TI; ++i) {
+        const int off = (wm * 32 * TI + i * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8;
         fh[i] = *reinterpret_cast<const bf16x8*>(&Ah[cur][off]);
         fl[i] = *reinterpret_cast<const bf16x8*>(&Al[cur][off]);
       }
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        fb[j] = *reinterpret_cast<const bf16x8*>(&Bs[cur][(wn * 64 + j * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8]);
+      for (int j = 0; j < TJ; ++j)
+        fb[j] = *reinterpret_cast<const bf16x8*>(&Bs[cur][(wn * 32 * TJ + j * 32 + (lane & 31)) * LD + ks + (lane >> 5) * 8]);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < TI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
+        for (int j = 0; j < TJ; ++j) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fh[i], fb[j], acc[i][j], 0, 0, 0);
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fl[i], fb[j], acc[i][j], 0, 0, 0);
         }
     }
   };
-  const int nk = L.K / BK;  // >= 1
+  const int nk = L.K / BK;  // >= 2, even
   fetch(f0, 0);
   fetch(f1, BK);
   __syncthreads();  // the gain vector
@@ -693,41 +732,79 @@ __global__ __launch_bounds__(256, 2) void gemm_mfma_big_kernel(Linear L, int gr)
   // step kt: request step kt + 2, run step kt's MFMAs, stage step kt + 1 (fetched a
   // step earlier) into the other LDS stage
   // (nk is even: two steps per iteration, each register set and LDS stage in a fixed
-  // place)
+  // place).  The requests are unconditional (past the end they re-read the last step,
+  // unused): a request under a branch makes the compiler wait for every load at the
+  // join, the current step's request included, which leaves one step of prefetch.
+  const int klast = (nk - 1) * BK;
   for (int kt = 0; kt < nk; kt += 2) {
-    if (kt + 2 < nk) fetch(f0, (kt + 2) * BK);
+    fetch(f0, min((kt + 2) * BK, klast));
     mfmas(0);
     stage(f1, (kt + 1) * BK, 1);
     __syncthreads();
-    if (kt + 3 < nk) fetch(f1, (kt + 3) * BK);
+    fetch(f1, min((kt + 3) * BK, klast));
     mfmas(1);
     if (kt + 2 < nk) stage(f0, (kt + 2) * BK, 0);
     __syncthreads();
   }
-  const bool pair = L.epi.kind == EPI_SWIGLU || L.epi.kind == EPI_QKV;
-  // the two threads of a staged row hold its sum of squares over K
-  ss += xor_lane<1>(ss);
-  if (NORM && (tid & 1) == 0) rs[lr] = 1.0f / sqrtf(ss / (float)L.K + L.eps);
+  // the eight threads of a staged row hold its sum of squares over K
+  if (NORM) {
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      float t = ss[v];
+      t += xor_lane<1>(t);
+      t += xor_lane<2>(t);
+      t += xor_lane<4>(t);
+      if ((tid & 7) == 0) rs[ar + AR * v] = 1.0f / sqrtf(t / (float)L.K + L.eps);
+    }
+  }
   __syncthreads();
   const int jj = lane & 31;
-  auto out_block = [&](const f32x16& c, int i, int j) {
-    const int n = n0 + wn * 64 + j * 32 + jj;
+  // The epilogue branches on its kind once per block.  Every accumulator block is
+  // named by constant indices, inline (a loop the compiler leaves rolled, or an
+  // out-of-line call, would move acc to scratch memory).  Row of element r of block i:
+  auto row_of = [&](int i, int r) { return wm * 32 * TI + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); };
+  auto each = [&](auto&& f) __attribute__((always_inline)) {
+    static_for<TI * TJ>([&](auto ij) __attribute__((always_inline)) {
+      constexpr int i = decltype(ij)::value / TJ, j = decltype(ij)::value % TJ;
+      const int n = n0 + wn * 32 * TJ + j * 32 + jj;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int ml = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int m = m0 + ml;
-      const float val = NORM ? c[r] * rs[ml] : c[r];
-      const float partner = xor_lane<1>(val);  // column n + 1, same row (used by even columns)
-      if (m < L.M) {
-        if (!pair) epi_single(L.epi, m, n, val);
-        else if ((jj & 1) == 0) epi_pair(L.epi, m, n, val, partner);
+      for (int r = 0; r < 16; ++r) {
+        const int ml = row_of(i, r);
+        f(m0 + ml, n, NORM ? acc[i][j][r] * rs[ml] : acc[i][j][r]);
       }
-    }
+    });
   };
-  out_block(acc[0][0], 0, 0);
-  out_block(acc[0][1], 0, 1);
-  out_block(acc[1][0], 1, 0);
-  out_block(acc[1][1], 1, 1);
+  // pairs: lane value of block j and of block j + TJ / 2 are columns (n, n + 1)
+  auto each_pair = [&](auto&& f) __attribute__((always_inline)) {
+    constexpr int TH = TJ / 2;
+    static_for<TI * TH>([&](auto ij) __attribute__((always_inline)) {
+      constexpr int i = decltype(ij)::value / TH, j = decltype(ij)::value % TH;
+      const int n = n0 + wn * 32 * TJ + 2 * (j * 32 + jj);  // the pair's even column
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int ml = row_of(i, r);
+        const float sc = NORM ? rs[ml] : 1.0f;
+        f(m0 + ml, n, acc[i][j][r] * sc, acc[i][j + TH][r] * sc);
+      }
+    });
+  };
+  if (L.epi.kind == EPI_SWIGLU) {
+    each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
+      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + (n >> 1)] = silu(a0) * a1;
+    });
+  } else if (L.epi.kind == EPI_QKV) {
+    each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
+      if (m < L.M) epi_pair(L.epi, m, n, a0, a1);
+    });
+  } else if (L.epi.kind == EPI_STORE) {
+    each([&](int m, int n, float v) __attribute__((always_inline)) {
+      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + n] = v;
+    });
+  } else if (L.epi.kind == EPI_RESID) {
+    each([&](int m, int n, float v) __attribute__((always_inline)) {
+      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + n] += v;
+    });
+  }
 }
 
 // ------------------------------------------------------------- attention ------
@@ -1978,17 +2055,31 @@ hipError_t rows_launch(const Linear& L, hipStream_t st, const Ev& ev) {
   return ns == 4 ? rows_launch_t<2, 4>(L, st, ev) : ns == 2 ? rows_launch_t<2, 2>(L, st, ev) : rows_launch_t<2, 1>(L, st, ev);
 }
 
+template <int WM, int WN, int TI, int TJ>
+hipError_t big_launch_t(BigTile<WM, WN, TI, TJ>, const Linear& L, hipStream_t st, const Ev& ev) {
+  using T = BigTile<WM, WN, TI, TJ>;
+  // row blocks per L2 group: about 2 MiB of float32 X rows
+  const int gr = std::max(1, std::min(8, (int)((2 << 20) / ((int64_t)T::BM * L.K * 4))));
+  const dim3 grid(L.N / T::BN, (L.M + T::BM - 1) / T::BM);
+  if (L.gain != nullptr)
+    return klaunch(gemm_mfma_big_kernel<WM, WN, TI, TJ, true>, grid, dim3(T::threads), 0, st, ev.start, ev.stop, L, gr);
+  return klaunch(gemm_mfma_big_kernel<WM, WN, TI, TJ, false>, grid, dim3(T::threads), 0, st, ev.start, ev.stop, L, gr);
+}
+
+template <typename T>
+hipError_t big_launch(const Linear& L, hipStream_t st, const Ev& ev) {
+  return big_launch_t(T{}, L, st, ev);
+}
+
 template <typename W>
 hipError_t linear_t(const Linear& L, float* inv_rms, hipStream_t st, const Ev& ev) {
-  // large M: the 128x128 tile, once its grid fills every compute unit twice
-  if (mfma_fits<W>(L) && L.N % kBigBN == 0 && L.K % (2 * kBigBK) == 0 && L.gain2 == nullptr &&
-      (L.gain == nullptr || L.K <= kBigMaxGainK) &&
-      (int64_t)(L.N / kBigBN) * ((L.M + kBigBM - 1) / kBigBM) >= 256) {
-    // row blocks per L2 group: about 2 MiB of float32 X rows
-    const int gr = std::max(1, std::min(8, (int)((2 << 20) / ((int64_t)kBigBM * L.K * 4))));
-    const dim3 grid(L.N / kBigBN, (L.M + kBigBM - 1) / kBigBM);
-    if (L.gain != nullptr) return klaunch(gemm_mfma_big_kernel<true>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
-    return klaunch(gemm_mfma_big_kernel<false>, grid, dim3(256), 0, st, ev.start, ev.stop, L, gr);
+  // large M: the 256x256 tile once its grid fills every compute unit twice, else the
+  // 128x128 tile once its grid fills every compute unit
+  if (mfma_fits<W>(L) && L.K % (2 * kBigBK) == 0 && L.gain2 == nullptr && (L.gain == nullptr || L.K <= kBigMaxGainK)) {
+    if (L.N % BigTile256::BN == 0 && (int64_t)(L.N / BigTile256::BN) * ((L.M + BigTile256::BM - 1) / BigTile256::BM) >= 512)
+      return big_launch<BigTile256>(L, st, ev);
+    if (L.N % BigTile128::BN == 0 && (int64_t)(L.N / BigTile128::BN) * ((L.M + BigTile128::BM - 1) / BigTile128::BM) >= 256)
+      return big_launch<BigTile128>(L, st, ev);
   }
   if (rows_fits<W>(L)) return rows_launch(L, st, ev);
   if (mfma_fits<W>(L)) {
