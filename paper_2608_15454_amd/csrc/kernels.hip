@@ -291,19 +291,18 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   const bool norm = L.gain != nullptr;
   const float* ag = norm ? row_gain(L, aok ? am : 0) : nullptr;
   const uint16_t* brow = mat_row<uint16_t>(L.mats, n0 + lr, L.K);
-  float a[16];
+  // Loads are unconditional (rows past M read row 0 and are zeroed when staged) and
+  // only move data: a load under a branch, or arithmetic on its result in the same
+  // step, makes the compiler wait for it at once instead of during the MFMAs.
+  float4 a[4], g[4];
   float ss = 0.f;  // sum of squares of this thread's staged elements (norm)
   uint4 b0, b1;
+  const uint32_t keep = aok ? 0xffffffffu : 0u;
   auto fetch = [&](int k0) {
 #pragma unroll
-    for (int v = 0; v < 16; v += 4) {
-      float4 t = aok ? *reinterpret_cast<const float4*>(arow + k0 + lk + v) : make_float4(0.f, 0.f, 0.f, 0.f);
-      if (norm && aok) {
-        ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
-        const float4 g = *reinterpret_cast<const float4*>(ag + k0 + lk + v);
-        t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
-      }
-      a[v] = t.x; a[v + 1] = t.y; a[v + 2] = t.z; a[v + 3] = t.w;
+    for (int v = 0; v < 4; ++v) {
+      a[v] = *reinterpret_cast<const float4*>(arow + k0 + lk + 4 * v);
+      if (norm) g[v] = *reinterpret_cast<const float4*>(ag + k0 + lk + 4 * v);
     }
     b0 = *reinterpret_cast<const uint4*>(brow + k0 + lk);
     b1 = *reinterpret_cast<const uint4*>(brow + k0 + lk + 8);
@@ -311,7 +310,19 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   auto stage = [&](int buf) {
     uint32_t p[8], q[8];
 #pragma unroll
-    for (int v = 0; v < 8; ++v) bf16_hi_lo2(a[2 * v], a[2 * v + 1], p[v], q[v]);
+    for (int v = 0; v < 4; ++v) {
+      float4 t;
+      t.x = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[v].x) & keep);
+      t.y = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[v].y) & keep);
+      t.z = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[v].z) & keep);
+      t.w = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, a[v].w) & keep);
+      if (norm) {
+        ss += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+        t.x *= g[v].x; t.y *= g[v].y; t.z *= g[v].z; t.w *= g[v].w;
+      }
+      bf16_hi_lo2(t.x, t.y, p[2 * v], q[2 * v]);
+      bf16_hi_lo2(t.z, t.w, p[2 * v + 1], q[2 * v + 1]);
+    }
     uint4* ad = reinterpret_cast<uint4*>(&As[buf][lr * LD + lk]);
     ad[0] = make_uint4(p[0], p[1], p[2], p[3]);
     ad[1] = make_uint4(p[4], p[5], p[6], p[7]);
@@ -333,7 +344,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(Linear L, int ksplit) {
   __syncthreads();
   for (int kt = kt0; kt < kt1; ++kt) {
     const int cur = 0;
-    if (kt + 1 < kt1) fetch((kt + 1) * BK);  // in flight during this step's MFMAs
+    fetch(min(kt + 1, kt1 - 1) * BK);  // in flight during this step's MFMAs (the last step re-reads itself)
     const int aoff = (wm * 32 + (lane & 31)) * LD + (lane >> 5) * 8;
     const uint16_t* ab = &As[cur][aoff];
     const uint16_t* alo = &Al[cur][aoff];
@@ -1140,20 +1151,26 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
   float m_run = -INFINITY, l_run = 0.f;
   for (int k0 = k_begin; k0 < kvmax; k0 += 64) {
     __syncthreads();  // the previous block's K and V are consumed
+    // every load first, unconditionally (a load under a branch is waited for at once):
+    // keys past kvmax read the last visible row, a written cache entry, and are masked
+    // out of the softmax (probability 0 times a finite value)
+    const int32_t gl = gt != nullptr ? gt[min(k0 + (tid & 63), kvmax - 1)] : 0;
+    uint4 kv4[4], vv4[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7, j = k0 + c;
-      uint4 kv4 = make_uint4(0, 0, 0, 0), vv4 = make_uint4(0, 0, 0, 0);
-      if (j < kvmax) {
-        kv4 = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH + part * 8);
-        vv4 = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH + part * 8);
-      }
-      *reinterpret_cast<uint4*>(&Ks[c * LD + part * 8]) = kv4;
-      const _Float16* ve = reinterpret_cast<const _Float16*>(&vv4);
+      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7, j = min(k0 + c, kvmax - 1);
+      kv4[i] = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH + part * 8);
+      vv4[i] = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH + part * 8);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7;
+      *reinterpret_cast<uint4*>(&Ks[c * LD + part * 8]) = kv4[i];
+      const _Float16* ve = reinterpret_cast<const _Float16*>(&vv4[i]);
 #pragma unroll
       for (int e = 0; e < 8; ++e) Vt[(part * 8 + e) * LD + c] = ve[e];
     }
-    if (tid < 64) Gs[tid] = (gt != nullptr && k0 + tid < kvmax) ? gt[k0 + tid] : 0;
+    if (tid < 64) Gs[tid] = k0 + tid < kvmax ? gl : 0;
     __syncthreads();
     // S^T blocks: keys 32 cb + (row of the accumulator), this lane's query
     f32x16 s[2];
