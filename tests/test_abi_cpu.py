@@ -138,3 +138,23 @@ def test_null_handle_calls(mbp):
     assert L.mbp_reset(None) == mbp.EINVAL
     assert L.mbp_row_length(None, 0) == mbp.EINVAL
     L.mbp_destroy(None)
+
+
+def test_kernels_use_no_scratch_memory(mbp):
+    """Every kernel keeps its working state in registers and LDS.  Scratch memory inside
+    a hot loop costs a multiple of the kernel's time: an accumulator array that the
+    compiler indexed at run time, and so placed in scratch, made the tiled GEMM three
+    times slower with no error.  The build records each kernel's resources from the
+    compiler's remarks.  Allowed: the d=2048 engine's multi-row and split variants,
+    which spill a few dwords at the 256-VGPR limit (the d=2048 verification workload
+    launches the engine twice per run; its decode steps run on the per-kernel path)."""
+    path = os.path.join(ROOT, "paper_2608_15454_amd", "_build", "kernel_resources.tsv")
+    assert os.path.exists(path), "rebuild: the build writes _build/kernel_resources.tsv"
+    rows = [line.rstrip("\n").split("\t") for line in open(path)][1:]
+    assert len(rows) > 50 and {r[0] for r in rows} >= {"kernels.hip", "engine.hip"}
+    bad = []
+    for src, name, _vgprs, _agprs, scratch, _occ, _lds in rows:
+        if int(scratch) == 0 or (src == "engine.hip" and "Li2048E" in name and int(scratch) <= 64):
+            continue
+        bad.append((src, name, int(scratch)))
+    assert not bad, bad
