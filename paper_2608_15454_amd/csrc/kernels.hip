@@ -1075,8 +1075,10 @@ __global__ __launch_bounds__(256) void attn_prefill_kernel(Attn a, const int32_t
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
 // The same attention on the matrix cores, for float16 caches and head size 64: a
-// block of two waves takes a tile of up to 64 query rows (32 per wave) and walks the
-// visible keys in blocks of 64.  Everything is computed transposed, S^T = K Q^T and
+// block takes a tile of up to 64 query rows (32 per wave of a two-wave group) and walks
+// the visible keys in blocks of 64; with KG groups, group g takes key blocks g, g + KG,
+// ... of the tile and the groups' softmax states merge at the end (a tile's key chain is
+// what bounds a grid of few tiles, such as one long sequence's causal layers).  Everything is computed transposed, S^T = K Q^T and
 // O^T += V^T P^T (32x32x16 float16 MFMAs, float32 accumulation), so that each lane
 // owns one query: lane l holds query l % 32 and, in its accumulator registers, the
 // keys 8 (r / 4) + 4 (l / 32) + r % 4 of each 32-key block.  The softmax's max and sum
@@ -1089,7 +1091,10 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // MFMA operand layout: lane l supplies row / column l % 32 and the 8 k positions
 // 8 (l / 32) .. +7 of each 16-wide k step.  Three waves per SIMD: 147 VGPRs, no
 // spills, six blocks in the LDS (a budget for four spills).
-__global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
+constexpr int kPrefillSplitBelow = 3072;  // blocks of the one-group grid
+
+template <int KG>
+__global__ __launch_bounds__(128 * KG, 3) void attn_prefill_mfma_kernel(Attn a, const int32_t* tiles) {
   constexpr int DH = 64, LD = DH + 8;
   // XCD-aware order (workgroups go to the 8 XCDs round-robin by linear id): with a
   // multiple of 8 heads, XCD k takes heads k, k+8, ..., so it reads only their keys and
@@ -1100,13 +1105,19 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
     h = (bid & 7) + 8 * (l / gridDim.x);
     tile = l % gridDim.x;
   }
+  // KG groups of two waves split the tile's key blocks (group g takes blocks g, g + KG,
+  // ...) and merge their softmax states at the end; wave qw of a group holds the tile's
+  // queries 32 qw .. +31
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int grp = wave >> 1, qw = wave & 1, gtid = tid & 127;
   const int t0 = tiles[2 * tile], cnt = tiles[2 * tile + 1];
   const int b = a.tok.b[t0], slot0 = a.tok.slot[t0];
   const int kvmax = slot0 + cnt;
-  __shared__ __attribute__((aligned(16))) _Float16 Ks[64 * LD];
-  __shared__ __attribute__((aligned(16))) _Float16 Vt[DH * LD];
-  __shared__ int32_t Gs[64];
+  __shared__ __attribute__((aligned(16))) _Float16 kvs[KG][2][64 * LD];
+  __shared__ int32_t Gsa[KG][64];
+  _Float16* Ks = kvs[grp][0];
+  _Float16* Vt = kvs[grp][1];
+  int32_t* Gs = Gsa[grp];
   const int32_t* gt = a.grp_tab != nullptr ? a.grp_tab + (size_t)b * a.cap : nullptr;
   int k_begin = 0;
   if (gt != nullptr) {
@@ -1121,7 +1132,7 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
   }
   const int col = lane & 31, half = lane >> 5;
   // this lane's query: row qi of the tile (padding rows repeat row 0 and are not stored)
-  const int qi = wave * 32 + col;
+  const int qi = qw * 32 + col;
   const int qrow = t0 + (qi < cnt ? qi : 0);
   const int islot = slot0 + qi;
   const int gq = gt != nullptr ? a.tok.grp[qrow] : 0;
@@ -1149,29 +1160,54 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
     o1[r] = 0.f;
   }
   float m_run = -INFINITY, l_run = 0.f;
-  for (int k0 = k_begin; k0 < kvmax; k0 += 64) {
+  const int nkb = (kvmax - k_begin + 63) / 64;  // >= 1
+  for (int it = 0; it < (nkb + KG - 1) / KG; ++it) {
+    // every group stages a block in every round (past its last one, a valid block it
+    // does not use), so that all waves meet at the same barriers
+    const int kbi = it * KG + grp;
+    const int k0 = k_begin + 64 * min(kbi, nkb - 1);
     __syncthreads();  // the previous block's K and V are consumed
     // every load first, unconditionally (a load under a branch is waited for at once):
     // keys past kvmax read the last visible row, a written cache entry, and are masked
     // out of the softmax (probability 0 times a finite value)
-    const int32_t gl = gt != nullptr ? gt[min(k0 + (tid & 63), kvmax - 1)] : 0;
+    const int32_t gl = gt != nullptr ? gt[min(k0 + (gtid & 63), kvmax - 1)] : 0;
+    // keys: eight lanes per 128-byte row (item i: key idx / 8, dims 8 (idx % 8) ..);
+    // values: a lane takes keys 2q, 2q + 1 of one 8-dim part p (q fastest across lanes),
+    // so that each transposed write is one 4-byte word holding both keys' values of a
+    // dim, and the 32 lanes of a part write 32 different banks
     uint4 kv4[4], vv4[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7, j = min(k0 + c, kvmax - 1);
+      const int idx = gtid + 128 * i, c = idx >> 3, part = idx & 7, j = min(k0 + c, kvmax - 1);
       kv4[i] = *reinterpret_cast<const uint4*>(kb + (size_t)j * DH + part * 8);
-      vv4[i] = *reinterpret_cast<const uint4*>(vb + (size_t)j * DH + part * 8);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int iu = gtid + 128 * u, q = iu & 31, pp = iu >> 5;
+      vv4[2 * u] = *reinterpret_cast<const uint4*>(vb + (size_t)min(k0 + 2 * q, kvmax - 1) * DH + pp * 8);
+      vv4[2 * u + 1] = *reinterpret_cast<const uint4*>(vb + (size_t)min(k0 + 2 * q + 1, kvmax - 1) * DH + pp * 8);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int idx = tid + 128 * i, c = idx >> 3, part = idx & 7;
+      const int idx = gtid + 128 * i, c = idx >> 3, part = idx & 7;
       *reinterpret_cast<uint4*>(&Ks[c * LD + part * 8]) = kv4[i];
-      const _Float16* ve = reinterpret_cast<const _Float16*>(&vv4[i]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[(part * 8 + e) * LD + c] = ve[e];
     }
-    if (tid < 64) Gs[tid] = k0 + tid < kvmax ? gl : 0;
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int iu = gtid + 128 * u, q = iu & 31, pp = iu >> 5;
+      const uint32_t* va = reinterpret_cast<const uint32_t*>(&vv4[2 * u]);
+      const uint32_t* vb2 = reinterpret_cast<const uint32_t*>(&vv4[2 * u + 1]);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        // dim 8 pp + e: key 2q's value in the low half, key 2q + 1's in the high half
+        const uint32_t w = (e & 1) ? ((va[e >> 1] >> 16) | (vb2[e >> 1] & 0xffff0000u))
+                                   : ((va[e >> 1] & 0xffffu) | (vb2[e >> 1] << 16));
+        *reinterpret_cast<uint32_t*>(&Vt[(pp * 8 + e) * LD + 2 * q]) = w;
+      }
+    }
+    if (gtid < 64) Gs[gtid] = k0 + gtid < kvmax ? gl : 0;
     __syncthreads();
+    if (kbi >= nkb) continue;
     // S^T blocks: keys 32 cb + (row of the accumulator), this lane's query
     f32x16 s[2];
 #pragma unroll
@@ -1247,6 +1283,40 @@ __global__ __launch_bounds__(128, 3) void attn_prefill_mfma_kernel(Attn a, const
         o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v1, ph, o1, 0, 0, 0);
         o1 = __builtin_amdgcn_mfma_f32_32x32x16_f16(v1, pl, o1, 0, 0, 0);
       }
+  }
+  if constexpr (KG > 1) {
+    // merge: groups 1.. leave (max, sum, unnormalized output) per lane in the LDS that
+    // held their K/V tiles ([KG - 1][2 waves][34][64] floats, lane fastest); group 0
+    // folds them into its own state
+    __syncthreads();
+    float* mbuf = reinterpret_cast<float*>(&kvs[0][0][0]);
+    if (grp > 0) {
+      float* w = mbuf + (size_t)((grp - 1) * 2 + qw) * 34 * 64 + lane;
+      w[0] = m_run;
+      w[64] = l_run;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        w[(2 + r) * 64] = o0[r];
+        w[(18 + r) * 64] = o1[r];
+      }
+    }
+    __syncthreads();
+    if (grp > 0) return;
+#pragma unroll
+    for (int g = 1; g < KG; ++g) {
+      const float* w = mbuf + (size_t)((g - 1) * 2 + qw) * 34 * 64 + lane;
+      const float mg = w[0];
+      if (mg == -INFINITY) continue;  // no visible key in that group's blocks
+      const float mn = fmaxf(m_run, mg);
+      const float a0 = (m_run == -INFINITY) ? 0.f : expf(m_run - mn), a1 = expf(mg - mn);
+      l_run = l_run * a0 + w[64] * a1;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        o0[r] = o0[r] * a0 + w[(2 + r) * 64] * a1;
+        o1[r] = o1[r] * a0 + w[(18 + r) * 64] * a1;
+      }
+      m_run = mn;
+    }
   }
   if (qi < cnt) {
     float* op = a.O + (size_t)(t0 + qi) * a.ldo + h * DH;
@@ -2194,7 +2264,14 @@ template <typename KV>
 hipError_t attn_prefill_t(const Attn& a, const int32_t* tiles, int ntiles, hipStream_t st, const Ev& ev) {
   const dim3 grid(ntiles, a.H);
   if constexpr (std::is_same<KV, _Float16>::value)
-    if (a.dh == 64) return klaunch(attn_prefill_mfma_kernel, grid, dim3(128), 0, st, ev.start, ev.stop, a, tiles);
+    if (a.dh == 64) {
+      // a grid that fills the compute units a few times over runs each tile's keys in one
+      // group; a smaller one (one long sequence) splits them over two groups, since its
+      // last tiles' key chains would otherwise set the kernel's time
+      if ((int64_t)ntiles * a.H < kPrefillSplitBelow)
+        return klaunch(attn_prefill_mfma_kernel<2>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
+      return klaunch(attn_prefill_mfma_kernel<1>, grid, dim3(128), 0, st, ev.start, ev.stop, a, tiles);
+    }
   if (a.dh == 64) return klaunch(attn_prefill_kernel<KV, 64>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
   return klaunch(attn_prefill_kernel<KV, 32>, grid, dim3(256), 0, st, ev.start, ev.stop, a, tiles);
 }

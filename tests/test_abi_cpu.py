@@ -145,9 +145,14 @@ def test_kernels_use_no_scratch_memory(mbp):
     a hot loop costs a multiple of the kernel's time: an accumulator array that the
     compiler indexed at run time, and so placed in scratch, made the tiled GEMM three
     times slower with no error.  The build records each kernel's resources from the
-    compiler's remarks.  Allowed: the d=2048 engine's multi-row and split variants,
-    which spill a few dwords at the 256-VGPR limit (the d=2048 verification workload
-    launches the engine twice per run; its decode steps run on the per-kernel path)."""
+    compiler's remarks.  Allowed, each measured:
+    - the d=2048 engine's multi-row and split variants, which spill a few dwords at the
+      256-VGPR limit (the d=2048 verification workload launches the engine twice per
+      run; its decode steps run on the per-kernel path);
+    - the MFMA prefill attention, two dwords over the 168 VGPRs of three waves per SIMD.
+      At two waves per SIMD it needs no scratch but ran slower: the forward's attention
+      took 36.6 against 31.9 ms over 20 forwards, the batch-64 prefill's 19.5 against
+      16.1 ms."""
     path = os.path.join(ROOT, "paper_2608_15454_amd", "_build", "kernel_resources.tsv")
     assert os.path.exists(path), "rebuild: the build writes _build/kernel_resources.tsv"
     rows = [line.rstrip("\n").split("\t") for line in open(path)][1:]
@@ -155,6 +160,8 @@ def test_kernels_use_no_scratch_memory(mbp):
     bad = []
     for src, name, _vgprs, _agprs, scratch, _occ, _lds in rows:
         if int(scratch) == 0 or (src == "engine.hip" and "Li2048E" in name and int(scratch) <= 64):
+            continue
+        if src == "kernels.hip" and "attn_prefill_mfma_kernel" in name and int(scratch) <= 8:
             continue
         bad.append((src, name, int(scratch)))
     assert not bad, bad
