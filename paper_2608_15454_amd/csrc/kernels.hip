@@ -2,11 +2,16 @@
 //
 // Numerics: weights are stored in the model dtype (float32 or bfloat16), KV caches
 // in float32, bfloat16 or float16; every activation, residual stream, norm, softmax
-// and accumulation is float32.  Linear layers are weight-streaming GEMV kernels for
-// up to 64 rows (each weight byte is read from HBM once per launch with 16-byte
-// loads, issued before the activations are even loaded) and an LDS-tiled kernel for
-// more rows.  Decode attention splits the keys over blocks of four waves; the last
-// block of each (query, head) merges the splits.
+// and accumulation is float32 (on the matrix cores, activations enter as bfloat16 or
+// float16 hi + lo pairs).  Linear layers:
+// - weight-streaming GEMV kernels for up to 16 rows of bfloat16 weights (64 of
+//   float32): each weight byte is read from HBM once per launch with 16-byte loads,
+//   issued before the activations are loaded;
+// - for more rows of bfloat16 weights, the row GEMM (17..64 rows) and MFMA tiles of
+//   64 x 64 (split-K), 128 x 128 and 256 x 256.
+// Decode attention splits the keys over blocks and merges the splits in a second
+// kernel; several rows of one sequence share each K/V tile (the multi-query kernel).
+// Prefill and the full-sequence forward use MFMA attention over 64-query tiles.
 #include <hip/hip_ext.h>
 
 #include <math.h>
