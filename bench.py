@@ -66,8 +66,8 @@ def cpu_threads():
 # readings scale the HBM counters of the kernels that follow.
 COPY_CAL_BYTES = 256 << 20
 # HBM traffic per launch of the dominant kernel class, from counter runs of this
-# command (profiles/<class>_<workload>_hbm_counters.md), valid only while the source
-# the class is built from is the one that was measured.
+# command (profiles/<class>_<workload>_hbm_counters.md), valid only while the code of
+# the source the class is built from is the code that was measured.
 CSRC = os.path.join(ROOT, "paper_2608_15454_amd", "csrc")
 CLASS_SOURCE = {"engine": "engine.hip", "gemv": "kernels.hip", "gemm": "kernels.hip", "attention": "kernels.hip",
                 "other": "kernels.hip"}
@@ -79,11 +79,22 @@ def traffic_key(workload, logit_gain=1.0):
     return workload if logit_gain == 1.0 else f"{workload}_gain{logit_gain:g}"
 
 
+def code_digest(path):
+    """sha256 of a C++ / HIP source with its comments removed and its whitespace
+    collapsed: edits to comments or layout leave it, and so a counter record, valid."""
+    import hashlib
+    import re
+
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    src = re.sub(r"\s+", " ", src).strip()
+    return hashlib.sha256(src.encode()).hexdigest()
+
+
 def measured_traffic(kernel_class, workload):
     """Bytes per launch recorded for kernel_class on workload, or None when there is no
-    record or the class's source has changed since the counters were taken."""
-    import hashlib
-
+    record or the code of the class's source has changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", f"{kernel_class}_{workload}_hbm_counters.md")
     source = CLASS_SOURCE.get(kernel_class)
     if source is None or not os.path.exists(path):
@@ -93,9 +104,8 @@ def measured_traffic(kernel_class, workload):
         if line.startswith("- ") and ": " in line:
             k, v = line[2:].split(": ", 1)
             fields[k.strip()] = v.strip().strip("`")
-    digest = hashlib.sha256(open(os.path.join(CSRC, source), "rb").read()).hexdigest()
-    if fields.get(f"{source} sha256") != digest or fields.get("class") != kernel_class \
-            or fields.get("workload") != workload:
+    if fields.get(f"{source} code sha256") != code_digest(os.path.join(CSRC, source)) \
+            or fields.get("class") != kernel_class or fields.get("workload") != workload:
         return None
     return int(fields["hbm bytes per launch"])
 

@@ -1083,10 +1083,11 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // block takes a tile of up to 64 query rows (32 per wave of a two-wave group) and walks
 // the visible keys in blocks of 64; with KG groups, group g takes key blocks g, g + KG,
 // ... of the tile and the groups' softmax states merge at the end (a tile's key chain is
-// what bounds a grid of few tiles, such as one long sequence's causal layers).  Everything is computed transposed, S^T = K Q^T and
-// O^T += V^T P^T (32x32x16 float16 MFMAs, float32 accumulation), so that each lane
-// owns one query: lane l holds query l % 32 and, in its accumulator registers, the
-// keys 8 (r / 4) + 4 (l / 32) + r % 4 of each 32-key block.  The softmax's max and sum
+// what bounds a grid of few tiles, such as one long sequence's causal layers).
+// Everything is computed transposed, S^T = K Q^T and O^T += V^T P^T (32x32x16 float16
+// MFMAs, float32 accumulation), so that each lane owns one query: lane l holds query
+// l % 32 and, in its accumulator registers, the keys 8 (r / 4) + 4 (l / 32) + r % 4 of
+// each 32-key block.  The softmax's max and sum
 // over a query's keys are then in-lane plus one exchange between the wave's halves,
 // and P^T feeds the second product straight from the registers: a contraction may
 // take its k positions in any order, so V^T is read in the key order the registers
@@ -1094,8 +1095,8 @@ typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 // two MFMAs each), so their rounding stays near float32; K and V are the cache's own
 // float16 values, staged in LDS as [key][dim] and [dim][key].
 // MFMA operand layout: lane l supplies row / column l % 32 and the 8 k positions
-// 8 (l / 32) .. +7 of each 16-wide k step.  Three waves per SIMD: 147 VGPRs, no
-// spills, six blocks in the LDS (a budget for four spills).
+// 8 (l / 32) .. +7 of each 16-wide k step.  Three waves per SIMD: 168 VGPRs and 8 bytes
+// of scratch (two waves per SIMD need no scratch and measure slower).
 constexpr int kPrefillSplitBelow = 3072;  // blocks of the one-group grid
 
 template <int KG>

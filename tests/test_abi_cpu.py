@@ -165,3 +165,27 @@ def test_kernels_use_no_scratch_memory(mbp):
             continue
         bad.append((src, name, int(scratch)))
     assert not bad, bad
+
+
+def test_counter_records_follow_code_not_comments(tmp_path):
+    """A counter record stays valid across edits to comments and layout, and only
+    those: bench.py compares a digest of the source's code."""
+    import bench
+
+    base = "int f(int a) {\n  return a + 1;  // one more\n}\n/* note */\n"
+    cases = {
+        "comment": "int f(int a) {\n  return a + 1;  // one more than a\n}\n/* another note */\n",
+        "layout": "int f(int a)\n{\n    return a + 1;\n}\n",
+        "code": "int f(int a) {\n  return a + 2;  // one more\n}\n/* note */\n",
+    }
+    p0 = tmp_path / "base.hip"
+    p0.write_text(base)
+    d0 = bench.code_digest(str(p0))
+    for name, text in cases.items():
+        p = tmp_path / f"{name}.hip"
+        p.write_text(text)
+        assert (bench.code_digest(str(p)) == d0) == (name != "code"), name
+    # every record in profiles/ names a code digest
+    for rec in os.listdir(os.path.join(ROOT, "profiles")):
+        if rec.endswith("_hbm_counters.md"):
+            assert "code sha256: `" in open(os.path.join(ROOT, "profiles", rec)).read(), rec
