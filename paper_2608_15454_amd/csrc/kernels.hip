@@ -598,7 +598,9 @@ __global__ __launch_bounds__(512) void gemm_rows_kernel(Linear L) {
 // v_mfma_f32_32x32x16_bf16 (X in bfloat16 hi + lo as above), K in steps of 32.  Two
 // LDS stages and two register stages: the X and weight rows of step k+2 are requested
 // while step k's MFMAs run and step k+1 is staged, so each fetch has two steps to
-// arrive (the steps are latency-bound otherwise); one barrier per step.  Every thread
+// arrive (the steps are latency-bound otherwise); one barrier per step.  The 256 x 256
+// tile stages step k+1 before step k's MFMAs in program order, the 128 x 128 tile after
+// them (each order measured faster on its tile).  Every thread
 // stages four 4-wide pieces of X rows and two 8-wide pieces of weight rows per step
 // (BM = BN = threads / 2).
 // Two shapes: 128 x 128 (four waves of 64 x 64, two blocks per CU) and 256 x 256 (eight
@@ -643,17 +645,15 @@ __global__ __launch_bounds__(64 * WM * WN, 2) void gemm_mfma_big_kernel(Linear L
   // loads in row order: eight lanes read the 128 bytes of one X row's step (rows
   // t / 8 + NT / 8 * v), four lanes the 64 bytes of one weight row's step (rows
   // t / 4 + NT / 4 * u), so each load instruction covers whole lines of few rows.  Rows
-  // past M load row 0 of X and are zeroed before staging.
+  // past M load row 0 of X: their results are finite and never stored (an output row
+  // depends only on its own X row, and so does its sum of squares).
   constexpr int AR = NT / 8, BR = NT / 4;
   const int ar = tid >> 3, ak = (tid & 7) * 4, br = tid >> 2, bk = (tid & 3) * 8;
   const float* arow[4];
-  unsigned aok = 0;
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const int m = m0 + ar + AR * v;
-    const bool ok = m < L.M;
-    aok |= (ok ? 1u : 0u) << v;
-    arow[v] = L.X + (size_t)(ok ? (L.xidx ? L.xidx[m] : m) : 0) * L.ldx + ak;
+    arow[v] = L.X + (size_t)(m < L.M ? (L.xidx ? L.xidx[m] : m) : 0) * L.ldx + ak;
   }
   if (NORM)
     for (int k = tid * 4; k < L.K; k += NT * 4) *reinterpret_cast<float4*>(&gs[k]) = *reinterpret_cast<const float4*>(L.gain + k);
@@ -683,20 +683,15 @@ __global__ __launch_bounds__(64 * WM * WN, 2) void gemm_mfma_big_kernel(Linear L
     f.b0 = *reinterpret_cast<const uint4*>(brow0 + k0);
     f.b1 = *reinterpret_cast<const uint4*>(brow1 + k0);
   };
-  auto stage = [&](const Fetch& f, int k0, int buf) {
+  // w = 1 adds the step to the sums of squares, w = 0 (a restaged last step) does not
+  auto stage = [&](const Fetch& f, int k0, int buf, float w) {
     float4 g;
     if (NORM) g = *reinterpret_cast<const float4*>(&gs[k0 + ak]);
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      // rows past M: all bits cleared (a mask, not a branch, keeps the waits in order)
-      const uint32_t keep = 0u - ((aok >> v) & 1u);
-      float4 t;
-      t.x = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].x) & keep);
-      t.y = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].y) & keep);
-      t.z = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].z) & keep);
-      t.w = __builtin_bit_cast(float, __builtin_bit_cast(uint32_t, f.a[v].w) & keep);
+      float4 t = f.a[v];
       if (NORM) {
-        ss[v] += t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w;
+        ss[v] = fmaf(t.x * t.x + t.y * t.y + t.z * t.z + t.w * t.w, w, ss[v]);
         t.x *= g.x; t.y *= g.y; t.z *= g.z; t.w *= g.w;
       }
       uint32_t p0, p1, q0, q1;
@@ -743,23 +738,37 @@ __global__ __launch_bounds__(64 * WM * WN, 2) void gemm_mfma_big_kernel(Linear L
   fetch(f0, 0);
   fetch(f1, BK);
   __syncthreads();  // the gain vector
-  stage(f0, 0, 0);
+  stage(f0, 0, 0, 1.f);
   __syncthreads();
   // step kt: request step kt + 2, run step kt's MFMAs, stage step kt + 1 (fetched a
   // step earlier) into the other LDS stage
   // (nk is even: two steps per iteration, each register set and LDS stage in a fixed
-  // place).  The requests are unconditional (past the end they re-read the last step,
-  // unused): a request under a branch makes the compiler wait for every load at the
-  // join, the current step's request included, which leaves one step of prefetch.
+  // place).  The requests and the staging are unconditional (past the end the last step
+  // is re-read and restaged, unused): a load or a staging under a branch splits the
+  // loop body, and the compiler then waits for every load at the join (the current
+  // step's request included, which leaves one step of prefetch) and cannot interleave
+  // the staging with the MFMAs.
+  constexpr bool stage_first = WM * WN == 8;
   const int klast = (nk - 1) * BK;
   for (int kt = 0; kt < nk; kt += 2) {
     fetch(f0, min((kt + 2) * BK, klast));
-    mfmas(0);
-    stage(f1, (kt + 1) * BK, 1);
+    if constexpr (stage_first) {
+      stage(f1, (kt + 1) * BK, 1, 1.f);
+      mfmas(0);
+    } else {
+      mfmas(0);
+      stage(f1, (kt + 1) * BK, 1, 1.f);
+    }
     __syncthreads();
     fetch(f1, min((kt + 3) * BK, klast));
-    mfmas(1);
-    if (kt + 2 < nk) stage(f0, (kt + 2) * BK, 0);
+    const float w = kt + 2 < nk ? 1.f : 0.f;
+    if constexpr (stage_first) {
+      stage(f0, min((kt + 2) * BK, klast), 0, w);
+      mfmas(1);
+    } else {
+      mfmas(1);
+      stage(f0, min((kt + 2) * BK, klast), 0, w);
+    }
     __syncthreads();
   }
   // the eight threads of a staged row hold its sum of squares over K
