@@ -220,6 +220,11 @@ __device__ __forceinline__ float wave_sum(float v) { return group_sum<64>(v); }
 __device__ __forceinline__ float wave_max(float v) { return group_max<64>(v); }
 
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + expf(-x)); }
+// The same with the hardware exp2 and reciprocal (v_exp_f32 on -x log2 e, v_rcp_f32,
+// each within about 1 ulp): a few ulp from the division form for |x| up to about 20, the
+// exp2 argument's own rounding growing with |x|.  Used where silu is a measurable part
+// of a kernel's time (the SwiGLU epilogue of the large-tile GEMM).
+__device__ __forceinline__ float silu_fast(float x) { return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 template <typename W>
 __device__ __forceinline__ const W* mat_row(const Mats& mt, int n, int K) {

@@ -788,47 +788,74 @@ __global__ __launch_bounds__(64 * WM * WN, 2) void gemm_mfma_big_kernel(Linear L
   // named by constant indices, inline (a loop the compiler leaves rolled, or an
   // out-of-line call, would move acc to scratch memory).  Row of element r of block i:
   auto row_of = [&](int i, int r) { return wm * 32 * TI + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); };
+  // Rows outer, column blocks inner, so a row's scale and address are computed once.
   auto each = [&](auto&& f) __attribute__((always_inline)) {
-    static_for<TI * TJ>([&](auto ij) __attribute__((always_inline)) {
-      constexpr int i = decltype(ij)::value / TJ, j = decltype(ij)::value % TJ;
-      const int n = n0 + wn * 32 * TJ + j * 32 + jj;
+    static_for<TI>([&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ml = row_of(i, r);
-        f(m0 + ml, n, NORM ? acc[i][j][r] * rs[ml] : acc[i][j][r]);
+        const float sc = NORM ? rs[ml] : 1.0f;
+        static_for<TJ>([&](auto jc) __attribute__((always_inline)) {
+          constexpr int j = decltype(jc)::value;
+          f(m0 + ml, n0 + wn * 32 * TJ + j * 32 + jj, acc[i][j][r] * sc);
+        });
       }
     });
   };
   // pairs: lane value of block j and of block j + TJ / 2 are columns (n, n + 1)
   auto each_pair = [&](auto&& f) __attribute__((always_inline)) {
     constexpr int TH = TJ / 2;
-    static_for<TI * TH>([&](auto ij) __attribute__((always_inline)) {
-      constexpr int i = decltype(ij)::value / TH, j = decltype(ij)::value % TH;
-      const int n = n0 + wn * 32 * TJ + 2 * (j * 32 + jj);  // the pair's even column
+    static_for<TI>([&](auto ic) __attribute__((always_inline)) {
+      constexpr int i = decltype(ic)::value;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int ml = row_of(i, r);
         const float sc = NORM ? rs[ml] : 1.0f;
-        f(m0 + ml, n, acc[i][j][r] * sc, acc[i][j + TH][r] * sc);
+        static_for<TH>([&](auto jc) __attribute__((always_inline)) {
+          constexpr int j = decltype(jc)::value;
+          f(m0 + ml, n0 + wn * 32 * TJ + 2 * (j * 32 + jj), acc[i][j][r] * sc, acc[i][j + TH][r] * sc);
+        });
       }
     });
   };
+  // A tile with no row past M stores without a check per element (the check is a
+  // branch around each store).  The output pointer is held in registers (the compiler
+  // reloads kernel arguments after every store through a plain pointer).
+  float* const Y = L.epi.Y;
+  const size_t ldy = (size_t)L.epi.ldy;
+  const bool full = m0 + BM <= L.M;
   if (L.epi.kind == EPI_SWIGLU) {
-    each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
-      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + (n >> 1)] = silu(a0) * a1;
-    });
+    if (full)
+      each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
+        Y[(size_t)m * ldy + (n >> 1)] = silu_fast(a0) * a1;
+      });
+    else
+      each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
+        if (m < L.M) Y[(size_t)m * ldy + (n >> 1)] = silu_fast(a0) * a1;
+      });
   } else if (L.epi.kind == EPI_QKV) {
-    each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
-      if (m < L.M) epi_pair(L.epi, m, n, a0, a1);
-    });
+    const Epi e = L.epi;
+    if (full)
+      each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) { epi_pair(e, m, n, a0, a1); });
+    else
+      each_pair([&](int m, int n, float a0, float a1) __attribute__((always_inline)) {
+        if (m < L.M) epi_pair(e, m, n, a0, a1);
+      });
   } else if (L.epi.kind == EPI_STORE) {
-    each([&](int m, int n, float v) __attribute__((always_inline)) {
-      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + n] = v;
-    });
+    if (full)
+      each([&](int m, int n, float v) __attribute__((always_inline)) { Y[(size_t)m * ldy + n] = v; });
+    else
+      each([&](int m, int n, float v) __attribute__((always_inline)) {
+        if (m < L.M) Y[(size_t)m * ldy + n] = v;
+      });
   } else if (L.epi.kind == EPI_RESID) {
-    each([&](int m, int n, float v) __attribute__((always_inline)) {
-      if (m < L.M) L.epi.Y[(size_t)m * L.epi.ldy + n] += v;
-    });
+    if (full)
+      each([&](int m, int n, float v) __attribute__((always_inline)) { Y[(size_t)m * ldy + n] += v; });
+    else
+      each([&](int m, int n, float v) __attribute__((always_inline)) {
+        if (m < L.M) Y[(size_t)m * ldy + n] += v;
+      });
   }
 }
 
