@@ -75,7 +75,8 @@ typedef enum { MBP_ACCEPT_THRESHOLD = 0, MBP_ACCEPT_SELF_VERIFY = 1 } mbp_mode;
  *   max_window                MB window rows; 0 = 2*max_patch + max_n - 2 (needs
  *                             max_patch > 0).
  *   max_chunk                 tokens per internal pass of a long commit (0 = max_batch
- *                             x max_ctx, clamped to [4096, 32768]).
+ *                             x max_ctx, clamped to [4096, 131072]).  The workspace
+ *                             grows by about 32 d_model bytes per token of a pass.
  *   rope_base, rms_eps, attn_scale   1e5, 1e-6 and 1.0 in the paper.  Attention
  *                             scores are q.k / sqrt(d_head) * attn_scale.
  *   window_mode               0: the MB layers run on the window of Algorithm 1 only

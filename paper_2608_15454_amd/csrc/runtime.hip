@@ -190,10 +190,10 @@ Sizes sizes_of(const mbp_config& c) {
   s.Wcap = c.max_window > 0     ? c.max_window
            : c.window_mode == 1 ? c.max_ctx + c.max_n
                                 : std::max(2 * c.max_patch + c.max_n - 2, c.max_n);
-  // default pass: the whole batch's context up to 32768 rows (larger passes keep the
-  // matrix cores busier; the scratch grows by about 32 d bytes per row)
+  // default pass: the whole batch's context up to 131072 rows (larger passes keep the
+  // matrix cores busier; the scratch grows by about 32 d bytes per row, 4 GiB at d=1024)
   const int chunk = c.max_chunk > 0 ? c.max_chunk
-                                    : (int)std::min<int64_t>(32768, std::max<int64_t>(4096, (int64_t)c.max_batch * c.max_ctx));
+                                    : (int)std::min<int64_t>(131072, std::max<int64_t>(4096, (int64_t)c.max_batch * c.max_ctx));
   s.Mc = std::max({chunk, s.B * s.nmax, s.B * s.Wcap});
   s.Ml = s.Mc + s.B;
   s.Mm = s.B * s.Wcap;
