@@ -748,6 +748,7 @@ __device__ __forceinline__ AttnRow attn_row(const ECall& c, int i) {
 // each.  The waves' (max, sum,
 // numerator) are combined in LDS and the block writes one partial.  r0: the rows of
 // the block's first item (it = the block index), loaded once per launch.
+// Softmax exps are __expf (v_exp_f32 on x log2 e), as in the per-kernel attention.
 template <typename KV, int DH, class Late = NoHook>
 __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t base, uint32_t tag, int* err,
                                         float* lds, const AttnRow& r0, const VG& vg, Late&& late = Late()) {
@@ -843,13 +844,13 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
         mx = across_max<G>(mx);
         if (mx == -INFINITY) continue;  // wave-uniform
         const float m_new = fmaxf(m_run, mx);
-        const float alpha = (m_run == -INFINITY) ? 0.f : expf(m_run - m_new);
+        const float alpha = (m_run == -INFINITY) ? 0.f : __expf(m_run - m_new);
 #pragma unroll
         for (int v = 0; v < VEC; ++v) o[v] *= alpha;
         float ps = 0.f;
 #pragma unroll
         for (int r = 0; r < NR; ++r) {
-          const float p = (sc[r] == -INFINITY) ? 0.f : expf(sc[r] - m_new);
+          const float p = (sc[r] == -INFINITY) ? 0.f : __expf(sc[r] - m_new);
           ps += p;
           float fv[VEC];
           WT<KV>::unpack(vr[r], fv);
@@ -898,7 +899,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
         const float sc = vis ? dot : -INFINITY;
         const float mx = across_max<G>(sc);
         if (mx != -INFINITY) {  // wave-uniform
-          const float p = vis ? expf(sc - mx) : 0.f;
+          const float p = vis ? __expf(sc - mx) : 0.f;
 #pragma unroll
           for (int v = 0; v < VEC; ++v) o[v] = p * vrow[v];
           l_run = p;
@@ -928,7 +929,7 @@ __device__ __forceinline__ void op_attn(const EAttn& a, const ECall& c, uint32_t
 #pragma unroll
       for (int w = 0; w < EW; ++w) {
         if (wm[w] != -INFINITY) {
-          const float e = expf(wm[w] - mb);
+          const float e = __expf(wm[w] - mb);
           num += e * wo[w * DH + tid];
           den += e * wl[w];
         }
@@ -968,7 +969,7 @@ __device__ __forceinline__ void op_merge(const EMerge& g, const ECall& c, uint32
       }
     }
     const float mg = wave_max(ms);
-    const float w = (lane < S && ms != -INFINITY) ? expf(ms - mg) : 0.f;
+    const float w = (lane < S && ms != -INFINITY) ? __expf(ms - mg) : 0.f;
     const float den = wave_sum(w * ds);
     float num = 0.f;
     for (int s0 = 0; s0 < S; s0 += 8) {
