@@ -2152,14 +2152,19 @@ hipError_t gemv_launch(const Linear& L, hipStream_t st, const Ev& ev) {
   return gemv_launch_r<W, KC, R>(L, st, ev);
 }
 
-// Linears of more rows than this use the matrix cores (bfloat16 weights).
-constexpr int kMfmaMinRows = 16;
+// Linears of more rows than this use the matrix cores (bfloat16 weights).  With
+// K >= kMfmaWideK, from three rows on: the GEMV re-reads all M input rows in every wave
+// (M x K x 4 bytes from L2 per R weight rows), which at K = 2048 / 8192 (R = 4 / 1)
+// costs more than the tiled kernel's split-K round trip (d=2048 self-verification,
+// passes of 3..16 rows: 9.7k -> 10.7k accepted B/s).
+constexpr int kMfmaMinRows = 16, kMfmaMinRowsWideK = 2, kMfmaWideK = 2048;
 // split K until about this many blocks stream the weights (two 55 KiB blocks fit a CU)
 constexpr int kMfmaTargetBlocks = 512;
 
 template <typename W>
 bool mfma_fits(const Linear& L) {
-  return std::is_same<W, uint16_t>::value && L.M > kMfmaMinRows && L.N % 64 == 0 && L.K % kMfmaBK == 0;
+  return std::is_same<W, uint16_t>::value && L.M > (L.K >= kMfmaWideK ? kMfmaMinRowsWideK : kMfmaMinRows) &&
+         L.N % 64 == 0 && L.K % kMfmaBK == 0;
 }
 
 // The row kernel: 17..64 rows, K a whole number of eight 32/64/128-column slices, no
