@@ -47,6 +47,7 @@ class Stats:
         self.exempt = 0
         self.max_err = 0.0
         self.accepted = 0
+        self.timing = None  # kernel classes of the decode steps (forced_run with timing=True)
 
     def __repr__(self):
         return f"Stats(steps={self.steps}, exempt={self.exempt}, max_err={self.max_err:.3g}, accepted={self.accepted})"
@@ -78,11 +79,14 @@ def new_decoder(model, W, batch, max_ctx, max_n=8, **kw):
     return Decoder(make_config(model, max_batch=batch, max_ctx=max_ctx, max_n=max_n, **kw), W)
 
 
-def forced_run(dec, W, model, prompts, steps, n, tau, mode=THRESHOLD, tol=None, label=""):
+def forced_run(dec, W, model, prompts, steps, n, tau, mode=THRESHOLD, tol=None, label="", timing=False):
     """Teacher-forced comparison over ``steps`` steps; returns Stats.  ``n`` is the
-    candidate count of every step, or a list cycled over the steps."""
+    candidate count of every step, or a list cycled over the steps.  ``timing``: count
+    the kernel launches of the compared steps (not the prefill) into Stats.timing."""
     tol = base_tol(model) if tol is None else tol
     dec.prefill(prompts)
+    if timing:
+        dec.set_timing(True)
     xs = [[int(b) for b in p] for p in prompts]
     st = Stats()
     ns = list(n) if isinstance(n, (list, tuple)) else [n]
@@ -103,6 +107,9 @@ def forced_run(dec, W, model, prompts, steps, n, tau, mode=THRESHOLD, tol=None, 
             st.accepted += len(a)
         st.steps += 1
     st.seqs = xs  # the committed byte sequences the run ended on
+    if timing:
+        st.timing = dec.read_timing()
+        dec.set_timing(False)
     return st
 
 

@@ -95,8 +95,11 @@ def test_d2048_verify():
     prompts = [synth.make_prompt(20, 150), synth.make_prompt(21, 90)]
     dec = new_decoder(D2048, raw, 2, 400)
     st = forced_run(dec, W, D2048, prompts, 4, 7, 0.0, mode=SELF_VERIFY, tol=base_tol(D2048) * GAIN,
-                    label="d2048 verify")
-    print(st)
+                    label="d2048 verify", timing=True)
+    print(st, st.timing)
+    # the verification passes (up to 2 x 8 rows, K = 2048) ran on the matrix-core GEMM,
+    # which takes linears with K >= 2048 from three rows on
+    assert st.timing["gemm"][0] > 0, st.timing
     got_v, _ = free_run(dec, prompts, 24, 7, 0.0, mode=SELF_VERIFY)
     got_g, _ = free_run(dec, prompts, 24, 1, 0.0)
     for b in range(2):
