@@ -4,9 +4,9 @@
 // in float32, bfloat16 or float16; every activation, residual stream, norm, softmax
 // and accumulation is float32 (on the matrix cores, activations enter as bfloat16 or
 // float16 hi + lo pairs).  Linear layers:
-// - weight-streaming GEMV kernels for up to 16 rows of bfloat16 weights (64 of
-//   float32): each weight byte is read from HBM once per launch with 16-byte loads,
-//   issued before the activations are loaded;
+// - weight-streaming GEMV kernels for up to 16 rows of bfloat16 weights (up to 2 when
+//   K >= 2048; 64 of float32): each weight byte is read from HBM once per launch with
+//   16-byte loads, issued before the activations are loaded;
 // - for more rows of bfloat16 weights, the row GEMM (17..64 rows) and MFMA tiles of
 //   64 x 64 (split-K), 128 x 128 and 256 x 256.
 // Decode attention splits the keys over blocks and merges the splits in a second
